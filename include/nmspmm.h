@@ -1,0 +1,217 @@
+/*
+ * nmspmm.h -- C ABI of libnmspmm: N:M sparse INT8 GEMM for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The operation (paper: "Realizable N:M Sparse Transformer Inference via
+ * Search-Kernel Co-Design"; N:M sparsity Sec. 2.1, MD-SpMM Sec. 4):
+ *
+ *     Y[i][j] = sum_t X[i][t] * W[j][t]          (exact, int32)
+ *     Yh[i][j] = fp16( fp32(Y[i][j]) * scale[j] ) (optional dequantisation)
+ *
+ * X is int8 [m x k] row-major (m tokens, k = in_features), W is int8 [n x k]
+ * row-major (n = out_features, the layout of a PyTorch Linear weight) with at
+ * most N nonzeros in every aligned window of M consecutive entries along k.
+ * Y is int32 [m x n] row-major, Yh binary16 [m x n] row-major.
+ *
+ * Conventions for every entry point:
+ *   - Every buffer is owned by the caller.  The library never allocates device
+ *     memory and never frees anything it is given.
+ *   - "host" pointers are ordinary CPU memory; "device" pointers are GPU
+ *     memory of the current HIP device (hipMalloc or a PyTorch CUDA tensor).
+ *   - Device pointers must be 16-byte aligned.
+ *   - GEMM entry points are asynchronous: they enqueue kernels on `stream`
+ *     (a hipStream_t; NULL means the default stream) and return.  A status of
+ *     NM_OK means the arguments were valid and the launch was accepted; faults
+ *     inside a kernel surface at the next synchronising HIP call.
+ *   - On any error status nothing has been written to any caller buffer
+ *     (except the diagnostic fields of an nm_desc).
+ *   - The library has no global mutable state besides a thread-safe cache of
+ *     per-device properties.
+ */
+#ifndef NMSPMM_H
+#define NMSPMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum nm_status {
+    NM_OK = 0,
+    NM_ERR_ARG = 1,          /* null pointer, misaligned pointer, bad plan, negative size */
+    NM_ERR_SHAPE = 2,        /* k % M != 0, k % 16 != 0, n % 4 != 0, size too large */
+    NM_ERR_PATTERN = 3,      /* a window of W holds more than N nonzeros */
+    NM_ERR_UNSUPPORTED = 4,  /* (N, M) outside {1..4}:4 and {1..8}:8 */
+    NM_ERR_WORKSPACE = 5,    /* workspace missing or smaller than required */
+    NM_ERR_HIP = 6           /* a HIP call (launch, device query) failed */
+} nm_status;
+
+/* Output selection bits (used by the planners and workspace queries). */
+#define NM_OUT_I32 1
+#define NM_OUT_F16 2
+
+/* Physical layout of the packed weight produced by nm_compress. */
+#define NM_LAYOUT_SP42 1
+
+/*
+ * Descriptor of a packed weight.  Filled by nm_compress / nm_compress_size and
+ * treated as read-only afterwards.
+ *
+ * Layout NM_LAYOUT_SP42 ("4:2 streams"):  the paper's packed form B_pack keeps
+ * each window's nonzero values together with their positions inside the
+ * window (Sec. 4.2).  Here every window is cut into aligned 4-wide groups and
+ * each group is stored as `streams` pairs of (value, 2-bit position): the form
+ * the gfx950 structured-sparse matrix instruction consumes directly, so the
+ * kernels need no decode step.  Patterns with at most 2 nonzeros in any
+ * 4-group (1:4, 2:4, 1:8, 2:8) use one stream; the others (3:4, 4:4, 3:8 ..
+ * 8:8) use two.  Inside a group the slots hold the group's nonzeros by
+ * ascending position, then zero-valued padding at the smallest unused
+ * positions; the slot positions are distinct and ascending.
+ *
+ * With F = ceil(n / 16) row fragments and S = ceil(k / 128) k-steps, the packed
+ * weight is a sequence of F * S * streams blocks, block b = (f * S + s) *
+ * streams + q.  Block b holds
+ *     vals[b * 1024 + 16 * L + 2 * g + t]   (int8)
+ *     meta[b * 256 + 4 * L .. + 3]          (uint32, little endian)
+ * for lane L in 0..63, group g in 0..7 and slot t in 0..1 of stream q:
+ *     row     = 16 * f + (L % 16)
+ *     group   = the 4 entries of W[row] starting at k0 = 128 * s + 32 * (L / 16) + 4 * g
+ *     vals[...] = value of slot (2 * q + t) of that group
+ *     bits [4 * g + 2 * t + 1 : 4 * g + 2 * t] of the meta word = its position (0..3)
+ * Rows >= n and columns >= k are zero padding.
+ *   vals_bytes = F * S * streams * 1024,  meta_bytes = F * S * streams * 256.
+ */
+typedef struct nm_desc {
+    int32_t n, k;          /* logical W shape [n x k] */
+    int32_t nm_n, nm_m;    /* pattern: at most nm_n nonzeros per aligned window of nm_m */
+    int32_t streams;       /* 4:2 streams per 4-group: 1 or 2 */
+    int32_t layout;        /* NM_LAYOUT_SP42 */
+    int32_t n_frags;       /* ceil(n / 16) */
+    int32_t k_steps;       /* ceil(k / 128) */
+    int64_t vals_bytes;    /* bytes of the packed values */
+    int64_t meta_bytes;    /* bytes of the packed positions */
+    int32_t bad_row;       /* first offending row when NM_ERR_PATTERN, else -1 */
+    int32_t bad_group;     /* its window index (k / nm_m units), else -1 */
+} nm_desc;
+
+/*
+ * Launch plan of a GEMM (paper Sec. 4.3, adaptive parallelism): a workgroup
+ * tile of tile_n output channels x tile_m tokens, and split_k partitions of
+ * the reduction axis whose partial sums are merged at the end.  Plans come
+ * from the planners below; callers may also build one from nm_tile_info to
+ * force a schedule.  Every valid plan gives bit-identical results.
+ */
+typedef struct nm_plan {
+    int32_t kind;      /* NM_KIND_* */
+    int32_t tile;      /* index into the tile table, 0 .. nm_num_tiles()-1 */
+    int32_t tile_n;    /* output channels per workgroup (filled by the library) */
+    int32_t tile_m;    /* tokens per workgroup (filled by the library) */
+    int32_t split_k;   /* 1, 2, 4 or 8 */
+    int32_t grid;      /* workgroups launched (filled by the library) */
+} nm_plan;
+
+#define NM_KIND_SP42 1     /* structured-sparse MFMA, one 4:2 stream */
+#define NM_KIND_SP42X2 2   /* structured-sparse MFMA, two 4:2 streams */
+#define NM_KIND_DENSE 3    /* dense MFMA on a plain row-major W */
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *nm_status_string(nm_status s);
+
+/* ---------------------------------------------------------------- packing
+ * Offline packing of W into B_pack (Sec. 4.1-4.2; done once before
+ * deployment, Sec. 6.1).  Host memory only, synchronous, thread-safe. */
+
+/* Fills desc (shape, streams, sizes) for W [n x k] with pattern nm_n:nm_m
+ * without reading any weight.  Errors: NM_ERR_ARG (desc NULL, n or k < 1),
+ * NM_ERR_UNSUPPORTED, NM_ERR_SHAPE. */
+nm_status nm_compress_size(int n, int k, int nm_n, int nm_m, nm_desc *desc);
+
+/* Packs host W [n x k] (row-major int8) into host buffers vals
+ * (desc->vals_bytes) and meta (desc->meta_bytes), and fills desc.
+ * Errors: as nm_compress_size, plus NM_ERR_ARG for NULL W/vals/meta and
+ * NM_ERR_PATTERN (desc->bad_row / bad_group name the first offending window
+ * in row-major order; vals and meta are untouched). */
+nm_status nm_compress(const int8_t *W, int n, int k, int nm_n, int nm_m,
+                      int8_t *vals, uint8_t *meta, nm_desc *desc);
+
+/* Inverse of nm_compress: writes host W [n x k].  Errors: NM_ERR_ARG for NULL
+ * pointers, an inconsistent desc, or packed data that is not in canonical
+ * form (two slots of a group at one position holding a nonzero, a nonzero in
+ * the padding rows/columns, more nonzeros in a window than nm_n). */
+nm_status nm_decompress(const nm_desc *desc, const int8_t *vals, const uint8_t *meta, int8_t *W);
+
+/* ---------------------------------------------------------------- planning */
+
+/* Number of workgroup tiles the kernels are built for, and their sizes. */
+int nm_num_tiles(void);
+nm_status nm_tile_info(int tile, int *tile_n, int *tile_m);
+
+/* Planner for nm_spmm (Sec. 4.3): picks tile and split_k from
+ * (m, n, k, pattern) so that small-token shapes still occupy every compute
+ * unit, with split_k from {1, 2, 4, 8}, k-splits on 128-wide k-step
+ * boundaries and at least two k-steps per split.  Needs no GPU: without one
+ * it assumes 256 compute units.  out_mode is a mask of NM_OUT_* bits. */
+nm_status nm_spmm_plan(const nm_desc *desc, int m, int out_mode, nm_plan *plan);
+
+/* Same for the dense baseline GEMM of shape (m, n, k). */
+nm_status nm_gemm_i8_dense_plan(int m, int n, int k, int out_mode, nm_plan *plan);
+
+/* Device workspace needed by a plan for an [m x n] output: 0 when
+ * split_k == 1, else a 16384-byte block of per-tile counters followed by
+ * split_k partial int32 [m x n] tiles.  A split-K plan may cover at most 4096
+ * output tiles.  Errors: NM_ERR_ARG (bad plan or NULL bytes). */
+nm_status nm_workspace_size(const nm_plan *plan, int m, int n, size_t *bytes);
+
+/* Zero-fills a workspace on `stream` with a kernel (no memset node, so it
+ * may be captured in a HIP graph).  The counter block of a workspace must be
+ * zero before its first use; every GEMM call leaves it at zero again, for any
+ * plan, so one initialisation per buffer suffices.  Calls that share a
+ * workspace must be ordered on one stream (concurrent calls would race on it). */
+nm_status nm_workspace_init(void *ws, size_t bytes, void *stream);
+
+/* ---------------------------------------------------------------- GEMMs */
+
+/* Sparse GEMM on a packed weight (Sec. 4.2-4.3): Y = X W^T and/or
+ * Yh = fp16(fp32(Y) * scale[j]).
+ *   X      device int8 [m x k], row-major (k = desc->k)
+ *   vals   device copy of nm_compress's vals (desc->vals_bytes)
+ *   meta   device copy of nm_compress's meta (desc->meta_bytes)
+ *   desc   host descriptor from nm_compress
+ *   Y      device int32 [m x n] or NULL
+ *   scale  device float32 [n], required when Yh != NULL, else ignored
+ *   Yh     device binary16 bits [m x n] or NULL (Y and Yh may not both be NULL)
+ *   ws     device workspace of ws_bytes (nm_workspace_size of the plan;
+ *          may be NULL when the plan needs none)
+ *   stream hipStream_t or NULL
+ * m == 0 is a valid no-op (no pointer is examined, nothing is launched).  Errors: NM_ERR_ARG, NM_ERR_SHAPE (m < 0 or an
+ * output larger than 2^31 - 1 elements per row block), NM_ERR_WORKSPACE,
+ * NM_ERR_HIP. */
+nm_status nm_spmm(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
+                  const nm_desc *desc, int32_t *Y, const float *scale, uint16_t *Yh,
+                  void *ws, size_t ws_bytes, void *stream);
+
+/* nm_spmm with an explicit plan (NULL = the planner's); the plan's kind must
+ * match the descriptor (NM_KIND_SP42 for one stream, NM_KIND_SP42X2 for two). */
+nm_status nm_spmm_ex(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
+                     const nm_desc *desc, int32_t *Y, const float *scale, uint16_t *Yh,
+                     void *ws, size_t ws_bytes, void *stream, const nm_plan *plan);
+
+/* Dense INT8 GEMM baseline on the same shapes (the paper compares against a
+ * vendor dense GEMM, Sec. 6.1): Y = X W^T with W device int8 [n x k] plain
+ * row-major, same outputs, workspace and error rules as nm_spmm; requires
+ * k % 16 == 0 and n % 4 == 0. */
+nm_status nm_gemm_i8_dense(const int8_t *X, int m, const int8_t *W, int n, int k,
+                           int32_t *Y, const float *scale, uint16_t *Yh,
+                           void *ws, size_t ws_bytes, void *stream);
+
+nm_status nm_gemm_i8_dense_ex(const int8_t *X, int m, const int8_t *W, int n, int k,
+                              int32_t *Y, const float *scale, uint16_t *Yh,
+                              void *ws, size_t ws_bytes, void *stream, const nm_plan *plan);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NMSPMM_H */

@@ -1,0 +1,154 @@
+// C ABI entry points: argument checks, planning and dispatch (host only).
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "nmspmm_internal.h"
+
+using namespace nmspmm;
+
+namespace {
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+int out_mode_of(const int32_t *Y, const uint16_t *Yh) {
+    return (Y ? NM_OUT_I32 : 0) | (Yh ? NM_OUT_F16 : 0);
+}
+
+nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint8_t *meta, int n, int k,
+                   int k_steps, int n_frags, int32_t *Y, const float *scale, uint16_t *Yh, void *ws,
+                   size_t ws_bytes, void *stream, const nm_plan *forced) {
+    if (m < 0) return NM_ERR_SHAPE;
+    if (m == 0) return NM_OK;  // nothing to compute; empty tensors may carry null pointers
+    if (!X || !A || (kind != NM_KIND_DENSE && !meta)) return NM_ERR_ARG;
+    if (!Y && !Yh) return NM_ERR_ARG;
+    if (Yh && !scale) return NM_ERR_ARG;
+    if (!aligned16(X) || !aligned16(A) || (meta && !aligned16(meta)) || (Y && !aligned16(Y)) ||
+        (Yh && !aligned16(Yh)) || (Yh && !aligned16(scale)))
+        return NM_ERR_ARG;
+    if ((int64_t)m * n > ((int64_t)1 << 40)) return NM_ERR_SHAPE;
+    nm_plan plan;
+    if (forced) {
+        plan = *forced;
+        nm_status st = complete_plan(kind, m, n, k_steps, &plan);
+        if (st != NM_OK) return st;
+    } else {
+        nm_status st = make_plan(kind, m, n, k_steps, out_mode_of(Y, Yh), &plan);
+        if (st != NM_OK) return st;
+    }
+    const int tiles = plan.grid / plan.split_k;
+    const size_t need = workspace_bytes(plan.split_k, tiles, m, n);
+    if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return NM_ERR_WORKSPACE;
+
+    GemmArgs a;
+    a.X = X;
+    a.A = A;
+    a.meta = meta;
+    a.Y = Y;
+    a.Yh = Yh;
+    a.scale = scale;
+    a.counters = need ? (int32_t *)ws : nullptr;
+    a.partials = need ? (int32_t *)((char *)ws + kCounterBytes) : nullptr;
+    a.m = m;
+    a.n = n;
+    a.k = k;
+    a.k_steps = k_steps;
+    a.n_frags = n_frags;
+    a.tiles_n = (n + plan.tile_n - 1) / plan.tile_n;
+    a.tiles_m = (m + plan.tile_m - 1) / plan.tile_m;
+    a.split_k = plan.split_k;
+    int err = launch_gemm(kind, plan.tile, a, plan.grid, stream);
+    return err == 0 ? NM_OK : NM_ERR_HIP;
+}
+
+nm_status check_desc(const nm_desc *d) {
+    if (!d || d->layout != NM_LAYOUT_SP42) return NM_ERR_ARG;
+    nm_desc chk;
+    if (nm_compress_size(d->n, d->k, d->nm_n, d->nm_m, &chk) != NM_OK) return NM_ERR_ARG;
+    if (chk.streams != d->streams || chk.n_frags != d->n_frags || chk.k_steps != d->k_steps) return NM_ERR_ARG;
+    return NM_OK;
+}
+
+int kind_of(const nm_desc *d) { return d->streams == 1 ? NM_KIND_SP42 : NM_KIND_SP42X2; }
+
+}  // namespace
+
+extern "C" const char *nm_status_string(nm_status s) {
+    switch (s) {
+        case NM_OK: return "ok";
+        case NM_ERR_ARG: return "invalid argument";
+        case NM_ERR_SHAPE: return "unsupported shape";
+        case NM_ERR_PATTERN: return "weight violates the N:M pattern";
+        case NM_ERR_UNSUPPORTED: return "unsupported N:M pattern";
+        case NM_ERR_WORKSPACE: return "workspace missing or too small";
+        case NM_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+extern "C" int nm_num_tiles(void) { return kNumTiles; }
+
+extern "C" nm_status nm_tile_info(int tile, int *tile_n, int *tile_m) {
+    if (tile < 0 || tile >= kNumTiles || !tile_n || !tile_m) return NM_ERR_ARG;
+    *tile_n = kTiles[tile].tile_n();
+    *tile_m = kTiles[tile].tile_m();
+    return NM_OK;
+}
+
+extern "C" nm_status nm_spmm_plan(const nm_desc *desc, int m, int out_mode, nm_plan *plan) {
+    nm_status st = check_desc(desc);
+    if (st != NM_OK) return st;
+    return make_plan(kind_of(desc), m, desc->n, desc->k_steps, out_mode, plan);
+}
+
+extern "C" nm_status nm_gemm_i8_dense_plan(int m, int n, int k, int out_mode, nm_plan *plan) {
+    if (n < 1 || k < 1) return NM_ERR_ARG;
+    if (k % 16 != 0 || n % 4 != 0) return NM_ERR_SHAPE;
+    return make_plan(NM_KIND_DENSE, m, n, (k + kKStep - 1) / kKStep, out_mode, plan);
+}
+
+extern "C" nm_status nm_workspace_size(const nm_plan *plan, int m, int n, size_t *bytes) {
+    if (!plan || !bytes || m < 0 || n < 1 || plan->split_k < 1 || plan->tile < 0 || plan->tile >= kNumTiles)
+        return NM_ERR_ARG;
+    const int tn = kTiles[plan->tile].tile_n(), tm = kTiles[plan->tile].tile_m();
+    const int64_t tiles = (int64_t)((n + tn - 1) / tn) * (((m > 0 ? m : 1) + tm - 1) / tm);
+    *bytes = workspace_bytes(plan->split_k, (int)tiles, m, n);
+    return NM_OK;
+}
+
+extern "C" nm_status nm_workspace_init(void *ws, size_t bytes, void *stream) {
+    if (bytes == 0) return NM_OK;
+    if (!ws || !aligned16(ws)) return NM_ERR_ARG;
+    return launch_zero(ws, bytes, stream) == 0 ? NM_OK : NM_ERR_HIP;
+}
+
+extern "C" nm_status nm_spmm_ex(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
+                                const nm_desc *desc, int32_t *Y, const float *scale, uint16_t *Yh,
+                                void *ws, size_t ws_bytes, void *stream, const nm_plan *plan) {
+    nm_status st = check_desc(desc);
+    if (st != NM_OK) return st;
+    return run_gemm(kind_of(desc), X, m, vals, meta, desc->n, desc->k, desc->k_steps, desc->n_frags, Y, scale,
+                    Yh, ws, ws_bytes, stream, plan);
+}
+
+extern "C" nm_status nm_spmm(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
+                             const nm_desc *desc, int32_t *Y, const float *scale, uint16_t *Yh,
+                             void *ws, size_t ws_bytes, void *stream) {
+    return nm_spmm_ex(X, m, vals, meta, desc, Y, scale, Yh, ws, ws_bytes, stream, nullptr);
+}
+
+extern "C" nm_status nm_gemm_i8_dense_ex(const int8_t *X, int m, const int8_t *W, int n, int k,
+                                         int32_t *Y, const float *scale, uint16_t *Yh,
+                                         void *ws, size_t ws_bytes, void *stream, const nm_plan *plan) {
+    if (n < 1 || k < 1) return NM_ERR_ARG;
+    if (k % 16 != 0 || n % 4 != 0) return NM_ERR_SHAPE;
+    const int k_steps = (k + kKStep - 1) / kKStep;
+    return run_gemm(NM_KIND_DENSE, X, m, W, nullptr, n, k, k_steps, (n + kFragRows - 1) / kFragRows, Y, scale,
+                    Yh, ws, ws_bytes, stream, plan);
+}
+
+extern "C" nm_status nm_gemm_i8_dense(const int8_t *X, int m, const int8_t *W, int n, int k,
+                                      int32_t *Y, const float *scale, uint16_t *Yh,
+                                      void *ws, size_t ws_bytes, void *stream) {
+    return nm_gemm_i8_dense_ex(X, m, W, n, k, Y, scale, Yh, ws, ws_bytes, stream, nullptr);
+}

@@ -1,0 +1,279 @@
+"""Thin ctypes binding of libnmspmm (C ABI in include/nmspmm.h).
+
+Names follow the C entry points.  This module only marshals arguments: every
+step of the GEMM runs in the library's HIP kernels.  PyTorch supplies device
+memory and the current HIP stream; NumPy arrays carry host data for packing.
+There is no fallback: if the library is missing, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+import threading
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libnmspmm.so")
+
+NM_OK, NM_ERR_ARG, NM_ERR_SHAPE, NM_ERR_PATTERN, NM_ERR_UNSUPPORTED, NM_ERR_WORKSPACE, NM_ERR_HIP = range(7)
+NM_OUT_I32, NM_OUT_F16 = 1, 2
+NM_KIND_SP42, NM_KIND_SP42X2, NM_KIND_DENSE = 1, 2, 3
+NM_LAYOUT_SP42 = 1
+
+# Every symbol the header declares (checked by the CPU tests).
+EXPORTED = (
+    "nm_status_string", "nm_compress_size", "nm_compress", "nm_decompress", "nm_num_tiles",
+    "nm_tile_info", "nm_spmm_plan", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
+    "nm_spmm", "nm_spmm_ex", "nm_gemm_i8_dense", "nm_gemm_i8_dense_ex",
+)
+
+
+class NmDesc(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("k", ctypes.c_int32), ("nm_n", ctypes.c_int32), ("nm_m", ctypes.c_int32),
+                ("streams", ctypes.c_int32), ("layout", ctypes.c_int32), ("n_frags", ctypes.c_int32),
+                ("k_steps", ctypes.c_int32), ("vals_bytes", ctypes.c_int64), ("meta_bytes", ctypes.c_int64),
+                ("bad_row", ctypes.c_int32), ("bad_group", ctypes.c_int32)]
+
+
+class NmPlan(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("tile", ctypes.c_int32), ("tile_n", ctypes.c_int32),
+                ("tile_m", ctypes.c_int32), ("split_k", ctypes.c_int32), ("grid", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+class NmError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library.  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_12505_amd/build.py")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+        pd, pp = ctypes.POINTER(NmDesc), ctypes.POINTER(NmPlan)
+        sig = {
+            "nm_status_string": ([i32], ctypes.c_char_p),
+            "nm_compress_size": ([i32, i32, i32, i32, pd], i32),
+            "nm_compress": ([vp, i32, i32, i32, i32, vp, vp, pd], i32),
+            "nm_decompress": ([pd, vp, vp, vp], i32),
+            "nm_num_tiles": ([], i32),
+            "nm_tile_info": ([i32, ctypes.POINTER(i32), ctypes.POINTER(i32)], i32),
+            "nm_spmm_plan": ([pd, i32, i32, pp], i32),
+            "nm_gemm_i8_dense_plan": ([i32, i32, i32, i32, pp], i32),
+            "nm_workspace_size": ([pp, i32, i32, ctypes.POINTER(sz)], i32),
+            "nm_workspace_init": ([vp, sz, vp], i32),
+            "nm_spmm": ([vp, i32, vp, vp, pd, vp, vp, vp, vp, sz, vp], i32),
+            "nm_spmm_ex": ([vp, i32, vp, vp, pd, vp, vp, vp, vp, sz, vp, pp], i32),
+            "nm_gemm_i8_dense": ([vp, i32, vp, i32, i32, vp, vp, vp, vp, sz, vp], i32),
+            "nm_gemm_i8_dense_ex": ([vp, i32, vp, i32, i32, vp, vp, vp, vp, sz, vp, pp], i32),
+        }
+        for name, (args, res) in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+        return L
+
+
+def status_string(status: int) -> str:
+    return lib().nm_status_string(int(status)).decode()
+
+
+def _check(status: int, what: str):
+    if status != NM_OK:
+        raise NmError(status, what)
+
+
+# ---------------------------------------------------------------- packing (host)
+
+@dataclasses.dataclass
+class Packed:
+    """Host result of nm_compress: packed values, packed positions, descriptor."""
+    vals: np.ndarray
+    meta: np.ndarray
+    desc: NmDesc
+
+
+def compress_size(n: int, k: int, N: int, M: int) -> NmDesc:
+    d = NmDesc()
+    _check(lib().nm_compress_size(n, k, N, M, ctypes.byref(d)), "nm_compress_size")
+    return d
+
+
+def compress(W: np.ndarray, N: int, M: int) -> Packed:
+    W = np.ascontiguousarray(W)
+    if W.dtype != np.int8 or W.ndim != 2:
+        raise TypeError("W must be a 2-D int8 array")
+    n, k = W.shape
+    d = NmDesc()
+    st = lib().nm_compress_size(n, k, N, M, ctypes.byref(d))
+    if st != NM_OK:
+        raise NmError(st, "nm_compress")
+    vals = np.empty(d.vals_bytes, np.int8)
+    meta = np.empty(d.meta_bytes, np.uint8)
+    st = lib().nm_compress(W.ctypes.data, n, k, N, M, vals.ctypes.data, meta.ctypes.data, ctypes.byref(d))
+    if st != NM_OK:
+        err = NmError(st, "nm_compress")
+        err.bad_row, err.bad_group = d.bad_row, d.bad_group
+        raise err
+    return Packed(vals, meta, d)
+
+
+def decompress(p: Packed) -> np.ndarray:
+    W = np.empty((p.desc.n, p.desc.k), np.int8)
+    vals = np.ascontiguousarray(p.vals)
+    meta = np.ascontiguousarray(p.meta)
+    _check(lib().nm_decompress(ctypes.byref(p.desc), vals.ctypes.data, meta.ctypes.data, W.ctypes.data),
+           "nm_decompress")
+    return W
+
+
+# ---------------------------------------------------------------- planning
+
+def num_tiles() -> int:
+    return lib().nm_num_tiles()
+
+
+def tile_info(tile: int):
+    a, b = ctypes.c_int(), ctypes.c_int()
+    _check(lib().nm_tile_info(tile, ctypes.byref(a), ctypes.byref(b)), "nm_tile_info")
+    return a.value, b.value
+
+
+def spmm_plan(desc: NmDesc, m: int, out_mode: int = NM_OUT_I32) -> NmPlan:
+    p = NmPlan()
+    _check(lib().nm_spmm_plan(ctypes.byref(desc), m, out_mode, ctypes.byref(p)), "nm_spmm_plan")
+    return p
+
+
+def dense_plan(m: int, n: int, k: int, out_mode: int = NM_OUT_I32) -> NmPlan:
+    p = NmPlan()
+    _check(lib().nm_gemm_i8_dense_plan(m, n, k, out_mode, ctypes.byref(p)), "nm_gemm_i8_dense_plan")
+    return p
+
+
+def make_plan(kind: int, tile: int, split_k: int) -> NmPlan:
+    p = NmPlan()
+    p.kind, p.tile, p.split_k = kind, tile, split_k
+    return p
+
+
+def workspace_size(plan: NmPlan, m: int, n: int) -> int:
+    b = ctypes.c_size_t()
+    _check(lib().nm_workspace_size(ctypes.byref(plan), m, n, ctypes.byref(b)), "nm_workspace_size")
+    return b.value
+
+
+# ---------------------------------------------------------------- device side (torch for memory/streams)
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+class Workspace:
+    """A zero-initialised device buffer that grows on demand (one per device).
+
+    The library keeps its counters at zero after every call, so the buffer is
+    initialised once, when it is (re)allocated."""
+
+    def __init__(self):
+        self._bufs = {}
+
+    def get(self, nbytes: int, device):
+        torch = _torch()
+        if nbytes == 0:
+            return None, 0
+        key = torch.device(device).index or 0
+        buf = self._bufs.get(key)
+        if buf is None or buf.numel() < nbytes:
+            buf = torch.zeros(max(nbytes, 1 << 20), dtype=torch.uint8, device=device)
+            self._bufs[key] = buf
+        return buf, buf.numel()
+
+
+_WS = Workspace()
+
+
+@dataclasses.dataclass
+class DeviceWeight:
+    """A packed weight resident on the GPU (values, positions, host descriptor)."""
+    vals: object
+    meta: object
+    desc: NmDesc
+
+    @classmethod
+    def from_packed(cls, p: Packed, device="cuda"):
+        torch = _torch()
+        v = torch.from_numpy(p.vals).to(device)
+        m = torch.from_numpy(p.meta).to(device)
+        return cls(v, m, p.desc)
+
+
+def spmm(X, w: DeviceWeight, Y=None, scale=None, Yh=None, plan: Optional[NmPlan] = None, ws=None,
+         stream=None):
+    """nm_spmm / nm_spmm_ex on torch device tensors.  Y (int32) and Yh (float16 or
+    int16 view of binary16) are written in place; returns (Y, Yh)."""
+    m = X.shape[0]
+    out_mode = (NM_OUT_I32 if Y is not None else 0) | (NM_OUT_F16 if Yh is not None else 0)
+    p = plan if plan is not None else spmm_plan(w.desc, m, out_mode or NM_OUT_I32)
+    need = workspace_size(p, m, w.desc.n)
+    if ws is None:
+        ws, ws_bytes = _WS.get(need, X.device)
+    else:
+        ws_bytes = ws.numel() * ws.element_size()
+    st = lib().nm_spmm_ex(_ptr(X), m, _ptr(w.vals), _ptr(w.meta), ctypes.byref(w.desc), _ptr(Y), _ptr(scale),
+                          _ptr(Yh), _ptr(ws), ws_bytes, _stream(stream),
+                          ctypes.byref(plan) if plan is not None else None)
+    _check(st, "nm_spmm")
+    return Y, Yh
+
+
+def gemm_i8_dense(X, W, Y=None, scale=None, Yh=None, plan: Optional[NmPlan] = None, ws=None, stream=None):
+    """nm_gemm_i8_dense / nm_gemm_i8_dense_ex on torch device tensors."""
+    m, k = X.shape
+    n = W.shape[0]
+    out_mode = (NM_OUT_I32 if Y is not None else 0) | (NM_OUT_F16 if Yh is not None else 0)
+    p = plan if plan is not None else dense_plan(m, n, k, out_mode or NM_OUT_I32)
+    need = workspace_size(p, m, n)
+    if ws is None:
+        ws, ws_bytes = _WS.get(need, X.device)
+    else:
+        ws_bytes = ws.numel() * ws.element_size()
+    st = lib().nm_gemm_i8_dense_ex(_ptr(X), m, _ptr(W), n, k, _ptr(Y), _ptr(scale), _ptr(Yh), _ptr(ws), ws_bytes,
+                                   _stream(stream), ctypes.byref(plan) if plan is not None else None)
+    _check(st, "nm_gemm_i8_dense")
+    return Y, Yh
+
+
+def workspace_init(ws, stream=None):
+    _check(lib().nm_workspace_init(_ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
+           "nm_workspace_init")

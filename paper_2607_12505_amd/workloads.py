@@ -32,7 +32,7 @@ def rng_for(cfg: int, layer: int, linear: int, pattern: int, role: int) -> np.ra
 
 
 def gen_x(m: int, k: int, rng: np.random.Generator) -> np.ndarray:
-    return rng.integers(-127, 128, size=(m, k), dtype=np.int64).astype(np.int8)
+    return rng.integers(-127, 128, size=(m, k), dtype=np.int8)
 
 
 def gen_w(n: int, k: int, N: int, M: int, rng: np.random.Generator) -> Tuple[np.ndarray, np.ndarray]:
@@ -161,13 +161,10 @@ def random_nm(n: int, k: int, N: int, M: int, rng: np.random.Generator, full: bo
     """Random int8 matrix with 0..N nonzeros (exactly N if full) per aligned window,
     values drawn from the whole int8 range (edge values -128/127 included)."""
     G = k // M
-    W = np.zeros((n, G, M), np.int8)
-    for j in range(n):
-        for g in range(G):
-            c = N if full else int(rng.integers(0, N + 1))
-            pos = rng.choice(M, size=c, replace=False)
-            lo = -128 if extremes else -127
-            v = rng.integers(lo, 128, size=c)
-            v[v == 0] = 1
-            W[j, g, pos] = v
-    return W.reshape(n, k)
+    cnt = np.full((n, G), N) if full else rng.integers(0, N + 1, size=(n, G))
+    # a uniformly random subset of cnt positions per window: ranks of random keys
+    rank = np.argsort(np.argsort(rng.random((n, G, M)), axis=2), axis=2)
+    lo = -128 if extremes else -127
+    v = rng.integers(lo, 128, size=(n, G, M))
+    v[v == 0] = 1
+    return np.where(rank < cnt[..., None], v, 0).astype(np.int8).reshape(n, k)

@@ -1,0 +1,124 @@
+"""Host packing (nm_compress / nm_decompress) against the N:M rule, the
+documented physical layout and the oracle's canonical packed form (CPU only)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_12505_amd import nmspmm
+from paper_2607_12505_amd import workloads as wl
+
+PATTERNS = [(1, 4), (2, 4), (3, 4), (4, 4), (1, 8), (2, 8), (3, 8), (4, 8), (6, 8), (8, 8)]
+
+
+def decode_documented(vals, meta, d):
+    """Reads the packed buffers exactly as the header documents them and
+    returns the slot lists per (row, 4-group): (values, positions)."""
+    F, S, Q = d.n_frags, d.k_steps, d.streams
+    v = vals.reshape(F, S, Q, 4, 16, 8, 2)            # f, s, q, L/16, L%16, g, t
+    w = meta.view(np.uint32).reshape(F, S, Q, 4, 16)  # f, s, q, L/16, L%16
+    pos = (w[..., None, None] >> (4 * np.arange(8)[:, None] + 2 * np.arange(2)[None, :])) & 3
+    # -> rows (f, L%16), groups (s, L/16, g), slots (q, t)
+    v = v.transpose(0, 4, 1, 3, 5, 2, 6).reshape(F * 16, S * 32, 2 * Q)
+    p = pos.transpose(0, 4, 1, 3, 5, 2, 6).reshape(F * 16, S * 32, 2 * Q)
+    return v, p
+
+
+@pytest.mark.parametrize("N,M", PATTERNS)
+def test_roundtrip(N, M):
+    rng = np.random.default_rng(N * 10 + M)
+    for (n, k) in ((16, 128), (36, 192), (20, 4 * M * 3 + 16 * M)):
+        if k % M or k % 16:
+            continue
+        W = wl.random_nm(n, k, N, M, rng)
+        p = nmspmm.compress(W, N, M)
+        assert p.desc.n == n and p.desc.k == k and p.desc.streams == (1 if N <= 2 else 2)
+        assert np.array_equal(nmspmm.decompress(p), W)
+        # canonical idempotence
+        p2 = nmspmm.compress(nmspmm.decompress(p), N, M)
+        assert np.array_equal(p2.vals, p.vals) and np.array_equal(p2.meta, p.meta)
+
+
+@pytest.mark.parametrize("N,M", PATTERNS)
+def test_layout_matches_header_and_oracle(N, M):
+    rng = np.random.default_rng(7 + N * 10 + M)
+    n, k = 40, 320
+    W = wl.random_nm(n, k, N, M, rng, full=True)
+    p = nmspmm.compress(W, N, M)
+    v, pos = decode_documented(p.vals, p.meta, p.desc)
+    Q = p.desc.streams
+    # rebuild W from the documented formula
+    Wr = np.zeros((v.shape[0], v.shape[1] * 4), np.int8)
+    for t in range(2 * Q):
+        cols = 4 * np.arange(v.shape[1])[None, :] + pos[:, :, t]
+        np.put_along_axis(Wr, cols, v[:, :, t], axis=1)
+    assert np.array_equal(Wr[:n, :k], W)
+    assert not Wr[n:].any() and not Wr[:, k:].any()
+    # slot positions ascending and distinct inside every group
+    assert (np.diff(pos.astype(int), axis=2) > 0).all()
+    # every 4-group's slots are the oracle's canonical packing of that group
+    G4 = W.reshape(n, k // 4, 4)
+    ov, oo = oracle.pack_logical(G4.reshape(n * k // 4, 4), min(2 * Q, 4), 4)
+    assert np.array_equal(v[:n, : k // 4].reshape(-1, 2 * Q), ov.reshape(-1, 2 * Q))
+    assert np.array_equal(pos[:n, : k // 4].reshape(-1, 2 * Q), oo.reshape(-1, 2 * Q))
+
+
+def test_sizes():
+    d = nmspmm.compress_size(768, 192, 2, 4)
+    assert (d.n_frags, d.k_steps, d.streams) == (48, 2, 1)
+    assert d.vals_bytes == 48 * 2 * 1024 and d.meta_bytes == 48 * 2 * 256
+    d = nmspmm.compress_size(100, 384, 4, 8)
+    assert (d.n_frags, d.k_steps, d.streams) == (7, 3, 2)
+
+
+def test_error_codes():
+    W = np.zeros((16, 128), np.int8)
+    with pytest.raises(nmspmm.NmError) as e:
+        nmspmm.compress(W, 2, 5)
+    assert e.value.status == nmspmm.NM_ERR_UNSUPPORTED
+    with pytest.raises(nmspmm.NmError) as e:
+        nmspmm.compress(W, 0, 4)
+    assert e.value.status == nmspmm.NM_ERR_UNSUPPORTED
+    with pytest.raises(nmspmm.NmError) as e:
+        nmspmm.compress(np.zeros((16, 132), np.int8), 2, 8)   # k % M
+    assert e.value.status == nmspmm.NM_ERR_SHAPE
+    with pytest.raises(nmspmm.NmError) as e:
+        nmspmm.compress(np.zeros((16, 136), np.int8), 2, 4)   # k % 16
+    assert e.value.status == nmspmm.NM_ERR_SHAPE
+    with pytest.raises(nmspmm.NmError) as e:
+        nmspmm.compress(np.zeros((18, 128), np.int8), 2, 4)   # n % 4
+    assert e.value.status == nmspmm.NM_ERR_SHAPE
+    bad = np.zeros((16, 128), np.int8)
+    bad[5, 8:11] = 1                                          # 3 nonzeros in window 2
+    with pytest.raises(nmspmm.NmError) as e:
+        nmspmm.compress(bad, 2, 4)
+    assert e.value.status == nmspmm.NM_ERR_PATTERN
+    assert (e.value.bad_row, e.value.bad_group) == (5, 2)
+
+
+def test_decompress_rejects_non_canonical():
+    W = wl.random_nm(16, 128, 2, 4, np.random.default_rng(1), full=True)
+    p = nmspmm.compress(W, 2, 4)
+    meta = p.meta.copy()
+    word = meta[:4].view(np.uint32)
+    # point slot 1 of group 0 at the position of slot 0 (both values nonzero)
+    first = int(word[0]) & 3
+    word[0] = (int(word[0]) & ~0xC) | (first << 2)
+    with pytest.raises(nmspmm.NmError):
+        nmspmm.decompress(nmspmm.Packed(p.vals, meta, p.desc))
+    # a nonzero in the padding rows (n is 16 here, so use a 20-row weight)
+    W2 = wl.random_nm(20, 128, 2, 4, np.random.default_rng(2), full=True)
+    p2 = nmspmm.compress(W2, 2, 4)
+    v2 = p2.vals.copy()
+    v2[1024 * 1 + 16 * 10] = 5   # block of fragment 1, lane 10 -> row 26 >= 20
+    with pytest.raises(nmspmm.NmError):
+        nmspmm.decompress(nmspmm.Packed(v2, p2.meta, p2.desc))
+
+
+def test_generated_config_weights_roundtrip():
+    for cfg in (0, 1, 2):
+        for g in wl.workload(cfg).gemms[:4]:
+            if g.m > 2000:
+                continue
+            _, W, _ = wl.inputs_for(cfg, g)
+            p = nmspmm.compress(W, g.N, g.M)
+            assert np.array_equal(nmspmm.decompress(p), W)

@@ -1,0 +1,246 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+INT32 outputs must be bit-exact; fp16 outputs within |g - r| <= 1e-3 |r| or
+2^-24 (one fp16 subnormal step); every output element is prefilled with a
+sentinel and followed by a guard band, so unwritten elements and overruns are
+caught.  Small cases are compared element by element over every pattern, tile
+and split-K; the benchmark workloads are run at full size in the planner's
+launch configuration and compared at sampled positions.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_12505_amd import nmspmm
+from paper_2607_12505_amd import workloads as wl
+import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+ALL_PATTERNS = [(1, 4), (2, 4), (3, 4), (4, 4), (1, 8), (2, 8), (3, 8), (4, 8), (5, 8), (8, 8)]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    torch = gu.torch()
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    nmspmm.lib()  # fails loudly when the HIP library is missing
+    yield
+    torch.cuda.synchronize()
+
+
+def _case(m, n, k, N, M, seed):
+    rng = np.random.default_rng(seed)
+    X = rng.integers(-128, 128, (m, k)).astype(np.int8)   # the library accepts -128 too
+    W = wl.random_nm(n, k, N, M, rng, full=bool(seed % 2))
+    scale = rng.uniform(1e-6, 1e-3, n).astype(np.float32)
+    return X, W, scale
+
+
+# ---------------------------------------------------------------- small, full comparison
+
+@pytest.mark.parametrize("N,M", ALL_PATTERNS)
+@pytest.mark.parametrize("m,n,k", [(1, 16, 128), (17, 36, 64), (197, 768, 192), (130, 260, 384), (64, 132, 1024)])
+def test_sparse_matches_oracle(N, M, m, n, k):
+    if k % M:
+        pytest.skip("k not a multiple of M")
+    print(f"sparse {N}:{M} m={m} n={n} k={k}", flush=True)
+    X, W, scale = _case(m, n, k, N, M, seed=m * 7 + n * 3 + k + N * 10 + M)
+    packed = nmspmm.compress(W, N, M)
+    Y, Yh = gu.run_sparse(X, packed, scale, want_i32=True, want_f16=True)
+    ref = oracle.matmul_i8(X, W)
+    assert np.array_equal(Y, ref)
+    gu.assert_f16_close(Yh, oracle.dequant_f16(ref, scale))
+
+
+@pytest.mark.parametrize("m,n,k", [(1, 16, 128), (17, 36, 64), (197, 768, 192), (130, 260, 384), (300, 64, 2048)])
+def test_dense_matches_oracle(m, n, k):
+    print(f"dense m={m} n={n} k={k}", flush=True)
+    rng = np.random.default_rng(m + n + k)
+    X = rng.integers(-128, 128, (m, k)).astype(np.int8)
+    W = rng.integers(-128, 128, (n, k)).astype(np.int8)
+    scale = rng.uniform(1e-6, 1e-3, n).astype(np.float32)
+    Y, Yh = gu.run_dense(X, W, scale, want_i32=True, want_f16=True)
+    ref = oracle.matmul_i8(X, W)
+    assert np.array_equal(Y, ref)
+    gu.assert_f16_close(Yh, oracle.dequant_f16(ref, scale))
+
+
+def test_output_modes_independent():
+    X, W, scale = _case(100, 128, 256, 2, 4, seed=5)
+    packed = nmspmm.compress(W, 2, 4)
+    ref = oracle.matmul_i8(X, W)
+    Y, Yh = gu.run_sparse(X, packed, scale, want_i32=True, want_f16=False)
+    assert Yh is None and np.array_equal(Y, ref)
+    Y, Yh = gu.run_sparse(X, packed, scale, want_i32=False, want_f16=True)
+    assert Y is None
+    gu.assert_f16_close(Yh, oracle.dequant_f16(ref, scale))
+
+
+def test_extreme_values_and_fp16_overflow():
+    # all -128 x -128 products: Y = 16384 k, the largest magnitude int8 allows;
+    # a large scale pushes Yh beyond 65504 -> +inf must match exactly
+    m, n, k = 48, 64, 512
+    X = np.full((m, k), -128, np.int8)
+    W = np.zeros((n, k), np.int8)
+    W.reshape(n, k // 4, 4)[:, :, 1:3] = -128
+    scale = np.full(n, 1.0, np.float32)
+    scale[::3] = 1e-5
+    packed = nmspmm.compress(W, 2, 4)
+    Y, Yh = gu.run_sparse(X, packed, scale, want_i32=True, want_f16=True)
+    ref = oracle.matmul_i8(X, W)
+    assert np.array_equal(Y, ref) and ref.max() == 128 * 128 * k // 2
+    gu.assert_f16_close(Yh, oracle.dequant_f16(ref, scale))
+    assert np.isinf(Yh.view(np.float16)).any()
+
+
+# ---------------------------------------------------------------- schedule invariance
+
+@pytest.mark.parametrize("kind", [nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_SP42X2, nmspmm.NM_KIND_DENSE])
+def test_every_tile_and_split_is_bit_identical(kind):
+    # spans several tiles of every size plus ragged tails in m and n
+    m, n, k = 333, 404, 1024
+    N, M = {nmspmm.NM_KIND_SP42: (2, 8), nmspmm.NM_KIND_SP42X2: (4, 8), nmspmm.NM_KIND_DENSE: (8, 8)}[kind]
+    X, W, scale = _case(m, n, k, N, M, seed=kind)
+    ref = oracle.matmul_i8(X, W)
+    ref_h = oracle.dequant_f16(ref, scale)
+    packed = nmspmm.compress(W, N, M)
+    dw = nmspmm.DeviceWeight.from_packed(packed)
+    for tile in range(nmspmm.num_tiles()):
+        for split in (1, 2, 4, 8):
+            print(f"kind {kind} tile {tile} split {split}", flush=True)
+            plan = nmspmm.make_plan(kind, tile, split)
+            if kind == nmspmm.NM_KIND_DENSE:
+                Y, Yh = gu.run_dense(X, W, scale, True, True, plan=plan)
+            else:
+                Y, Yh = gu.run_sparse(X, packed, scale, True, True, plan=plan, dw=dw)
+            assert np.array_equal(Y, ref), (tile, split)
+            gu.assert_f16_close(Yh, ref_h)
+
+
+def test_repeated_split_k_runs_are_identical():
+    # split-K merges through counters in a reused workspace; repeat to catch races
+    torch = gu.torch()
+    m, n, k = 197, 768, 3072
+    X, W, scale = _case(m, n, k, 2, 4, seed=77)
+    ref = oracle.matmul_i8(X, W)
+    packed = nmspmm.compress(W, 2, 4)
+    dw = nmspmm.DeviceWeight.from_packed(packed)
+    plan = nmspmm.spmm_plan(packed.desc, m, nmspmm.NM_OUT_I32)
+    assert plan.split_k > 1
+    Xd = torch.from_numpy(X).cuda()
+    outs = [torch.empty((m, n), dtype=torch.int32, device="cuda") for _ in range(30)]
+    for Y in outs:
+        nmspmm.spmm(Xd, dw, Y=Y)
+    torch.cuda.synchronize()
+    for Y in outs:
+        assert np.array_equal(Y.cpu().numpy(), ref)
+
+
+def test_workspace_shared_by_plans_of_growing_size():
+    # one workspace reused by split-K calls whose tile counts grow: the counters
+    # of a later call must not land on partial sums of an earlier one
+    torch = gu.torch()
+    ws = torch.zeros(64 << 20, dtype=torch.uint8, device="cuda")
+    for (m, n, k) in ((64, 64, 512), (197, 768, 768), (197, 2304, 768), (100, 512, 1024), (197, 3072, 768)):
+        X, W, _ = _case(m, n, k, 2, 4, seed=m + n + k)
+        packed = nmspmm.compress(W, 2, 4)
+        dw = nmspmm.DeviceWeight.from_packed(packed)
+        plan = nmspmm.make_plan(nmspmm.NM_KIND_SP42, 5, 2)
+        Y = torch.full((m, n), -1, dtype=torch.int32, device="cuda")
+        nmspmm.spmm(torch.from_numpy(X).cuda(), dw, Y=Y, plan=plan, ws=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(Y.cpu().numpy(), oracle.matmul_i8(X, W)), (m, n, k)
+
+
+# ---------------------------------------------------------------- edge cases and errors
+
+def test_zero_tokens_is_a_noop():
+    torch = gu.torch()
+    packed = nmspmm.compress(np.zeros((16, 128), np.int8), 2, 4)
+    dw = nmspmm.DeviceWeight.from_packed(packed)
+    X = torch.zeros((0, 128), dtype=torch.int8, device="cuda")
+    Y = torch.zeros((0, 16), dtype=torch.int32, device="cuda")
+    nmspmm.spmm(X, dw, Y=Y)
+    torch.cuda.synchronize()
+
+
+def test_host_side_errors_write_nothing():
+    torch = gu.torch()
+    X, W, scale = _case(64, 64, 256, 2, 4, seed=3)
+    packed = nmspmm.compress(W, 2, 4)
+    dw = nmspmm.DeviceWeight.from_packed(packed)
+    Xd = torch.from_numpy(X).cuda()
+    Y = torch.full((64, 64), 7, dtype=torch.int32, device="cuda")
+    with pytest.raises(nmspmm.NmError) as e:          # no output at all
+        nmspmm.spmm(Xd, dw)
+    assert e.value.status == nmspmm.NM_ERR_ARG
+    Yh = torch.zeros((64, 64), dtype=torch.int16, device="cuda")
+    with pytest.raises(nmspmm.NmError):               # fp16 output without scale
+        nmspmm.spmm(Xd, dw, Yh=Yh)
+    raw = torch.zeros(64 * 256 + 1, dtype=torch.int8, device="cuda")
+    with pytest.raises(nmspmm.NmError):               # misaligned X
+        nmspmm.spmm(raw[1:].view(64, 256), dw, Y=Y)
+    plan = nmspmm.make_plan(nmspmm.NM_KIND_SP42, 5, 2)
+    small = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(nmspmm.NmError) as e:          # workspace too small
+        nmspmm.spmm(Xd, dw, Y=Y, plan=plan, ws=small)
+    assert e.value.status == nmspmm.NM_ERR_WORKSPACE
+    with pytest.raises(nmspmm.NmError):               # plan kind does not match the weight
+        nmspmm.spmm(Xd, dw, Y=Y, plan=nmspmm.make_plan(nmspmm.NM_KIND_DENSE, 0, 1))
+    torch.cuda.synchronize()
+    assert (Y.cpu().numpy() == 7).all()
+
+
+def test_workspace_init_clears():
+    torch = gu.torch()
+    ws = torch.full((4096 + 3,), 9, dtype=torch.uint8, device="cuda")
+    nmspmm.workspace_init(ws)
+    torch.cuda.synchronize()
+    assert not ws.cpu().numpy().any()
+
+
+# ---------------------------------------------------------------- benchmark workloads at full size
+
+def _run_workload_gemm(cfg, g, rng, x_cache):
+    X, W, scale = wl.inputs_for(cfg, g, x_cache)
+    out = wl.workload(cfg)
+    want_f16 = out.out_f16
+    print(f"cfg{cfg} {g.name} m={g.m} k={g.k} n={g.n}", flush=True)
+    if g.N == g.M and out.chain:
+        Y, Yh = gu.run_dense(X, W, scale, True, want_f16)
+    else:
+        Y, Yh = gu.run_sparse(X, nmspmm.compress(W, g.N, g.M), scale, True, want_f16)
+    gu.check_sampled(X, W, Y, rng, scale=scale, Yh=Yh)
+
+
+def test_config0_full():
+    g = wl.workload(0).gemms[0]
+    X, W, scale = wl.inputs_for(0, g)
+    Y, Yh = gu.run_sparse(X, nmspmm.compress(W, g.N, g.M), scale, True, True)
+    ref = oracle.matmul_i8(X, W)
+    assert np.array_equal(Y, ref)
+    gu.assert_f16_close(Yh, oracle.dequant_f16(ref, scale))
+    Yd, _ = gu.run_dense(X, W, None, True, False)
+    assert np.array_equal(Yd, ref)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_config_sampled(cfg):
+    rng = np.random.default_rng(cfg)
+    cache = {}
+    for g in wl.workload(cfg).gemms:
+        _run_workload_gemm(cfg, g, rng, cache)
+
+
+def test_config4_distinct_shapes_sampled():
+    # the 96-linear chain has four shapes; check each (shape, pattern) pair once
+    rng = np.random.default_rng(4)
+    seen = set()
+    cache = {}
+    for g in wl.workload(4).gemms:
+        key = (g.k, g.n, g.N, g.M)
+        if key in seen:
+            continue
+        seen.add(key)
+        _run_workload_gemm(4, g, rng, cache)

@@ -1,0 +1,79 @@
+"""Adaptive-parallelism planner (paper Sec. 4.3) on the host (CPU only;
+without a GPU the library assumes 256 compute units)."""
+import itertools
+
+import pytest
+
+from paper_2607_12505_amd import nmspmm
+from paper_2607_12505_amd import workloads as wl
+
+CUS = 256
+
+
+def all_shapes():
+    seen = set()
+    for cfg in range(5):
+        for g in wl.workload(cfg).gemms:
+            key = (g.m, g.k, g.n, g.N, g.M)
+            if key not in seen:
+                seen.add(key)
+                yield key
+    for m, n, k in itertools.product((1, 17, 64, 197, 512), (128, 1024), (128, 1024)):
+        yield (m, k, n, 2, 4)
+
+
+@pytest.mark.parametrize("shape", list(all_shapes()))
+def test_plan_rules(shape):
+    m, k, n, N, M = shape
+    d = nmspmm.compress_size(n, k, N, M)
+    for out in (nmspmm.NM_OUT_I32, nmspmm.NM_OUT_F16, nmspmm.NM_OUT_I32 | nmspmm.NM_OUT_F16):
+        p = nmspmm.spmm_plan(d, m, out)
+        assert p.kind == (nmspmm.NM_KIND_SP42 if N <= 2 else nmspmm.NM_KIND_SP42X2)
+        assert p.split_k in (1, 2, 4, 8)
+        tn, tm = nmspmm.tile_info(p.tile)
+        tiles = -(-n // tn) * -(-m // tm)
+        assert p.grid == tiles * p.split_k
+        if p.split_k > 1:
+            # k-splits whole 128-wide k-steps, at least two per split
+            assert d.k_steps // p.split_k >= 2
+            # split-K is only used when no tile alone fills the compute units
+            for t in range(nmspmm.num_tiles()):
+                a, b = nmspmm.tile_info(t)
+                assert -(-n // a) * -(-m // b) < CUS
+            assert nmspmm.workspace_size(p, m, n) >= p.split_k * m * n * 4
+        else:
+            assert nmspmm.workspace_size(p, m, n) == 0
+        # deterministic
+        q = nmspmm.spmm_plan(d, m, out)
+        assert q.as_dict() == p.as_dict()
+        dp = nmspmm.dense_plan(m, n, k, out)
+        assert dp.kind == nmspmm.NM_KIND_DENSE and dp.tile == p.tile and dp.split_k == p.split_k
+
+
+def test_small_m_fills_the_gpu_when_possible():
+    # DeiT-Base fc1 at batch 1: 197 tokens x 3072 channels, k = 768 (6 k-steps)
+    d = nmspmm.compress_size(3072, 768, 2, 4)
+    p = nmspmm.spmm_plan(d, 197, nmspmm.NM_OUT_I32)
+    assert p.grid >= CUS
+    # fc2 at batch 1: 768 channels, k = 3072 (24 k-steps) needs split-K
+    d = nmspmm.compress_size(768, 3072, 2, 4)
+    p = nmspmm.spmm_plan(d, 197, nmspmm.NM_OUT_I32)
+    assert p.split_k > 1 and p.grid >= CUS
+
+
+def test_forced_plan_validation():
+    d = nmspmm.compress_size(256, 256, 2, 4)
+    ok = nmspmm.make_plan(nmspmm.NM_KIND_SP42, 0, 2)
+    assert nmspmm.workspace_size(ok, 100, 256) > 0
+    with pytest.raises(nmspmm.NmError):
+        nmspmm.workspace_size(nmspmm.make_plan(nmspmm.NM_KIND_SP42, 99, 1), 100, 256)
+    with pytest.raises(nmspmm.NmError):
+        nmspmm.spmm_plan(d, -1)
+
+
+def test_split_k_tile_limit():
+    # split-K plans keep one counter per output tile in a fixed 16 KB block
+    p = nmspmm.make_plan(nmspmm.NM_KIND_SP42, 5, 2)
+    assert nmspmm.workspace_size(p, 64 * 64, 64 * 64) == 16384 + 2 * 64 * 64 * 64 * 64 * 4
+    p1 = nmspmm.make_plan(nmspmm.NM_KIND_SP42, 5, 1)
+    assert nmspmm.workspace_size(p1, 64 * 64, 64 * 64) == 0
