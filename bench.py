@@ -111,8 +111,7 @@ class Prepared:
             self.sparse_fn = L.nm_gemm_i8_dense_ex
 
     def kernel_name(self, plan):
-        kind = {1: "sp42", 2: "sp42x2", 3: "dense"}[plan.kind]
-        return f"{kind}/t{plan.tile_n}x{plan.tile_m}"
+        return nmspmm.plan_kernel_name(plan)
 
     def run_sparse(self):
         st = self.sparse_fn(*self.sparse_args)
@@ -125,29 +124,60 @@ class Prepared:
             raise nmspmm.NmError(st, f"dense {self.g.name}")
 
 
-def time_steps(preps, steps, torch, sleep_cycles):
-    """Runs `steps` steps; returns per-launch times [steps, gemms, 2] in ms."""
+def launch_groups(preps):
+    """Timed launch groups of a step: the sparse-side launches of one kernel
+    instantiation, then likewise for the dense baseline.  Events bracket whole
+    groups of back-to-back launches, so no event sits between two kernels of
+    a group."""
+    groups = {}
+    for i, p in enumerate(preps):
+        groups.setdefault(("sparse", p.kernel_name(p.splan)), []).append(i)
+    for i, p in enumerate(preps):
+        groups.setdefault(("dense", p.kernel_name(p.dplan)), []).append(i)
+    return list(groups.items())
+
+
+def time_steps(preps, groups, steps, torch, sleep_cycles):
+    """Runs `steps` steps; returns group times [steps, groups] in ms."""
     E = torch.cuda.Event
-    ev = [[(E(enable_timing=True), E(enable_timing=True), E(enable_timing=True)) for _ in preps]
-          for _ in range(steps)]
+    ev = [[E(enable_timing=True) for _ in range(len(groups) + 1)] for _ in range(steps)]
     for s in range(steps):
         if sleep_cycles:
             torch.cuda._sleep(sleep_cycles)
-        for i, p in enumerate(preps):
-            e0, e1, e2 = ev[s][i]
-            e0.record()
-            p.run_sparse()
-            e1.record()
-            p.run_dense()
-            e2.record()
+        ev[s][0].record()
+        for gi, ((side, _), idx) in enumerate(groups):
+            for i in idx:
+                if side == "sparse":
+                    preps[i].run_sparse()
+                else:
+                    preps[i].run_dense()
+            ev[s][gi + 1].record()
     torch.cuda.synchronize()
-    t = np.zeros((steps, len(preps), 2))
+    t = np.zeros((steps, len(groups)))
     for s in range(steps):
-        for i in range(len(preps)):
-            e0, e1, e2 = ev[s][i]
-            t[s, i, 0] = e0.elapsed_time(e1)
-            t[s, i, 1] = e1.elapsed_time(e2)
+        for gi in range(len(groups)):
+            t[s, gi] = ev[s][gi].elapsed_time(ev[s][gi + 1])
     return t
+
+
+def time_each(preps, torch, reps=5):
+    """Untimed detail pass: mean time of each GEMM, sparse and dense, each
+    over `reps` back-to-back launches (for the per-GEMM table only)."""
+    E = torch.cuda.Event
+    out = np.zeros((len(preps), 2))
+    for i, p in enumerate(preps):
+        for side, fn in ((0, p.run_sparse), (1, p.run_dense)):
+            fn()
+            torch.cuda.synchronize()
+            torch.cuda._sleep(int(2.4e9 * 20e-6 * reps))
+            e0, e1 = E(enable_timing=True), E(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            out[i, side] = e0.elapsed_time(e1) / reps
+    return out
 
 
 def cpu_baseline(preps, budget_s, check):
@@ -183,6 +213,171 @@ def cpu_baseline(preps, budget_s, check):
     }, mism
 
 
+def sweep(configs, torch, reps, out_path):
+    """Planner evaluation in the manner of the paper's Table 1: for every
+    distinct (shape, N:M) of the workloads, time every (tile, split_k)
+    candidate; the fastest is the sweep optimum.  Reports the planner's Top-1
+    hit rate, its average and worst performance normalised to the optimum, and
+    the gain over a fixed split_k = 1 setting (same tile)."""
+    E = torch.cuda.Event
+    rows = []
+    seen = set()
+    for cfg in configs:
+        work = wl.workload(cfg)
+        out = (nmspmm.NM_OUT_I32 if work.out_int32 else 0) | (nmspmm.NM_OUT_F16 if work.out_f16 else 0)
+        for g in work.gemms:
+            key = (g.m, g.k, g.n, g.N, g.M, out)
+            if key in seen:
+                continue
+            seen.add(key)
+            X, W, scale = wl.inputs_for(cfg, g)
+            Xd = torch.from_numpy(X).cuda()
+            sd = torch.from_numpy(scale).cuda()
+            sparse = g.N < g.M
+            if sparse:
+                dw = nmspmm.DeviceWeight.from_packed(nmspmm.compress(W, g.N, g.M))
+                planned = nmspmm.spmm_plan(dw.desc, g.m, out)
+            else:
+                Wd = torch.from_numpy(W).cuda()
+                planned = nmspmm.dense_plan(g.m, g.n, g.k, out)
+            nsets = max(1, min(4, int(400e6 // (6 * g.m * g.n))))
+            Ys = [torch.empty((g.m, g.n), dtype=torch.int32, device="cuda") if out & 1 else None for _ in range(nsets)]
+            Yhs = [torch.empty((g.m, g.n), dtype=torch.int16, device="cuda") if out & 2 else None for _ in range(nsets)]
+            ws = torch.zeros(64 << 20, dtype=torch.uint8, device="cuda")
+            times = {}
+            for tile in range(nmspmm.num_tiles()):
+                tn_, tm_ = nmspmm.tile_info(tile)
+                tiles = -(-g.n // tn_) * -(-g.m // tm_)
+                for split in (1, 2, 4, 8):
+                    if split > 1 and tiles >= 256 and (tile, split) != (planned.tile, planned.split_k):
+                        continue  # split-K only where the tiles alone leave compute units idle
+                    plan = nmspmm.make_plan(planned.kind, tile, split)
+                    try:
+                        if nmspmm.workspace_size(plan, g.m, g.n) > ws.numel():
+                            continue
+                        def run(i, plan=plan):
+                            if sparse:
+                                nmspmm.spmm(Xd, dw, Y=Ys[i], scale=sd, Yh=Yhs[i], plan=plan, ws=ws)
+                            else:
+                                nmspmm.gemm_i8_dense(Xd, Wd, Y=Ys[i], scale=sd, Yh=Yhs[i], plan=plan, ws=ws)
+                        run(0)
+                    except nmspmm.NmError:
+                        continue
+                    torch.cuda.synchronize()
+                    torch.cuda._sleep(int(2.4e9 * 20e-6 * reps))
+                    e0, e1 = E(enable_timing=True), E(enable_timing=True)
+                    e0.record()
+                    for r in range(reps):
+                        run(r % nsets)
+                    e1.record()
+                    torch.cuda.synchronize()
+                    times[(tile, split)] = e0.elapsed_time(e1) / reps * 1e3
+            best = min(times, key=times.get)
+            chosen = (planned.tile, planned.split_k)
+            t_plan = times.get(chosen)
+            t_fixed = times.get((planned.tile, 1))
+            rows.append({
+                "cfg": cfg, "gemm": g.name, "m": g.m, "k": g.k, "n": g.n, "pattern": pattern_name(g),
+                "planned": list(chosen), "best": list(best), "t_planned_us": t_plan, "t_best_us": times[best],
+                "t_fixed_split1_us": t_fixed, "times": {f"{t}/{s}": v for (t, s), v in times.items()},
+            })
+            log(f"cfg{cfg} {g.name:<20} m={g.m:<6} k={g.k:<5} n={g.n:<5} planned t{chosen[0]}/s{chosen[1]} "
+                f"{t_plan:7.1f} us  best t{best[0]}/s{best[1]} {times[best]:7.1f} us  "
+                f"norm {times[best] / t_plan:.3f}")
+    norm = np.array([r["t_best_us"] / r["t_planned_us"] for r in rows])
+    fixed = np.array([r["t_fixed_split1_us"] / r["t_planned_us"] for r in rows if r["t_fixed_split1_us"]])
+    summary = {
+        "cases": len(rows),
+        "top1_hit_rate": round(float(np.mean([r["planned"] == r["best"] for r in rows])), 3),
+        "avg_norm_perf": round(float(norm.mean()), 3),
+        "worst_norm_perf": round(float(norm.min()), 3),
+        "gain_over_fixed_split1": round(float(fixed.mean()), 3),
+    }
+    log(json.dumps(summary))
+    if out_path:
+        with open(out_path, "w") as f:
+            json.dump({"summary": summary, "rows": rows}, f, indent=1)
+    return summary
+
+
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_12505_amd", "csrc", "nmspmm_kernels.hip")
+
+
+def kernel_source_sha256():
+    import hashlib
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def default_traffic_path(workload_name):
+    return os.path.join(ROOT, "profiles", f"traffic_{workload_name}.json")
+
+
+def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, commands, out_md):
+    """Summarises rocprofv3 CSV output of a bench run: per-kernel durations
+    from the kernel trace, and FETCH_SIZE / WRITE_SIZE per dispatch scaled by
+    what the same counters read for the calibration copy (copy_mib MiB read
+    and written).  Writes a markdown summary and the traffic record of the
+    dominant kernel next to it."""
+    import csv
+    import glob
+    line = json.loads(open(bench_json).read().strip().splitlines()[-1])
+    dom = line["roofline"]["kernel"]
+    work = line["config"]["workload"]
+    stats = list(csv.DictReader(open(glob.glob(os.path.join(trace_dir, "*_kernel_stats.csv"))[0])))
+    stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
+
+    def counters(d):
+        per = {}
+        for r in csv.DictReader(open(glob.glob(os.path.join(d, "*_counter_collection.csv"))[0])):
+            per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return per
+
+    fetch, write = counters(fetch_dir), counters(write_dir)
+    calib = [k for k in fetch if "neg_kernel" in k]
+    if len(calib) != 1:
+        raise SystemExit("calibration copy kernel not found in the counter output")
+    true_bytes = copy_mib * (1 << 20)
+    f_scale = true_bytes / (np.mean(fetch[calib[0]]) * 1024)
+    w_scale = true_bytes / (np.mean(write[calib[0]]) * 1024)
+
+    def find(per, name):
+        ks = [k for k in per if name in k]
+        return per[ks[0]] if ks else None
+
+    dom_fetch, dom_write = find(fetch, dom), find(write, dom)
+    bytes_per_launch = (np.mean(dom_fetch) * 1024 * f_scale + np.mean(dom_write) * 1024 * w_scale)
+    dom_stats = [r for r in stats if dom in r["Name"]][0]
+    md = [f"# rocprofv3 summary: `{dom}` on workload `{work}`", ""]
+    md += ["Commands (repository root as working directory of the bench; rocprofv3 run from /tmp):", "", "```"]
+    md += commands + ["```", ""]
+    md += [f"Dominant sparse kernel: `{dom}`: {dom_stats['Calls']} calls, average "
+           f"{float(dom_stats['AverageNs']) / 1e3:.2f} us (min {float(dom_stats['MinNs']) / 1e3:.2f}, "
+           f"max {float(dom_stats['MaxNs']) / 1e3:.2f}); bench.py HIP-event average over the timed region: "
+           f"{line['roofline']['avg_launch_us']:.2f} us.", ""]
+    md += ["| kernel | calls | avg us | total ms |", "|---|---:|---:|---:|"]
+    for r in stats[:14]:
+        md.append(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                  f"{float(r['TotalDurationNs']) / 1e6:.3f} |")
+    md += ["", "HBM traffic per dispatch (FETCH_SIZE and WRITE_SIZE, KiB, scaled by the calibration copy of "
+           f"{copy_mib} MiB read + {copy_mib} MiB written: fetch x{f_scale:.3f}, write x{w_scale:.3f}):", "",
+           "| kernel | dispatches | FETCH KiB | WRITE KiB | scaled MB |", "|---|---:|---:|---:|---:|"]
+    for k in sorted(set(fetch) & set(write), key=lambda k: -np.mean(write[k]))[:10]:
+        mb = (np.mean(fetch[k]) * 1024 * f_scale + np.mean(write[k]) * 1024 * w_scale) / 1e6
+        md.append(f"| `{k[:90]}` | {len(fetch[k])} | {np.mean(fetch[k]):.0f} | {np.mean(write[k]):.0f} | {mb:.2f} |")
+    alg = line["roofline"]["algorithmic_bytes_per_launch"]
+    md += ["", f"Dominant kernel: measured traffic {bytes_per_launch / 1e6:.2f} MB per launch vs "
+           f"{alg / 1e6:.2f} MB algorithmic ({bytes_per_launch / alg:.3f}x)."]
+    with open(out_md, "w") as f:
+        f.write("\n".join(md) + "\n")
+    rec = {"kernel": dom, "workload": work, "bytes_per_launch": int(bytes_per_launch),
+           "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
+           "kernel_source_sha256": kernel_source_sha256(), "summary": os.path.basename(out_md)}
+    with open(default_traffic_path(work), "w") as f:
+        json.dump(rec, f, indent=1)
+    print("\n".join(md))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -191,9 +386,26 @@ def main():
     ap.add_argument("--config", type=int, default=1, help="0..4 (default 1: DeiT-Small linears, batch 64)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="after timing, run one plain device copy of MIB MiB (profiler counter calibration)")
+    ap.add_argument("--sweep", type=str, default=None,
+                    help="planner evaluation over the given comma-separated configs (e.g. 0,1,2,3,4)")
+    ap.add_argument("--sweep-out", type=str, default=None, help="JSON file for the sweep results")
     ap.add_argument("--traffic", type=str, default=None,
-                    help="JSON file with measured HBM bytes per launch of the dominant kernel")
+                    help="JSON record of measured HBM bytes per launch of the dominant kernel "
+                         "(default: profiles/traffic_<workload>.json, used only if it matches this kernel source)")
+    ap.add_argument("--rocprof-summary", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"), default=None,
+                    help="summarise rocprofv3 CSV output of a bench run (no GPU needed)")
+    ap.add_argument("--bench-json", type=str, default=None, help="bench output line used by --rocprof-summary")
+    ap.add_argument("--summary-out", type=str, default=None, help="markdown file written by --rocprof-summary")
+    ap.add_argument("--commands", type=str, default=None, help="file with the profiling commands to quote")
     args = ap.parse_args()
+
+    if args.rocprof_summary:
+        cmds = open(args.commands).read().strip().splitlines() if args.commands else []
+        rocprof_summary(*args.rocprof_summary, args.bench_json, args.copy_calibration or 256, cmds,
+                        args.summary_out)
+        return
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the method is a "
@@ -206,6 +418,10 @@ def main():
         sys.exit(1)
     nmspmm.lib()
     torch.cuda.set_device(0)
+    if args.sweep:
+        summary = sweep([int(c) for c in args.sweep.split(",")], torch, 10, args.sweep_out)
+        print(json.dumps({"planner_evaluation": summary}), flush=True)
+        return
 
     work = wl.workload(args.config)
     out_i32, out_f16 = work.out_int32, work.out_f16
@@ -220,23 +436,26 @@ def main():
 
     # sleep long enough for the host to enqueue one step ahead of the GPU
     sleep_cycles = int(2.4e9 * 25e-6 * len(preps) * 2)
-    time_steps(preps, max(1, args.warmup), torch, sleep_cycles)
+    groups = launch_groups(preps)
+    time_steps(preps, groups, max(1, args.warmup), torch, sleep_cycles)
 
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    t = time_steps(preps, args.steps, torch, sleep_cycles)
+    t = time_steps(preps, groups, args.steps, torch, sleep_cycles)
     wall = time.perf_counter() - w0
     ms_per_step = wall * 1e3 / args.steps
+    tg = t.mean(axis=0)  # per group: mean over steps (the paper averages repeated runs, Sec. 5.1)
 
-    # per GEMM: mean over steps (the paper averages repeated runs, Sec. 5.1)
-    ts = t[:, :, 0].mean(axis=0)
-    td = t[:, :, 1].mean(axis=0)
     ops = np.array([p.g.dense_eq_ops for p in preps], np.float64)
-    sparse_sel = np.array([p.sparse_kernel for p in preps])
-    value = ops[sparse_sel].sum() / (ts[sparse_sel].sum() * 1e-3) / 1e12
-    dense_tops = ops.sum() / (td.sum() * 1e-3) / 1e12
-    speedup = td[sparse_sel].sum() / ts[sparse_sel].sum()
+    sparse_ms = sum(tg[gi] for gi, ((side, _), _) in enumerate(groups) if side == "sparse")
+    dense_ms = sum(tg[gi] for gi, ((side, _), _) in enumerate(groups) if side == "dense")
+    value = ops.sum() / (sparse_ms * 1e-3) / 1e12
+    dense_tops = ops.sum() / (dense_ms * 1e-3) / 1e12
+    speedup = dense_ms / sparse_ms
 
+    # per GEMM and per pattern (detail pass, outside the timed region)
+    each = time_each(preps, torch)
+    ts, td = each[:, 0], each[:, 1]
     per_pattern = {}
     for pat in sorted({pattern_name(p.g) for p in preps}):
         sel = np.array([pattern_name(p.g) == pat for p in preps])
@@ -245,27 +464,26 @@ def main():
             "speedup_vs_dense": round(float(td[sel].sum() / ts[sel].sum()), 3),
         }
 
-    # dominant kernel: the (kind, tile) instantiation with the most sparse time per step
-    groups = {}
-    for i, p in enumerate(preps):
-        if not p.sparse_kernel:
+    # dominant kernel: the sparse-side kernel instantiation with the most time per step
+    gsum = {}
+    for gi, ((side, name), idx) in enumerate(groups):
+        if side != "sparse":
             continue
-        name = p.kernel_name(p.splan)
-        gr = groups.setdefault(name, {"time_ms": 0.0, "bytes": 0, "ops": 0.0, "launches": 0, "split": set()})
-        gr["time_ms"] += ts[i]
-        gr["bytes"] += algorithmic_bytes(p.g, out_i32, out_f16)
-        gr["ops"] += ops[i]
-        gr["launches"] += 1
-        gr["split"].add(p.splan.split_k)
-    dom_name = max(groups, key=lambda k: groups[k]["time_ms"])
-    dom = groups[dom_name]
+        gsum[name] = {"time_ms": tg[gi], "launches": len(idx),
+                      "bytes": sum(algorithmic_bytes(preps[i].g, out_i32, out_f16, sparse=preps[i].sparse_kernel)
+                                   for i in idx)}
+    dom_name = max(gsum, key=lambda k: gsum[k]["time_ms"])
+    dom = gsum[dom_name]
     avg_ms = dom["time_ms"] / dom["launches"]
     achieved = dom["bytes"] / dom["launches"] / (avg_ms * 1e-3) / 1e9
     traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        with open(args.traffic) as f:
+    tpath = args.traffic or default_traffic_path(work.name)
+    if os.path.exists(tpath):
+        with open(tpath) as f:
             tr = json.load(f)
-        if tr.get("kernel") == dom_name and tr.get("workload") == work.name:
+        # counters taken on another kernel (or an older build of it) do not count
+        if (tr.get("kernel") == dom_name and tr.get("workload") == work.name
+                and tr.get("kernel_source_sha256") == kernel_source_sha256()):
             traffic = tr.get("bytes_per_launch")
     roofline = {
         "bound": "hbm",
@@ -280,12 +498,12 @@ def main():
         "algorithmic_bytes_per_launch": int(dom["bytes"] / dom["launches"]),
     }
 
-    log(f"\n{'gemm':<22}{'m':>7}{'k':>6}{'n':>6}  {'plan':<18}{'sparse us':>10}{'dense us':>10}"
+    log(f"\n{'gemm':<22}{'m':>7}{'k':>6}{'n':>6}  {'sparse kernel':<30}{'sparse us':>10}{'dense us':>10}"
         f"{'TOPS':>8}{'dTOPS':>8}{'spd':>7}{'GB/s':>8}")
     for i, p in enumerate(preps):
         g = p.g
         b = algorithmic_bytes(g, out_i32, out_f16, sparse=p.sparse_kernel)
-        log(f"{g.name:<22}{g.m:>7}{g.k:>6}{g.n:>6}  {p.kernel_name(p.splan) + '/s' + str(p.splan.split_k):<18}"
+        log(f"{g.name:<22}{g.m:>7}{g.k:>6}{g.n:>6}  {p.kernel_name(p.splan) + '/s' + str(p.splan.split_k):<30}"
             f"{ts[i] * 1e3:>10.1f}{td[i] * 1e3:>10.1f}{ops[i] / ts[i] / 1e9:>8.0f}{ops[i] / td[i] / 1e9:>8.0f}"
             f"{td[i] / ts[i]:>7.2f}{b / ts[i] / 1e6:>8.0f}")
     log(f"\nsparse {value:.1f} TOPS dense-eq, dense {dense_tops:.1f} TOPS, speedup {speedup:.3f}; "
@@ -315,10 +533,19 @@ def main():
         "dense_tops": round(float(dense_tops), 2),
         "frac_of_int8_peak": round(float(value / PEAK_INT8_TOPS), 4),
         "per_pattern": per_pattern,
-        "sparse_ms_per_step": round(float(ts[sparse_sel].sum()), 4),
-        "dense_ms_per_step": round(float(td.sum()), 4),
+        "sparse_ms_per_step": round(float(sparse_ms), 4),
+        "dense_ms_per_step": round(float(dense_ms), 4),
         "roofline": roofline,
     }
+    if args.copy_calibration:
+        # a plain elementwise pass that reads and writes exactly MIB MiB each
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        line["copy_calibration_bytes"] = 4 * n
     if not args.no_cpu_baseline:
         cb, mism = cpu_baseline(preps, args.cpu_budget, check=True)
         line["cpu_baseline"] = cb

@@ -158,10 +158,16 @@ nm_status nm_spmm_plan(const nm_desc *desc, int m, int out_mode, nm_plan *plan);
 /* Same for the dense baseline GEMM of shape (m, n, k). */
 nm_status nm_gemm_i8_dense_plan(int m, int n, int k, int out_mode, nm_plan *plan);
 
+/* Writes into buf (NUL-terminated, at most len bytes) the name of the kernel
+ * template instance a plan launches, e.g. "k_gemm<1, 2, 2, 4, 4, 3>", as it
+ * appears in profiler traces.  For profiling tools; needs no GPU.
+ * Errors: NM_ERR_ARG (bad plan, NULL buf, len too small). */
+nm_status nm_plan_kernel_name(const nm_plan *plan, char *buf, int len);
+
 /* Device workspace needed by a plan for an [m x n] output: 0 when
  * split_k == 1, else a 16384-byte block of per-tile counters followed by
  * split_k partial int32 [m x n] tiles.  A split-K plan may cover at most 4096
- * output tiles.  Errors: NM_ERR_ARG (bad plan or NULL bytes). */
+ * output tiles and its partial tiles must total less than 2 GiB.  Errors: NM_ERR_ARG (bad plan or NULL bytes). */
 nm_status nm_workspace_size(const nm_plan *plan, int m, int n, size_t *bytes);
 
 /* Zero-fills a workspace on `stream` with a kernel (no memset node, so it

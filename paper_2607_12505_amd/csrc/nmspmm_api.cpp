@@ -2,6 +2,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <cstdio>
 
 #include "nmspmm_internal.h"
 
@@ -93,6 +94,20 @@ extern "C" nm_status nm_tile_info(int tile, int *tile_n, int *tile_m) {
     *tile_n = kTiles[tile].tile_n();
     *tile_m = kTiles[tile].tile_m();
     return NM_OK;
+}
+
+extern "C" nm_status nm_plan_kernel_name(const nm_plan *plan, char *buf, int len) {
+    if (!plan || !buf || len <= 0 || plan->tile < 0 || plan->tile >= kNumTiles) return NM_ERR_ARG;
+    if (plan->kind != NM_KIND_SP42 && plan->kind != NM_KIND_SP42X2 && plan->kind != NM_KIND_DENSE) return NM_ERR_ARG;
+    const TileCfg &t = kTiles[plan->tile];
+    int w;
+    if (t.layout == kKSliced)
+        w = std::snprintf(buf, (size_t)len, "k_gemm_ks<%d, %d, %d, %d>", plan->kind, t.fn, t.fm, t.nst);
+    else if (t.layout == kRowStat)
+        w = std::snprintf(buf, (size_t)len, "k_gemm_rs<%d, %d, %d, %d>", plan->kind, t.fn, t.fm, t.nst);
+    else
+        w = std::snprintf(buf, (size_t)len, "k_gemm<%d, %d, %d, %d, %d, %d>", plan->kind, t.wn, t.wm, t.fn, t.fm, t.nst);
+    return (w > 0 && w < len) ? NM_OK : NM_ERR_ARG;
 }
 
 extern "C" nm_status nm_spmm_plan(const nm_desc *desc, int m, int out_mode, nm_plan *plan) {

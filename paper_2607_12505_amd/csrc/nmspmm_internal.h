@@ -4,6 +4,8 @@
 #include <cstddef>
 #include <cstdint>
 
+#include <hip/hip_runtime.h>
+
 #include "../../include/nmspmm.h"
 
 namespace nmspmm {
@@ -15,24 +17,62 @@ constexpr int kVBlock = 1024;    // packed value bytes per (fragment, k-step, st
 constexpr int kMBlock = 256;     // packed position bytes per (fragment, k-step, stream)
 constexpr int kThreads = 256;    // threads per workgroup (4 waves of 64)
 
-// Workgroup tile: WN x WM waves, each owning FN x FM fragments of 16 x 16
-// outputs.  tile_n = WN * FN * 16 channels, tile_m = WM * FM * 16 tokens.
+// Kernel layouts of a workgroup tile.
+//   kOutSplit:  WN x WM waves, each owning FN x FM fragments of 16 x 16
+//               outputs (tile_n = WN * FN * 16 channels, tile_m = WM * FM * 16
+//               tokens); one output tile per workgroup.
+//   kKSliced:   every wave computes the whole FN x FM-fragment tile over a
+//               quarter of the k-steps (wn = wm = 1); one tile per workgroup.
+//   kRowStat:   2 x 2 consumer waves as kOutSplit plus one producer wave; the
+//               workgroup keeps a token block of X in LDS and walks a range of
+//               output tiles (row-stationary), so the grid is a fixed number
+//               of workgroups.
+// nst = depth of the ring of k-step slots staged in LDS.
+enum Layout { kOutSplit = 0, kKSliced = 1, kRowStat = 2 };
+
 struct TileCfg {
-    int wn, wm, fn, fm;
+    int wn, wm, fn, fm, nst, layout;
     constexpr int tile_n() const { return wn * fn * kFragRows; }
     constexpr int tile_m() const { return wm * fm * 16; }
 };
 
 // Tiles the kernels are instantiated for, from the largest to the smallest.
 constexpr TileCfg kTiles[] = {
-    {2, 2, 4, 4},  // 0: 128 ch x 128 tok
-    {4, 1, 4, 4},  // 1: 256 ch x  64 tok
-    {1, 4, 4, 4},  // 2:  64 ch x 256 tok
-    {2, 2, 4, 2},  // 3: 128 ch x  64 tok
-    {2, 2, 2, 4},  // 4:  64 ch x 128 tok
-    {2, 2, 2, 2},  // 5:  64 ch x  64 tok
+    {2, 2, 8, 8, 2, kOutSplit},  // 0: 256 ch x 256 tok
+    {2, 2, 8, 4, 3, kOutSplit},  // 1: 256 ch x 128 tok
+    {2, 2, 4, 4, 3, kOutSplit},  // 2: 128 ch x 128 tok
+    {4, 1, 4, 4, 3, kOutSplit},  // 3: 256 ch x  64 tok
+    {2, 2, 4, 2, 4, kOutSplit},  // 4: 128 ch x  64 tok
+    {2, 2, 2, 4, 4, kOutSplit},  // 5:  64 ch x 128 tok
+    {2, 2, 2, 2, 4, kOutSplit},  // 6:  64 ch x  64 tok
+    {1, 1, 4, 4, 3, kKSliced},   // 7:  64 ch x  64 tok, k-sliced over the waves
+    {1, 1, 2, 4, 3, kKSliced},   // 8:  32 ch x  64 tok, k-sliced
+    {1, 1, 4, 2, 3, kKSliced},   // 9:  64 ch x  32 tok, k-sliced
+    {1, 1, 2, 2, 3, kKSliced},   // 10: 32 ch x  32 tok, k-sliced
+    {2, 2, 4, 4, 3, kRowStat},   // 11: 128 ch x 128 tok, row-stationary
+    {2, 2, 4, 2, 3, kRowStat},   // 12: 128 ch x  64 tok, row-stationary
+    {2, 2, 8, 2, 3, kRowStat},   // 13: 256 ch x  64 tok, row-stationary
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
+
+// LDS of a row-stationary workgroup: the resident X block (every k-step of
+// tile_m tokens), the weight ring, and per-wave epilogue staging.
+struct RowStatLds {
+    size_t xblock, wslot, ring, staging, total;
+};
+inline RowStatLds rowstat_lds(int kind, const TileCfg &t, int k_steps) {
+    const bool sparse = kind != NM_KIND_DENSE;
+    const int S = kind == NM_KIND_SP42X2 ? 2 : 1;
+    const int BN = t.tile_n(), BM = t.tile_m();
+    RowStatLds L;
+    L.xblock = (size_t)k_steps * BM * 128;
+    L.wslot = sparse ? (size_t)(BN / 16) * S * (kVBlock + kMBlock) : (size_t)BN * 128;
+    L.ring = (size_t)t.nst * L.wslot;
+    L.staging = (size_t)4 * 16 * (t.fn * 64 + 16);
+    L.total = L.xblock + L.ring + L.staging;
+    return L;
+}
+constexpr size_t kLdsPerCu = 160 * 1024;
 
 // Everything a GEMM kernel needs; passed by value as the kernel argument.
 struct GemmArgs {

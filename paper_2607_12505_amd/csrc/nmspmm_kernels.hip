@@ -3,24 +3,32 @@
 //
 // Orientation: the weight is the A operand and the activations the B operand
 // of the matrix instruction, so a 16 x 16 accumulator holds 16 output channels
-// x 16 tokens and each lane ends up with 4 consecutive channels of one token:
-// one 16-byte store per lane into the row-major output.  This orientation is
-// forced by the structured-sparse instruction, whose sparse operand is A.
+// x 16 tokens.  This orientation is forced by the structured-sparse
+// instruction, whose sparse operand is A.
 //
 // Dataflow of one workgroup (4 waves) over its k range, one 128-wide k-step at
 // a time (paper Sec. 4.2: sparse handling confined to packed loading, the
 // compute stage purely matrix-instruction based):
-//   - the tile_m x 128 int8 slice of X goes global -> VGPR -> LDS, double
-//     buffered, 16-byte chunks XOR-swizzled by row so the B-operand reads of
-//     16 tokens hit distinct banks;
-//   - the packed weight fragments of the next k-step are loaded straight from
-//     global memory into VGPRs (each lane one 16-byte value load and one
-//     4-byte position load per fragment and stream) while the current step
-//     computes: no decode, the packed form is the operand;
-//   - each wave runs FN x FM accumulators; per token fragment it reads the
-//     B operand from LDS once and reuses it for all FN weight fragments.
-//   - split-K (Sec. 4.3): every split runs the same code on its k range,
-//     stores its int32 partial tile, and the last split to arrive at a tile
+//   - every operand byte reaches LDS through the direct-to-LDS 16-byte (and
+//     4-byte) loads of gfx950, into a ring of NST k-step slots filled NST-1
+//     steps ahead of the compute: the tile_m x 128 slice of X, and the weight
+//     slice (the packed 4:2 fragments as stored, or tile_n x 128 rows of a
+//     dense W).  Each workgroup fetches each byte once; no VGPRs are spent on
+//     staging, so the ring depth costs only LDS.  Each lane picks the source
+//     chunk that belongs at its LDS slot, so row-major slices land with their
+//     16-byte chunks XOR-swizzled by row and the operand reads of 16 rows hit
+//     distinct banks;
+//   - the loads are issued from inline assembly and their completion is
+//     awaited explicitly (vector-memory counter, then one barrier per k-step),
+//     so the compiler does not serialise the ring with conservative waits;
+//   - each wave runs FN x FM accumulators: per k-step it reads its FN weight
+//     fragments from LDS once, then per token fragment the B operand once,
+//     reused by all FN weight fragments;
+//   - the epilogue goes back through LDS, 16 tokens at a time, so that every
+//     store instruction writes whole rows of the wave's tile: 16 lanes cover
+//     256 contiguous bytes of int32 (128 of fp16) per token;
+//   - split-K (Sec. 4.3): every split runs the same code on its k range and
+//     stores its int32 partial tile; the last split to arrive at a tile
 //     (atomic counter) adds the partials and runs the epilogue, so merging
 //     happens once, at the end.
 #include <hip/hip_runtime.h>
@@ -46,42 +54,181 @@ __device__ inline int map_block(int bid, int nwg) {
     return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
-template <int FN, int S>
-struct SparseRegs {
-    v4i v[FN][S];
-    int ix[FN][S];
+// Buffer-resource word 3 for raw 32-bit accesses, and the cache-policy bit
+// that makes a buffer access coherent at agent scope (sc1).
+constexpr int kBufferFlags = 0x00020000;
+constexpr int kSc1 = 16;
+
+// Direct-to-LDS loads: lane L's bytes land at lds_base + L * size.  lds_base
+// must be wave-uniform (it goes through M0).
+__device__ inline void dma16(const void *g, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_base) : "memory", "m0");
+}
+__device__ inline void dma4(const void *g, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_base) : "memory", "m0");
+}
+
+// Wait until at most N of this wave's vector-memory operations are in flight
+// and all of its LDS operations are done, then the workgroup barrier.
+template <int N>
+__device__ inline void wait_then_barrier() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Wait (no barrier) until at most N of this wave's vector-memory operations
+// are in flight and all of its LDS operations are done.
+template <int N>
+__device__ inline void wait_only() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
+    asm volatile("" ::: "memory");
+}
+
+template <int L, int DMA>
+__device__ inline void wait_later(int later) {
+    if constexpr (L <= 0) {
+        wait_only<0>();
+    } else {
+        if (later >= L) {
+            constexpr int n = L * DMA <= 63 ? L * DMA : (63 / DMA) * DMA;
+            wait_only<n>();
+        } else {
+            wait_later<L - 1, DMA>(later);
+        }
+    }
+}
+
+// Barrier of k-step iteration with `later` k-steps (each DMA loads per wave)
+// still allowed in flight: dispatches to the matching immediate.  The vmcnt
+// field holds at most 63; beyond that fewer loads are allowed in flight
+// (waiting longer is always safe).
+template <int L, int DMA>
+__device__ inline void wait_later_then_barrier(int later) {
+    if constexpr (L <= 0) {
+        wait_then_barrier<0>();
+    } else {
+        if (later >= L) {
+            constexpr int n = L * DMA <= 63 ? L * DMA : (63 / DMA) * DMA;
+            wait_then_barrier<n>();
+        } else {
+            wait_later_then_barrier<L - 1, DMA>(later);
+        }
+    }
+}
+
+// Writes 4 consecutive channels of one token: int32 and/or fp16(fp32(y) * scale).
+__device__ inline void emit_out(const GemmArgs &a, int tok, int ch, const v4i &v, const v4f &sc) {
+    if (a.Y) *(v4i *)(a.Y + (size_t)tok * a.n + ch) = v;
+    if (a.Yh) {
+        v4u16 h;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const _Float16 x = (_Float16)((float)v[e] * sc[e]);
+            h[e] = __builtin_bit_cast(unsigned short, x);
+        }
+        *(v4u16 *)(a.Yh + (size_t)tok * a.n + ch) = h;
+    }
+}
+
+__device__ inline v4f load_scale(const GemmArgs &a, int ch) {
+    v4f sc = {0.f, 0.f, 0.f, 0.f};
+    if (a.Yh && ch < a.n) sc = *(const v4f *)(a.scale + ch);
+    return sc;
+}
+
+// Split-K partial sums: [split_k x m x n] int32 below 2 GiB (checked by the
+// planner), accessed with agent-coherent (sc1) buffer operations: visible to
+// every XCD once complete, with no write-back of the non-coherent L2 needed.
+__device__ inline __amdgpu_buffer_rsrc_t partial_rsrc(const GemmArgs &a) {
+    return __builtin_amdgcn_make_buffer_rsrc(a.partials, 0, a.split_k > 1 ? a.split_k * a.m * a.n * 4 : 0,
+                                             kBufferFlags);
+}
+
+__device__ inline void publish_partial(const GemmArgs &a, __amdgpu_buffer_rsrc_t r, int split, int tok, int ch,
+                                       const v4i &v) {
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, ((split * a.m + tok) * a.n + ch) << 2, 0, kSc1);
+}
+
+__device__ inline v4i merge_partials(const GemmArgs &a, __amdgpu_buffer_rsrc_t r, int tok, int ch) {
+    v4i sum = v4i{0, 0, 0, 0};
+    for (int sp = 0; sp < a.split_k; ++sp)
+        sum += __builtin_amdgcn_raw_buffer_load_b128(r, ((sp * a.m + tok) * a.n + ch) << 2, 0, kSc1);
+    return sum;
+}
+
+// After every thread published its part of this split's partial tile: wait
+// for the stores to complete, count the arrival, and tell whether this
+// workgroup is the last split of the tile (then it merges).  The counter is
+// left at zero for the next call.
+__device__ inline bool arrive_last(const GemmArgs &a, int tile, int *s_flag) {
+    __builtin_amdgcn_s_waitcnt(0);  // every store of this wave has completed
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int old = __hip_atomic_fetch_add(&a.counters[tile], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int last = old == a.split_k - 1;
+        if (last) __hip_atomic_store(&a.counters[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *s_flag = last;
+    }
+    __syncthreads();
+    return *s_flag != 0;
+}
+
+template <int KIND, int WN, int WM, int FN, int FM, int NST>
+struct Geometry {
+    static constexpr int BN = WN * FN * 16;
+    static constexpr int BM = WM * FM * 16;
+    static constexpr bool kSparse = KIND != NM_KIND_DENSE;
+    static constexpr int S = KIND == NM_KIND_SP42X2 ? 2 : 1;
+    static constexpr int XB = BM * 128;                              // X bytes per slot
+    static constexpr int WVB = kSparse ? (BN / 16) * S * kVBlock : BN * 128;  // weight value bytes
+    static constexpr int WMB = kSparse ? (BN / 16) * S * kMBlock : 0;         // weight position bytes
+    static constexpr int SLOT = XB + WVB + WMB;
+    static constexpr int XI = BM / 32;                               // X loads per wave per k-step
+    static constexpr int WI = kSparse ? (BN / 16) * S / 4 * 2 : BN / 32;      // weight loads per wave
+    static constexpr int DMA = XI + WI;
+    static constexpr int CPR = FN * 4;                               // 4-channel chunks per staged row
+    static constexpr int RPI = 64 / CPR;                             // staged rows read per instruction
+    static constexpr int ROWB = FN * 64 + 16;                        // padded bytes per staged int32 row
+    static constexpr int EPI = 4 * 16 * ROWB;
+    // ring depth: as asked, or as deep as 160 KB of LDS allows
+    static constexpr int RING = NST * SLOT <= 160 * 1024 - 1024 ? NST : (160 * 1024 - 1024) / SLOT;
+    static constexpr int LDSB = RING * SLOT > EPI ? RING * SLOT : EPI;
+    static_assert(WN * WM == 4 && RING >= 2 && 64 % CPR == 0 && BM % 32 == 0, "tile shape");
+    static_assert(!kSparse || ((BN / 16) * S) % 4 == 0, "weight blocks split evenly over 4 waves");
+    static_assert(LDSB <= 160 * 1024, "LDS budget");
 };
 
-template <int FN>
-struct DenseRegs {
-    v4i lo[FN], hi[FN];
-};
-
-template <int KIND, int WN, int WM, int FN, int FM>
+template <int KIND, int WN, int WM, int FN, int FM, int NST>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
-    constexpr int BN = WN * FN * 16;
-    constexpr int BM = WM * FM * 16;
-    constexpr bool kSparse = KIND != NM_KIND_DENSE;
-    constexpr int S = KIND == NM_KIND_SP42X2 ? 2 : 1;
-    constexpr int XCH = BM / 32;  // 16-byte chunks of X each thread stages per k-step
-    static_assert(WN * WM == 4, "4 waves per workgroup");
-    using ARegs = typename std::conditional<kSparse, SparseRegs<FN, S>, DenseRegs<FN>>::type;
+    using G = Geometry<KIND, WN, WM, FN, FM, NST>;
+    constexpr int BN = G::BN, BM = G::BM, S = G::S;
+    constexpr bool kSparse = G::kSparse;
+    constexpr int R = G::RING;
 
-    __shared__ __attribute__((aligned(16))) int8_t lds[2 * BM * 128];
+    __shared__ __attribute__((aligned(1024))) int8_t lds[G::LDSB];
     __shared__ int s_last;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
 
     const int lid = map_block(blockIdx.x, gridDim.x);
     const int tn = lid % a.tiles_n;
     const int rest = lid / a.tiles_n;
     const int split = rest % a.split_k;
     const int tm = rest / a.split_k;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wn = wave % WN, wm = wave / WN;
     const int lg = lane >> 4;
     const int tok0 = tm * BM;
     const int ch0 = tn * BN;
     const int s_begin = (int)((int64_t)split * a.k_steps / a.split_k);
     const int s_end = (int)((int64_t)(split + 1) * a.k_steps / a.split_k);
+    const int nsteps = s_end - s_begin;
+    const int f0 = ch0 >> 4;
 
     v4i acc[FN][FM];
 #pragma unroll
@@ -89,164 +236,551 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
 
-    v4i xr[XCH];
-    auto load_x = [&](int s) {
+    // Fill ring slot st with k-step s.  Rows of X past m, and weight rows past
+    // n, read a valid row instead: their outputs are never stored.  Past k the
+    // packed weight is zero, so X may hold anything there; for a dense weight
+    // the tail k-step is staged with zeros instead (see below).
+    auto issue = [&](int s, int st) {
+        const uint32_t slot = lds0 + st * G::SLOT;
 #pragma unroll
-        for (int c = 0; c < XCH; ++c) {
-            const int idx = tid + 256 * c;
-            const int row = idx >> 3, chunk = idx & 7;
-            const int tok = tok0 + row;
-            const int kk = s * 128 + chunk * 16;
-            if (tok < a.m && kk < a.k)
-                xr[c] = *(const v4i *)(a.X + (size_t)tok * a.k + kk);
-            else
-                xr[c] = v4i{0, 0, 0, 0};
+        for (int j = 0; j < G::XI; ++j) {
+            const int r = 8 * (4 * j + wave) + (lane >> 3);
+            const int c = (lane & 7) ^ (r & 7);
+            const int tok = tok0 + r < a.m ? tok0 + r : a.m - 1;
+            const int kk = s * 128 + c * 16 < a.k ? s * 128 + c * 16 : a.k - 16;
+            dma16(a.X + (size_t)tok * a.k + kk, slot + (4 * j + wave) * 1024);
         }
-    };
-    auto store_x = [&](int buf) {
-#pragma unroll
-        for (int c = 0; c < XCH; ++c) {
-            const int idx = tid + 256 * c;
-            const int row = idx >> 3, chunk = idx & 7;
-            *(v4i *)(lds + buf * BM * 128 + row * 128 + ((chunk ^ (row & 7)) << 4)) = xr[c];
-        }
-    };
-    auto load_a = [&](int s, ARegs &R) {
         if constexpr (kSparse) {
 #pragma unroll
-            for (int i = 0; i < FN; ++i) {
-                const int f = (ch0 >> 4) + wn * FN + i;
-#pragma unroll
-                for (int q = 0; q < S; ++q) {
-                    if (f < a.n_frags) {
-                        const size_t b = ((size_t)f * a.k_steps + s) * S + q;
-                        R.v[i][q] = *(const v4i *)(a.A + b * kVBlock + lane * 16);
-                        R.ix[i][q] = *(const int *)(a.meta + b * kMBlock + lane * 4);
-                    } else {
-                        R.v[i][q] = v4i{0, 0, 0, 0};
-                        R.ix[i][q] = 0;
-                    }
-                }
+            for (int j = 0; j < (BN / 16) * S / 4; ++j) {
+                const int bl = 4 * j + wave;               // weight block of the slot: fragment bl / S, stream bl % S
+                int f = f0 + bl / S;
+                f = f < a.n_frags ? f : a.n_frags - 1;
+                const size_t b = ((size_t)f * a.k_steps + s) * S + bl % S;
+                dma16(a.A + b * kVBlock + lane * 16, slot + G::XB + bl * kVBlock);
+                dma4(a.meta + b * kMBlock + lane * 4, slot + G::XB + G::WVB + bl * kMBlock);
             }
         } else {
+            if (s * 128 + 128 <= a.k) {
 #pragma unroll
-            for (int i = 0; i < FN; ++i) {
-                const int row = ch0 + (wn * FN + i) * 16 + (lane & 15);
-                const int kk = s * 128 + lg * 16;
-                const int8_t *p = a.A + (size_t)row * a.k + kk;
-                R.lo[i] = (row < a.n && kk < a.k) ? *(const v4i *)p : v4i{0, 0, 0, 0};
-                R.hi[i] = (row < a.n && kk + 64 < a.k) ? *(const v4i *)(p + 64) : v4i{0, 0, 0, 0};
+                for (int j = 0; j < BN / 32; ++j) {
+                    const int r = 8 * (4 * j + wave) + (lane >> 3);
+                    const int c = (lane & 7) ^ (r & 7);
+                    const int row = ch0 + r < a.n ? ch0 + r : a.n - 1;
+                    dma16(a.A + (size_t)row * a.k + s * 128 + c * 16, slot + G::XB + (4 * j + wave) * 1024);
+                }
+            } else {
+                // tail k-step of a dense weight: plain loads, zeros past k
+#pragma unroll
+                for (int j = 0; j < BN / 32; ++j) {
+                    const int r = 8 * (4 * j + wave) + (lane >> 3);
+                    const int c = (lane & 7) ^ (r & 7);
+                    const int row = ch0 + r < a.n ? ch0 + r : a.n - 1;
+                    const int kk = s * 128 + c * 16;
+                    v4i v = v4i{0, 0, 0, 0};
+                    if (kk < a.k) v = *(const v4i *)(a.A + (size_t)row * a.k + kk);
+                    *(v4i *)(lds + st * G::SLOT + G::XB + (4 * j + wave) * 1024 + lane * 16) = v;
+                }
             }
         }
     };
-    auto compute = [&](int buf, const ARegs &R) {
-        const int8_t *L = lds + buf * BM * 128;
+
+    auto compute = [&](int st) {
+        const int8_t *xs = lds + st * G::SLOT;
+        const int8_t *ws = xs + G::XB;
+        if constexpr (kSparse) {
+            v4i av[FN][S];
+            int ai[FN][S];
 #pragma unroll
-        for (int j = 0; j < FM; ++j) {
-            const int r = (wm * FM + j) * 16 + (lane & 15);
-            const int8_t *rowp = L + r * 128;
-            const v4i blo = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
-            const v4i bhi = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
-            if constexpr (kSparse) {
+            for (int i = 0; i < FN; ++i)
+#pragma unroll
+                for (int q = 0; q < S; ++q) {
+                    const int bl = (wn * FN + i) * S + q;
+                    av[i][q] = *(const v4i *)(ws + bl * kVBlock + lane * 16);
+                    ai[i][q] = *(const int *)(ws + G::WVB + bl * kMBlock + lane * 4);
+                }
+#pragma unroll
+            for (int j = 0; j < FM; ++j) {
+                const int r = (wm * FM + j) * 16 + (lane & 15);
+                const int8_t *rowp = xs + r * 128;
+                const v4i blo = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
+                const v4i bhi = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
                 const v8i b = {blo[0], blo[1], blo[2], blo[3], bhi[0], bhi[1], bhi[2], bhi[3]};
 #pragma unroll
                 for (int i = 0; i < FN; ++i)
 #pragma unroll
                     for (int q = 0; q < S; ++q)
-                        acc[i][j] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(R.v[i][q], b, acc[i][j], R.ix[i][q], 0, 0);
-            } else {
+                        acc[i][j] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(av[i][q], b, acc[i][j], ai[i][q], 0, 0);
+            }
+        } else {
+            v4i alo[FN], ahi[FN];
+#pragma unroll
+            for (int i = 0; i < FN; ++i) {
+                const int r = (wn * FN + i) * 16 + (lane & 15);
+                const int8_t *rowp = ws + r * 128;
+                alo[i] = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
+                ahi[i] = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
+            }
+#pragma unroll
+            for (int j = 0; j < FM; ++j) {
+                const int r = (wm * FM + j) * 16 + (lane & 15);
+                const int8_t *rowp = xs + r * 128;
+                const v4i blo = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
+                const v4i bhi = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
 #pragma unroll
                 for (int i = 0; i < FN; ++i) {
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(R.lo[i], blo, acc[i][j], 0, 0, 0);
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(R.hi[i], bhi, acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(alo[i], blo, acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ahi[i], bhi, acc[i][j], 0, 0, 0);
                 }
             }
         }
     };
 
-    ARegs cur, nxt;
-    load_x(s_begin);
-    load_a(s_begin, cur);
-    store_x(0);
-    for (int s = s_begin; s < s_end; ++s) {
-        const int buf = (s - s_begin) & 1;
-        __syncthreads();
-        const bool more = s + 1 < s_end;
-        if (more) {
-            load_x(s + 1);
-            load_a(s + 1, nxt);
-        }
-        compute(buf, cur);
-        if (more) {
-            store_x(buf ^ 1);
-            cur = nxt;
-        }
+#pragma unroll
+    for (int i = 0; i < R - 1; ++i)
+        if (i < nsteps) issue(s_begin + i, i);
+    for (int it = 0; it < nsteps; ++it) {
+        // k-step it was issued NST-1 iterations ago; only the loads of later
+        // k-steps may remain in flight.  The barrier then publishes every
+        // wave's slot and frees the slot computed in the previous iteration.
+        const int later = nsteps - 1 - it < R - 2 ? nsteps - 1 - it : R - 2;
+        wait_later_then_barrier<R - 2, G::DMA>(later);
+        if (it + R - 1 < nsteps) issue(s_begin + it + R - 1, (it + R - 1) % R);
+        compute(it % R);
     }
 
-    auto emit = [&](int tok, int ch, const v4i &v) {
-        if (a.Y) *(v4i *)(a.Y + (size_t)tok * a.n + ch) = v;
-        if (a.Yh) {
-            const v4f sc = *(const v4f *)(a.scale + ch);
-            v4u16 h;
+    // Epilogue through LDS: each wave stages 16 tokens x FN*16 channels of its
+    // accumulators as int32 rows, then reads them back row-contiguously.
+    __syncthreads();  // every wave is done with the ring
+    int8_t *stg = lds + wave * 16 * G::ROWB;
+    const int ec = lane % G::CPR;                     // 4-channel chunk this lane stores
+    const int er = lane / G::CPR;                     // row offset within a read group
+    const int ch = ch0 + wn * FN * 16 + ec * 4;       // first of the lane's 4 channels
+    const bool ch_ok = ch < a.n;
+    const v4f sc = load_scale(a, ch);
+    const __amdgpu_buffer_rsrc_t prsrc = partial_rsrc(a);
+
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const _Float16 x = (_Float16)((float)v[e] * sc[e]);
-                h[e] = __builtin_bit_cast(unsigned short, x);
+    for (int j = 0; j < FM; ++j) {
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+            *(v4i *)(stg + (lane & 15) * G::ROWB + (i * 16 + 4 * lg) * 4) = acc[i][j];
+#pragma unroll
+        for (int r0 = 0; r0 < 16; r0 += G::RPI) {
+            const int t = r0 + er;
+            const v4i v = *(const v4i *)(stg + t * G::ROWB + ec * 16);
+            const int tok = tok0 + (wm * FM + j) * 16 + t;
+            if (tok < a.m && ch_ok) {
+                if (a.split_k == 1)
+                    emit_out(a, tok, ch, v, sc);
+                else
+                    publish_partial(a, prsrc, split, tok, ch, v);
             }
-            *(v4u16 *)(a.Yh + (size_t)tok * a.n + ch) = h;
+        }
+    }
+    if (a.split_k == 1) return;
+
+    // Split-K: the last split to arrive adds every partial (integer addition:
+    // any order gives the same result) and writes the outputs.
+    if (!arrive_last(a, tm * a.tiles_n + tn, &s_last)) return;
+#pragma unroll
+    for (int j = 0; j < FM; ++j)
+#pragma unroll
+        for (int r0 = 0; r0 < 16; r0 += G::RPI) {
+            const int tok = tok0 + (wm * FM + j) * 16 + r0 + er;
+            if (tok < a.m && ch_ok) emit_out(a, tok, ch, merge_partials(a, prsrc, tok, ch), sc);
+        }
+}
+
+// ---------------------------------------------------------------------------
+// k-sliced variant for shapes with few output tiles (small token counts).
+// Each of the 4 waves computes the whole tile_n x tile_m tile over its own
+// quarter of the k-steps (k-step s goes to wave s % 4), through a ring of
+// LDS slots that only it fills and reads: no workgroup barrier in the main
+// loop, and FN x FM matrix instructions per wave per k-step to cover the LDS
+// latency.  The four partial tiles are added through LDS at the end -- a
+// split of the reduction merged in the final stage without leaving the CU.
+
+template <int KIND, int FN, int FM, int NST>
+struct GeometryKS {
+    static constexpr int BN = FN * 16;
+    static constexpr int BM = FM * 16;
+    static constexpr bool kSparse = KIND != NM_KIND_DENSE;
+    static constexpr int S = KIND == NM_KIND_SP42X2 ? 2 : 1;
+    static constexpr int XB = BM * 128;
+    static constexpr int WVB = kSparse ? (BN / 16) * S * kVBlock : BN * 128;
+    static constexpr int WMB = kSparse ? (BN / 16) * S * kMBlock : 0;
+    static constexpr int SLOT = XB + WVB + WMB;
+    static constexpr int XI = BM / 8;                                  // X loads per k-step (one wave)
+    static constexpr int WI = kSparse ? (BN / 16) * S * 2 : BN / 8;    // weight loads per k-step
+    static constexpr int DMA = XI + WI;
+    static constexpr int RING = 4 * NST * SLOT <= 160 * 1024 - 1024 ? NST : (160 * 1024 - 1024) / (4 * SLOT);
+    static constexpr int ROWB = BN * 4 + 16;                           // padded staged row (int32)
+    static constexpr int RED = 4 * BM * ROWB;
+    static constexpr int LDSB = 4 * RING * SLOT > RED ? 4 * RING * SLOT : RED;
+    static constexpr int CPR = BN / 4;                                 // 16-byte chunks per output row
+    static_assert(RING >= 2 && BM % 8 == 0 && BN % 16 == 0, "tile shape");
+};
+
+template <int KIND, int FN, int FM, int NST>
+__global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
+    using G = GeometryKS<KIND, FN, FM, NST>;
+    constexpr int BN = G::BN, BM = G::BM, S = G::S, R = G::RING;
+    constexpr bool kSparse = G::kSparse;
+
+    __shared__ __attribute__((aligned(1024))) int8_t lds[G::LDSB];
+    __shared__ int s_last;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
+
+    const int lid = map_block(blockIdx.x, gridDim.x);
+    const int tn = lid % a.tiles_n;
+    const int rest = lid / a.tiles_n;
+    const int split = rest % a.split_k;
+    const int tm = rest / a.split_k;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lg = lane >> 4;
+    const int tok0 = tm * BM;
+    const int ch0 = tn * BN;
+    const int s_begin = (int)((int64_t)split * a.k_steps / a.split_k);
+    const int s_end = (int)((int64_t)(split + 1) * a.k_steps / a.split_k);
+    const int nsteps = s_end - s_begin > wave ? (s_end - s_begin - wave + 3) / 4 : 0;  // this wave's k-steps
+    const int f0 = ch0 >> 4;
+    const uint32_t ring = lds0 + wave * R * G::SLOT;
+    int8_t *ringp = lds + wave * R * G::SLOT;
+
+    v4i acc[FN][FM];
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+
+    // k-step s into slot st of this wave's ring (same clamping rules as above)
+    auto issue = [&](int s, int st) {
+        const uint32_t slot = ring + st * G::SLOT;
+#pragma unroll
+        for (int j = 0; j < BM / 8; ++j) {
+            const int r = 8 * j + (lane >> 3);
+            const int c = (lane & 7) ^ (r & 7);
+            const int tok = tok0 + r < a.m ? tok0 + r : a.m - 1;
+            const int kk = s * 128 + c * 16 < a.k ? s * 128 + c * 16 : a.k - 16;
+            dma16(a.X + (size_t)tok * a.k + kk, slot + j * 1024);
+        }
+        if constexpr (kSparse) {
+#pragma unroll
+            for (int bl = 0; bl < (BN / 16) * S; ++bl) {
+                int f = f0 + bl / S;
+                f = f < a.n_frags ? f : a.n_frags - 1;
+                const size_t b = ((size_t)f * a.k_steps + s) * S + bl % S;
+                dma16(a.A + b * kVBlock + lane * 16, slot + G::XB + bl * kVBlock);
+                dma4(a.meta + b * kMBlock + lane * 4, slot + G::XB + G::WVB + bl * kMBlock);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < BN / 8; ++j) {
+                const int r = 8 * j + (lane >> 3);
+                const int c = (lane & 7) ^ (r & 7);
+                const int row = ch0 + r < a.n ? ch0 + r : a.n - 1;
+                const int kk = s * 128 + c * 16;
+                if (s * 128 + 128 <= a.k) {
+                    dma16(a.A + (size_t)row * a.k + kk, slot + G::XB + j * 1024);
+                } else {  // tail k-step of a dense weight: zeros past k
+                    v4i v = v4i{0, 0, 0, 0};
+                    if (kk < a.k) v = *(const v4i *)(a.A + (size_t)row * a.k + kk);
+                    *(v4i *)(ringp + st * G::SLOT + G::XB + j * 1024 + lane * 16) = v;
+                }
+            }
+        }
+    };
+    auto compute = [&](int st) {
+        const int8_t *xs = ringp + st * G::SLOT;
+        const int8_t *ws = xs + G::XB;
+        if constexpr (kSparse) {
+            v4i av[FN][S];
+            int ai[FN][S];
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+#pragma unroll
+                for (int q = 0; q < S; ++q) {
+                    av[i][q] = *(const v4i *)(ws + (i * S + q) * kVBlock + lane * 16);
+                    ai[i][q] = *(const int *)(ws + G::WVB + (i * S + q) * kMBlock + lane * 4);
+                }
+#pragma unroll
+            for (int j = 0; j < FM; ++j) {
+                const int r = j * 16 + (lane & 15);
+                const int8_t *rowp = xs + r * 128;
+                const v4i blo = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
+                const v4i bhi = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
+                const v8i b = {blo[0], blo[1], blo[2], blo[3], bhi[0], bhi[1], bhi[2], bhi[3]};
+#pragma unroll
+                for (int i = 0; i < FN; ++i)
+#pragma unroll
+                    for (int q = 0; q < S; ++q)
+                        acc[i][j] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(av[i][q], b, acc[i][j], ai[i][q], 0, 0);
+            }
+        } else {
+            v4i alo[FN], ahi[FN];
+#pragma unroll
+            for (int i = 0; i < FN; ++i) {
+                const int r = i * 16 + (lane & 15);
+                const int8_t *rowp = ws + r * 128;
+                alo[i] = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
+                ahi[i] = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
+            }
+#pragma unroll
+            for (int j = 0; j < FM; ++j) {
+                const int r = j * 16 + (lane & 15);
+                const int8_t *rowp = xs + r * 128;
+                const v4i blo = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
+                const v4i bhi = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
+#pragma unroll
+                for (int i = 0; i < FN; ++i) {
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(alo[i], blo, acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ahi[i], bhi, acc[i][j], 0, 0, 0);
+                }
+            }
         }
     };
 
-    if (a.split_k == 1) {
+    // k-step t of this wave is s_begin + wave + 4 t
+#pragma unroll
+    for (int i = 0; i < R - 1; ++i)
+        if (i < nsteps) issue(s_begin + wave + 4 * i, i);
+    for (int t = 0; t < nsteps; ++t) {
+        const int later = nsteps - 1 - t < R - 2 ? nsteps - 1 - t : R - 2;
+        wait_later<R - 2, G::DMA>(later);  // this wave's slot t is in LDS, its reads of slot t-1 done
+        if (t + R - 1 < nsteps) issue(s_begin + wave + 4 * (t + R - 1), (t + R - 1) % R);
+        compute(t % R);
+    }
+
+    // Add the four waves' partial tiles through LDS, then write rows.
+    __syncthreads();  // every wave is done with its ring
+    int8_t *stg = lds + wave * BM * G::ROWB;
+#pragma unroll
+    for (int j = 0; j < FM; ++j)
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+            *(v4i *)(stg + (j * 16 + (lane & 15)) * G::ROWB + (i * 16 + 4 * lg) * 4) = acc[i][j];
+    __syncthreads();
+    const __amdgpu_buffer_rsrc_t prsrc = partial_rsrc(a);
+    constexpr int CHUNKS = BM * G::CPR;
+    for (int c = tid; c < CHUNKS; c += 256) {
+        const int row = c / G::CPR, cc = c % G::CPR;
+        const int tok = tok0 + row, ch = ch0 + cc * 4;
+        v4i v = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int w = 0; w < 4; ++w) v += *(const v4i *)(lds + w * BM * G::ROWB + row * G::ROWB + cc * 16);
+        if (tok < a.m && ch < a.n) {
+            if (a.split_k == 1)
+                emit_out(a, tok, ch, v, load_scale(a, ch));
+            else
+                publish_partial(a, prsrc, split, tok, ch, v);
+        }
+    }
+    if (a.split_k == 1) return;
+    if (!arrive_last(a, tm * a.tiles_n + tn, &s_last)) return;
+    for (int c = tid; c < CHUNKS; c += 256) {
+        const int tok = tok0 + c / G::CPR, ch = ch0 + (c % G::CPR) * 4;
+        if (tok < a.m && ch < a.n) emit_out(a, tok, ch, merge_partials(a, prsrc, tok, ch), load_scale(a, ch));
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Row-stationary variant for shapes whose time goes into writing the output
+// (large token counts, short k).  The grid is a fixed number of workgroups;
+// each walks an equal, contiguous share of the output tiles in token-block
+// order.  While the token block stays the same, its X slice (all k-steps)
+// stays resident in LDS, so X is read once per workgroup instead of once per
+// output tile, and only the weight streams through a ring of k-step slots.
+// A fifth, producer wave issues every load and waits on their completion;
+// the four consumer waves only read LDS, run the matrix instructions and
+// store the outputs.  Because the consumers never wait on the vector-memory
+// counter, their output stores drain to HBM while the next tile computes.
+
+template <int KIND, int FN, int FM, int NST>
+__global__ __launch_bounds__(320) void k_gemm_rs(GemmArgs a) {
+    constexpr int BN = 2 * FN * 16;
+    constexpr int BM = 2 * FM * 16;
+    constexpr bool kSparse = KIND != NM_KIND_DENSE;
+    constexpr int S = KIND == NM_KIND_SP42X2 ? 2 : 1;
+    constexpr int WVB = kSparse ? (BN / 16) * S * kVBlock : BN * 128;
+    constexpr int WMB = kSparse ? (BN / 16) * S * kMBlock : 0;
+    constexpr int WSLOT = WVB + WMB;
+    constexpr int WI = kSparse ? (BN / 16) * S * 2 : BN / 8;  // producer loads per weight slot
+    constexpr int CPR = FN * 4;
+    constexpr int RPI = 64 / CPR;
+    constexpr int ROWB = FN * 64 + 16;
+    constexpr int R = NST;
+    static_assert(64 % CPR == 0 && R >= 2, "tile shape");
+
+    extern __shared__ __attribute__((aligned(1024))) int8_t lds[];
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
+    const int XBB = a.k_steps * BM * 128;            // resident X block
+    int8_t *ringp = lds + XBB;
+    const uint32_t ring = lds0 + XBB;
+    int8_t *stage_base = ringp + R * WSLOT;
+
+    const int T = a.tiles_m * a.tiles_n;
+    const int t_begin = (int)((int64_t)blockIdx.x * T / gridDim.x);
+    const int t_end = (int)((int64_t)(blockIdx.x + 1) * T / gridDim.x);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const bool producer = wave == 4;
+    const int wn = wave & 1, wm = (wave >> 1) & 1;
+    const int lg = lane >> 4;
+
+    // weight slice of (tile tn, k-step s) into ring slot st (producer)
+    auto issue_w = [&](int tn, int s, int st) {
+        const uint32_t slot = ring + st * WSLOT;
+        if constexpr (kSparse) {
+#pragma unroll
+            for (int bl = 0; bl < (BN / 16) * S; ++bl) {
+                int f = tn * (BN / 16) + bl / S;
+                f = f < a.n_frags ? f : a.n_frags - 1;
+                const size_t b = ((size_t)f * a.k_steps + s) * S + bl % S;
+                dma16(a.A + b * kVBlock + lane * 16, slot + bl * kVBlock);
+                dma4(a.meta + b * kMBlock + lane * 4, slot + WVB + bl * kMBlock);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < BN / 8; ++j) {
+                const int r = 8 * j + (lane >> 3);
+                const int c = (lane & 7) ^ (r & 7);
+                const int row = tn * BN + r < a.n ? tn * BN + r : a.n - 1;
+                const int kk = s * 128 + c * 16;
+                if (s * 128 + 128 <= a.k) {
+                    dma16(a.A + (size_t)row * a.k + kk, slot + j * 1024);
+                } else {  // tail k-step of a dense weight: zeros past k
+                    v4i v = v4i{0, 0, 0, 0};
+                    if (kk < a.k) v = *(const v4i *)(a.A + (size_t)row * a.k + kk);
+                    *(v4i *)(ringp + st * WSLOT + j * 1024 + lane * 16) = v;
+                }
+            }
+        }
+    };
+
+    v4i acc[FN][FM];
+    auto zero_acc = [&]() {
 #pragma unroll
         for (int i = 0; i < FN; ++i)
 #pragma unroll
+            for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+    };
+    auto compute = [&](int st, int s) {
+        const int8_t *xs = lds + s * BM * 128;
+        const int8_t *ws = ringp + st * WSLOT;
+        if constexpr (kSparse) {
+            v4i av[FN][S];
+            int ai[FN][S];
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+#pragma unroll
+                for (int q = 0; q < S; ++q) {
+                    const int bl = (wn * FN + i) * S + q;
+                    av[i][q] = *(const v4i *)(ws + bl * kVBlock + lane * 16);
+                    ai[i][q] = *(const int *)(ws + WVB + bl * kMBlock + lane * 4);
+                }
+#pragma unroll
             for (int j = 0; j < FM; ++j) {
-                const int ch = ch0 + (wn * FN + i) * 16 + 4 * lg;
-                const int tok = tok0 + (wm * FM + j) * 16 + (lane & 15);
-                if (tok < a.m && ch < a.n) emit(tok, ch, acc[i][j]);
+                const int r = (wm * FM + j) * 16 + (lane & 15);
+                const int8_t *rowp = xs + r * 128;
+                const v4i blo = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
+                const v4i bhi = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
+                const v8i b = {blo[0], blo[1], blo[2], blo[3], bhi[0], bhi[1], bhi[2], bhi[3]};
+#pragma unroll
+                for (int i = 0; i < FN; ++i)
+#pragma unroll
+                    for (int q = 0; q < S; ++q)
+                        acc[i][j] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(av[i][q], b, acc[i][j], ai[i][q], 0, 0);
             }
-        return;
-    }
+        } else {
+            v4i alo[FN], ahi[FN];
+#pragma unroll
+            for (int i = 0; i < FN; ++i) {
+                const int r = (wn * FN + i) * 16 + (lane & 15);
+                const int8_t *rowp = ws + r * 128;
+                alo[i] = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
+                ahi[i] = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
+            }
+#pragma unroll
+            for (int j = 0; j < FM; ++j) {
+                const int r = (wm * FM + j) * 16 + (lane & 15);
+                const int8_t *rowp = xs + r * 128;
+                const v4i blo = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
+                const v4i bhi = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
+#pragma unroll
+                for (int i = 0; i < FN; ++i) {
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(alo[i], blo, acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ahi[i], bhi, acc[i][j], 0, 0, 0);
+                }
+            }
+        }
+    };
+    // consumer epilogue of one tile: stage 16 tokens at a time, store rows
+    int8_t *stg = stage_base + (wave & 3) * 16 * ROWB;
+    const int ec = lane % CPR, er = lane / CPR;
+    auto epilogue = [&](int tm, int tn) {
+        const int ch = tn * BN + wn * FN * 16 + ec * 4;
+        const bool ch_ok = ch < a.n;
+        const v4f sc = load_scale(a, ch);
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+                *(v4i *)(stg + (lane & 15) * ROWB + (i * 16 + 4 * lg) * 4) = acc[i][j];
+#pragma unroll
+            for (int r0 = 0; r0 < 16; r0 += RPI) {
+                const int t = r0 + er;
+                const v4i v = *(const v4i *)(stg + t * ROWB + ec * 16);
+                const int tok = tm * BM + (wm * FM + j) * 16 + t;
+                if (tok < a.m && ch_ok) emit_out(a, tok, ch, v, sc);
+            }
+        }
+    };
 
-    // Split-K: publish this split's partial tile, then the last split to
-    // arrive adds all partials (integer addition: any order gives the same
-    // result) and writes the outputs.
+    for (int ta = t_begin; ta < t_end;) {
+        // one phase: the tiles of one token block
+        const int tm = ta / a.tiles_n;
+        const int tb = (tm + 1) * a.tiles_n < t_end ? (tm + 1) * a.tiles_n : t_end;
+        const int nq = (tb - ta) * a.k_steps;  // (tile, k-step) pairs of the phase
+        if (producer) {
+            const uint32_t xb = lds0;
+            for (int s = 0; s < a.k_steps; ++s)
 #pragma unroll
-    for (int i = 0; i < FN; ++i)
+                for (int j = 0; j < BM / 8; ++j) {
+                    const int r = 8 * j + (lane >> 3);
+                    const int c = (lane & 7) ^ (r & 7);
+                    const int tok = tm * BM + r < a.m ? tm * BM + r : a.m - 1;
+                    const int kk = s * 128 + c * 16 < a.k ? s * 128 + c * 16 : a.k - 16;
+                    dma16(a.X + (size_t)tok * a.k + kk, xb + s * BM * 128 + j * 1024);
+                }
 #pragma unroll
-        for (int j = 0; j < FM; ++j) {
-            const int ch = ch0 + (wn * FN + i) * 16 + 4 * lg;
-            const int tok = tok0 + (wm * FM + j) * 16 + (lane & 15);
-            if (tok < a.m && ch < a.n)
-                *(v4i *)(a.partials + ((size_t)split * a.m + tok) * a.n + ch) = acc[i][j];
-        }
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-        const int tile = tm * a.tiles_n + tn;
-        const int old = atomicAdd(&a.counters[tile], 1);
-        const int last = old == a.split_k - 1;
-        if (last) atomicExch(&a.counters[tile], 0);  // leave the counter ready for the next call
-        s_last = last;
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-#pragma unroll
-    for (int i = 0; i < FN; ++i)
-#pragma unroll
-        for (int j = 0; j < FM; ++j) {
-            const int ch = ch0 + (wn * FN + i) * 16 + 4 * lg;
-            const int tok = tok0 + (wm * FM + j) * 16 + (lane & 15);
-            if (tok >= a.m || ch >= a.n) continue;
-            v4i sum = acc[i][j];
-            for (int sp = 0; sp < a.split_k; ++sp) {
-                if (sp == split) continue;
-                sum += *(const v4i *)(a.partials + ((size_t)sp * a.m + tok) * a.n + ch);
+            for (int i = 0; i < R - 1; ++i)
+                if (i < nq) issue_w((ta + i / a.k_steps) % a.tiles_n, i % a.k_steps, i);
+            for (int q = 0; q < nq; ++q) {
+                // slot q (and, before it, the X block) has landed; the
+                // consumers are done with slot q-1, which is refilled next
+                const int later = nq - 1 - q < R - 2 ? nq - 1 - q : R - 2;
+                wait_later_then_barrier<R - 2, WI>(later);
+                const int qn = q + R - 1;
+                if (qn < nq) issue_w((ta + qn / a.k_steps) % a.tiles_n, qn % a.k_steps, qn % R);
             }
-            emit(tok, ch, sum);
+            wait_then_barrier<63>();  // end of phase: X block and ring are free again
+        } else {
+            zero_acc();
+            for (int q = 0; q < nq; ++q) {
+                wait_then_barrier<63>();  // own LDS reads done; slot q published
+                const int s = q % a.k_steps;
+                compute(q % R, s);
+                if (s == a.k_steps - 1) {
+                    epilogue(tm, (ta + q / a.k_steps) % a.tiles_n);
+                    zero_acc();
+                }
+            }
+            wait_then_barrier<63>();
         }
+        ta = tb;
+    }
 }
 
 __global__ void k_zero(int *p, size_t n4, unsigned char *tail, int tail_bytes) {
@@ -258,8 +792,23 @@ __global__ void k_zero(int *p, size_t n4, unsigned char *tail, int tail_bytes) {
 template <int KIND, int T>
 int launch_one(const GemmArgs &args, int grid, void *stream) {
     constexpr TileCfg t = kTiles[T];
-    hipLaunchKernelGGL((k_gemm<KIND, t.wn, t.wm, t.fn, t.fm>), dim3(grid), dim3(kThreads), 0,
-                       (hipStream_t)stream, args);
+    if constexpr (t.layout == kRowStat) {
+        const size_t bytes = rowstat_lds(KIND, t, args.k_steps).total;
+        static bool attr_set = false;  // the attribute is per kernel; setting it twice is harmless
+        if (!attr_set) {
+            hipError_t e = hipFuncSetAttribute((const void *)k_gemm_rs<KIND, t.fn, t.fm, t.nst>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsPerCu);
+            if (e != hipSuccess) return (int)e;
+            attr_set = true;
+        }
+        hipLaunchKernelGGL((k_gemm_rs<KIND, t.fn, t.fm, t.nst>), dim3(grid), dim3(320), bytes, (hipStream_t)stream,
+                           args);
+    } else if constexpr (t.layout == kKSliced)
+        hipLaunchKernelGGL((k_gemm_ks<KIND, t.fn, t.fm, t.nst>), dim3(grid), dim3(kThreads), 0,
+                           (hipStream_t)stream, args);
+    else
+        hipLaunchKernelGGL((k_gemm<KIND, t.wn, t.wm, t.fn, t.fm, t.nst>), dim3(grid), dim3(kThreads), 0,
+                           (hipStream_t)stream, args);
     return (int)hipGetLastError();
 }
 

@@ -26,7 +26,7 @@ NM_LAYOUT_SP42 = 1
 # Every symbol the header declares (checked by the CPU tests).
 EXPORTED = (
     "nm_status_string", "nm_compress_size", "nm_compress", "nm_decompress", "nm_num_tiles",
-    "nm_tile_info", "nm_spmm_plan", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
+    "nm_tile_info", "nm_plan_kernel_name", "nm_spmm_plan", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
     "nm_spmm", "nm_spmm_ex", "nm_gemm_i8_dense", "nm_gemm_i8_dense_ex",
 )
 
@@ -76,6 +76,7 @@ def lib() -> ctypes.CDLL:
             "nm_decompress": ([pd, vp, vp, vp], i32),
             "nm_num_tiles": ([], i32),
             "nm_tile_info": ([i32, ctypes.POINTER(i32), ctypes.POINTER(i32)], i32),
+            "nm_plan_kernel_name": ([pp, ctypes.c_char_p, i32], i32),
             "nm_spmm_plan": ([pd, i32, i32, pp], i32),
             "nm_gemm_i8_dense_plan": ([i32, i32, i32, i32, pp], i32),
             "nm_workspace_size": ([pp, i32, i32, ctypes.POINTER(sz)], i32),
@@ -156,6 +157,12 @@ def tile_info(tile: int):
     a, b = ctypes.c_int(), ctypes.c_int()
     _check(lib().nm_tile_info(tile, ctypes.byref(a), ctypes.byref(b)), "nm_tile_info")
     return a.value, b.value
+
+
+def plan_kernel_name(plan: NmPlan) -> str:
+    buf = ctypes.create_string_buffer(128)
+    _check(lib().nm_plan_kernel_name(ctypes.byref(plan), buf, 128), "nm_plan_kernel_name")
+    return buf.value.decode()
 
 
 def spmm_plan(desc: NmDesc, m: int, out_mode: int = NM_OUT_I32) -> NmPlan:

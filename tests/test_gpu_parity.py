@@ -108,14 +108,55 @@ def test_every_tile_and_split_is_bit_identical(kind):
     dw = nmspmm.DeviceWeight.from_packed(packed)
     for tile in range(nmspmm.num_tiles()):
         for split in (1, 2, 4, 8):
-            print(f"kind {kind} tile {tile} split {split}", flush=True)
             plan = nmspmm.make_plan(kind, tile, split)
+            try:
+                nmspmm.workspace_size(plan, m, n)
+                if "k_gemm_rs" in nmspmm.plan_kernel_name(plan) and split > 1:
+                    continue  # the row-stationary layout takes split_k = 1 only
+            except nmspmm.NmError:
+                continue
+            print(f"kind {kind} tile {tile} split {split}", flush=True)
+            try:
+                if kind == nmspmm.NM_KIND_DENSE:
+                    Y, Yh = gu.run_dense(X, W, scale, True, True, plan=plan)
+                else:
+                    Y, Yh = gu.run_sparse(X, packed, scale, True, True, plan=plan, dw=dw)
+            except nmspmm.NmError as e:
+                # a row-stationary tile whose X block does not fit in LDS at this k
+                assert e.status == nmspmm.NM_ERR_SHAPE and "k_gemm_rs" in nmspmm.plan_kernel_name(plan)
+                continue
+            assert np.array_equal(Y, ref), (tile, split)
+            gu.assert_f16_close(Yh, ref_h)
+
+
+@pytest.mark.parametrize("kind", [nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_SP42X2, nmspmm.NM_KIND_DENSE])
+@pytest.mark.parametrize("m,n,k", [(1000, 400, 384), (333, 1540, 256), (2600, 264, 640), (129, 128, 128)])
+def test_row_stationary_tiles(kind, m, n, k):
+    # workgroups walking several output tiles with the X block resident, phases
+    # that change token block mid-range, ragged m and n, a dense k tail
+    N, M = {nmspmm.NM_KIND_SP42: (2, 4), nmspmm.NM_KIND_SP42X2: (5, 8), nmspmm.NM_KIND_DENSE: (8, 8)}[kind]
+    X, W, scale = _case(m, n, k, N, M, seed=kind * 7 + m)
+    ref = oracle.matmul_i8(X, W)
+    ref_h = oracle.dequant_f16(ref, scale)
+    packed = nmspmm.compress(W, N, M)
+    ran = 0
+    for tile in range(nmspmm.num_tiles()):
+        plan = nmspmm.make_plan(kind, tile, 1)
+        if "k_gemm_rs" not in nmspmm.plan_kernel_name(plan):
+            continue
+        print(f"row-stationary kind {kind} tile {tile} m={m} n={n} k={k}", flush=True)
+        try:
             if kind == nmspmm.NM_KIND_DENSE:
                 Y, Yh = gu.run_dense(X, W, scale, True, True, plan=plan)
             else:
-                Y, Yh = gu.run_sparse(X, packed, scale, True, True, plan=plan, dw=dw)
-            assert np.array_equal(Y, ref), (tile, split)
-            gu.assert_f16_close(Yh, ref_h)
+                Y, Yh = gu.run_sparse(X, packed, scale, True, True, plan=plan)
+        except nmspmm.NmError as e:
+            assert e.status == nmspmm.NM_ERR_SHAPE  # LDS of this tile exceeded at this k
+            continue
+        assert np.array_equal(Y, ref), tile
+        gu.assert_f16_close(Yh, ref_h)
+        ran += 1
+    assert ran >= 2
 
 
 def test_repeated_split_k_runs_are_identical():
@@ -126,12 +167,11 @@ def test_repeated_split_k_runs_are_identical():
     ref = oracle.matmul_i8(X, W)
     packed = nmspmm.compress(W, 2, 4)
     dw = nmspmm.DeviceWeight.from_packed(packed)
-    plan = nmspmm.spmm_plan(packed.desc, m, nmspmm.NM_OUT_I32)
-    assert plan.split_k > 1
     Xd = torch.from_numpy(X).cuda()
     outs = [torch.empty((m, n), dtype=torch.int32, device="cuda") for _ in range(30)]
-    for Y in outs:
-        nmspmm.spmm(Xd, dw, Y=Y)
+    plans = [nmspmm.make_plan(nmspmm.NM_KIND_SP42, t, s) for t in (6, 10) for s in (2, 4, 8)]
+    for i, Y in enumerate(outs):
+        nmspmm.spmm(Xd, dw, Y=Y, plan=plans[i % len(plans)])
     torch.cuda.synchronize()
     for Y in outs:
         assert np.array_equal(Y.cpu().numpy(), ref)

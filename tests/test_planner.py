@@ -32,33 +32,43 @@ def test_plan_rules(shape):
         assert p.split_k in (1, 2, 4, 8)
         tn, tm = nmspmm.tile_info(p.tile)
         tiles = -(-n // tn) * -(-m // tm)
-        assert p.grid == tiles * p.split_k
-        if p.split_k > 1:
-            # k-splits whole 128-wide k-steps, at least two per split
-            assert d.k_steps // p.split_k >= 2
-            # split-K is only used when no tile alone fills the compute units
-            for t in range(nmspmm.num_tiles()):
-                a, b = nmspmm.tile_info(t)
-                assert -(-n // a) * -(-m // b) < CUS
-            assert nmspmm.workspace_size(p, m, n) >= p.split_k * m * n * 4
+        if "k_gemm_rs" in nmspmm.plan_kernel_name(p):
+            # row-stationary: a fixed grid, each workgroup walking several tiles
+            assert 0 < p.grid <= tiles and p.grid % CUS == 0
         else:
-            assert nmspmm.workspace_size(p, m, n) == 0
+            assert p.grid == tiles * p.split_k
+        # the reduction is split inside workgroups, never across them
+        assert p.split_k == 1 and nmspmm.workspace_size(p, m, n) == 0
         # deterministic
         q = nmspmm.spmm_plan(d, m, out)
         assert q.as_dict() == p.as_dict()
         dp = nmspmm.dense_plan(m, n, k, out)
-        assert dp.kind == nmspmm.NM_KIND_DENSE and dp.tile == p.tile and dp.split_k == p.split_k
+        assert dp.kind == nmspmm.NM_KIND_DENSE and dp.split_k == 1
 
 
-def test_small_m_fills_the_gpu_when_possible():
-    # DeiT-Base fc1 at batch 1: 197 tokens x 3072 channels, k = 768 (6 k-steps)
-    d = nmspmm.compress_size(3072, 768, 2, 4)
-    p = nmspmm.spmm_plan(d, 197, nmspmm.NM_OUT_I32)
-    assert p.grid >= CUS
-    # fc2 at batch 1: 768 channels, k = 3072 (24 k-steps) needs split-K
+def test_small_token_counts_split_the_reduction_inside_workgroups():
+    # DeiT-Base fc2 at batch 1: 197 tokens x 768 channels, k = 3072 (24 k-steps):
+    # 64 x 64 tiles would leave 208 of 256 compute units idle, so the planner
+    # takes the k-sliced 32 x 32 tile (the four waves split the reduction)
     d = nmspmm.compress_size(768, 3072, 2, 4)
     p = nmspmm.spmm_plan(d, 197, nmspmm.NM_OUT_I32)
-    assert p.split_k > 1 and p.grid >= CUS
+    assert (p.tile_n, p.tile_m) == (32, 32) and p.split_k == 1 and p.grid >= 128
+    # ... but not when k is too short for four slices (DeiT-Tiny fc1, k = 192)
+    d = nmspmm.compress_size(768, 192, 2, 4)
+    p = nmspmm.spmm_plan(d, 197, nmspmm.NM_OUT_I32)
+    assert (p.tile_n, p.tile_m) == (64, 64)
+
+
+def test_large_shapes_use_large_tiles():
+    d = nmspmm.compress_size(3072, 768, 2, 4)
+    p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # DeiT-Base fc1 at batch 128
+    assert nmspmm.plan_kernel_name(p).startswith("k_gemm_rs")   # X resident, weight streamed
+    d = nmspmm.compress_size(4096, 1024, 4, 8)
+    p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)    # ViT-L fc1, two-stream weight
+    assert (p.tile_n, p.tile_m) == (256, 256)
+    d = nmspmm.compress_size(768, 3072, 2, 4)
+    p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # fc2 at batch 128
+    assert (p.tile_n, p.tile_m) == (128, 128)
 
 
 def test_forced_plan_validation():
