@@ -11,6 +11,8 @@ library.  Functions follow the paper's definitions:
 * ``spmm_packed``         -- the product evaluated from the packed form (Sec. 4.2)
 * ``matmul_i8``           -- the plain product Y = X W^T (its definition)
 * ``dequant_f16`` / ``f64_to_f16`` -- per-channel dequantisation, one rounding
+* ``quantize_f16`` / ``requant_i8`` / ``f16_to_f32`` -- int8 quantisation on
+  either side of a linear in INT8 deployment (Sec. 6.3), decided in binary32
 """
 import ctypes
 import os
@@ -55,8 +57,13 @@ def _load():
     lib.orc_f64_to_f16.restype = ctypes.c_uint16
     lib.orc_f64_to_f16_array.argtypes = [_f64p, ctypes.c_int64, _u16p]
     lib.orc_dequant_f16.argtypes = [_i32p, _f32p, c_int, c_int, _u16p]
+    lib.orc_f16_to_f32.argtypes = [ctypes.c_uint16]
+    lib.orc_f16_to_f32.restype = ctypes.c_float
+    lib.orc_quantize_f16.argtypes = [_u16p, ctypes.c_int64, ctypes.c_float, _i8p]
+    lib.orc_requant_i8.argtypes = [_i32p, _f32p, c_int, c_int, _i8p]
     for f in (lib.orc_nm_check, lib.orc_pack_logical, lib.orc_unpack_logical, lib.orc_matmul_i8,
-              lib.orc_matmul_i8_sampled, lib.orc_spmm_packed, lib.orc_dequant_f16):
+              lib.orc_matmul_i8_sampled, lib.orc_spmm_packed, lib.orc_dequant_f16, lib.orc_quantize_f16,
+              lib.orc_requant_i8):
         f.restype = c_int
     _lib = lib
     return lib
@@ -170,4 +177,30 @@ def dequant_f16(Y, scale):
     out = np.zeros((m, n), np.uint16)
     _check(_load().orc_dequant_f16(_ptr(Y, _i32p), _ptr(scale, _f32p), m, n, _ptr(out, _u16p)),
            "dequant_f16")
+    return out
+
+
+def f16_to_f32(bits):
+    """binary32 values of binary16 bit patterns (exact)."""
+    bits = np.asarray(bits, np.uint16).ravel()
+    return np.array([_load().orc_f16_to_f32(int(b)) for b in bits], np.float32)
+
+
+def quantize_f16(xbits, inv_scale):
+    """int8 codes of binary16 activations: q8(f32(x) * inv_scale), decided in binary32."""
+    xbits = _c(np.asarray(xbits), np.uint16)
+    out = np.zeros(xbits.shape, np.int8)
+    _check(_load().orc_quantize_f16(_ptr(xbits, _u16p), xbits.size, ctypes.c_float(inv_scale),
+                                    _ptr(out, _i8p)), "quantize_f16")
+    return out
+
+
+def requant_i8(Y, qscale):
+    """int8 codes q8(f32(Y[i, j]) * qscale[j]), decided in binary32."""
+    Y = _c(Y, np.int32)
+    qscale = _c(np.asarray(qscale), np.float32)
+    m, n = Y.shape
+    out = np.zeros((m, n), np.int8)
+    _check(_load().orc_requant_i8(_ptr(Y, _i32p), _ptr(qscale, _f32p), m, n, _ptr(out, _i8p)),
+           "requant_i8")
     return out

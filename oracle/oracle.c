@@ -302,3 +302,60 @@ int orc_dequant_f16(const int32_t *Y, const float *scale, int m, int n, uint16_t
             Yh[i * n + j] = orc_f64_to_f16((double)Y[i * n + j] * (double)scale[j]);
     return ORC_OK;
 }
+
+/* ---- int8 quantisation on either side of a linear ------------------------
+ * The paper deploys the linears in INT8 end to end (Sec. 6.3) without
+ * spelling out the quantiser.  Reading used here: symmetric and saturating to
+ * [-127, 127]; the scale is a binary32 multiplier; the product is rounded to
+ * the nearest integer, ties to even, in binary32; NaN quantises to 0.  The
+ * code of a value is decided in binary32 because that is the precision the
+ * GPU kernels use, so both sides take the same decision. */
+static int8_t orc_q8_of(float v)
+{
+    if (isnan(v)) return 0;
+    float r = nearbyintf(v);   /* default rounding mode: nearest, ties to even */
+    if (r > 127.0f) r = 127.0f;
+    if (r < -127.0f) r = -127.0f;
+    return (int8_t)r;
+}
+
+/* binary16 bit pattern -> binary32 value (exact): sign, 5-bit exponent with
+ * bias 15, 10-bit fraction; exponent 0 holds subnormals f * 2^-24, exponent 31
+ * holds infinities (f = 0) and NaNs. */
+float orc_f16_to_f32(uint16_t h)
+{
+    int s = h >> 15, e = (h >> 10) & 31, f = h & 1023;
+    float mag;
+    if (e == 31) mag = f ? NAN : INFINITY;
+    else if (e == 0) mag = ldexpf((float)f, -24);
+    else mag = ldexpf((float)(f + 1024), e - 25);   /* (1 + f/1024) * 2^(e-15) */
+    return s ? -mag : mag;
+}
+
+/* Activation quantisation (prologue of the first linear):
+ * xq[c] = q8( f32(x[c]) * inv_scale ), x given as binary16 bit patterns. */
+int orc_quantize_f16(const uint16_t *x, int64_t count, float inv_scale, int8_t *xq)
+{
+    if ((!x || !xq) && count > 0) return ORC_ERR_ARG;
+    for (int64_t c = 0; c < count; ++c) {
+        float v = orc_f16_to_f32(x[c]) * inv_scale;
+        xq[c] = orc_q8_of(v);
+    }
+    return ORC_OK;
+}
+
+/* Requantisation epilogue (int32 accumulator -> int8 input of the next
+ * linear): Yq[i][j] = q8( f32(Y[i][j]) * qscale[j] ).  f32(Y) rounds to
+ * nearest-even when |Y| > 2^24.  A per-tensor requantisation is the case of
+ * equal qscale entries; with per-channel weight scales the multiplier
+ * s_x * s_w[j] / s_y is per channel anyway. */
+int orc_requant_i8(const int32_t *Y, const float *qscale, int m, int n, int8_t *Yq)
+{
+    if (!Y || !qscale || !Yq || m < 0 || n < 0) return ORC_ERR_ARG;
+    for (int64_t i = 0; i < m; ++i)
+        for (int64_t j = 0; j < n; ++j) {
+            float v = (float)Y[i * n + j] * qscale[j];
+            Yq[i * n + j] = orc_q8_of(v);
+        }
+    return ORC_OK;
+}

@@ -5,7 +5,10 @@
 * the packed form against hand-worked examples (tests/golden), the round trip,
   the canonical-form invariants and brute-force window counts;
 * the binary16 rounding exhaustively against the format's own grid
-  (every half value and every midpoint) and against NumPy's converter.
+  (every half value and every midpoint) and against NumPy's converter;
+* the int8 quantiser and requantiser against hand-worked codes (ties, saturation,
+  NaN, infinities) and against NumPy's IEEE binary32 arithmetic on every
+  binary16 input.
 """
 import os
 
@@ -305,3 +308,61 @@ def test_dequant_matches_numpy():
     sc = (rng.uniform(1e-7, 1e-4, 33)).astype(np.float32)
     want = (Y.astype(np.float64) * sc.astype(np.float64)[None, :]).astype(np.float16).view(np.uint16)
     assert np.array_equal(oracle.dequant_f16(Y, sc), want)
+
+
+# ---------------------------------------------------------------- int8 (re)quantisation
+
+def np_q8(v32):
+    """Reference codes from NumPy's IEEE binary32 values: nearest-even, clamp, NaN -> 0."""
+    with np.errstate(invalid="ignore"):
+        r = np.rint(v32)
+    r = np.where(np.isnan(r), 0, np.clip(r, -127, 127))
+    return r.astype(np.int8)
+
+
+def test_f16_decode_every_pattern_matches_numpy():
+    bits = np.arange(65536, dtype=np.uint16)
+    ref = bits.view(np.float16).astype(np.float32)
+    got = oracle.f16_to_f32(bits)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan].view(np.uint32), ref[~nan].view(np.uint32))   # signed zeros too
+
+
+@pytest.mark.parametrize("inv_scale", [1.0, 0.37, 128.0, 3.0e-3, 1.0e4])
+def test_quantize_every_half_matches_numpy(inv_scale):
+    bits = np.arange(65536, dtype=np.uint16)
+    with np.errstate(invalid="ignore"):
+        ref = np_q8(bits.view(np.float16).astype(np.float32) * np.float32(inv_scale))
+    assert np.array_equal(oracle.quantize_f16(bits, inv_scale), ref)
+
+
+def test_quantize_hand_worked_codes():
+    vals = [0.5, 1.5, 2.5, -0.5, -1.5, -2.5, 126.5, 127.4, 200.0, -300.0, np.inf, -np.inf, np.nan, 0.0, -0.0, 3.25]
+    want = [0, 2, 2, 0, -2, -2, 126, 127, 127, -127, 127, -127, 0, 0, 0, 3]
+    bits = np.array(vals, np.float16).view(np.uint16)
+    assert oracle.quantize_f16(bits, 1.0).tolist() == want
+    # the multiplier is applied before rounding: 3 * 0.5 = 1.5 -> 2, 5 * 0.5 = 2.5 -> 2
+    assert oracle.quantize_f16(np.array([3.0, 5.0, -7.0], np.float16).view(np.uint16), 0.5).tolist() == [2, 2, -4]
+
+
+def test_requant_hand_worked_codes():
+    Y = np.array([[0, 1, -1, 127, -127, 128, -128, 100000],
+                  [3, 5, -3, -5, 7, 254, 255, -2 ** 31]], np.int32)
+    got_1 = oracle.requant_i8(Y, np.ones(8, np.float32))
+    assert got_1.tolist() == [[0, 1, -1, 127, -127, 127, -127, 127], [3, 5, -3, -5, 7, 127, 127, -127]]
+    half = np.full(8, 0.5, np.float32)
+    assert oracle.requant_i8(Y, half)[1].tolist() == [2, 2, -2, -2, 4, 127, 127, -127]
+    per_ch = np.array([1, 1, 1, 0.5, 0.5, 0.25, 0.25, 1e-6], np.float32)
+    assert oracle.requant_i8(Y, per_ch)[0].tolist() == [0, 1, -1, 64, -64, 32, -32, 0]
+
+
+def test_requant_matches_numpy():
+    rng = np.random.default_rng(11)
+    Y = rng.integers(-2 ** 31, 2 ** 31, (37, 64), dtype=np.int64).astype(np.int32)
+    Y[:, :16] = rng.integers(-40000, 40000, (37, 16))
+    Y[:, 16:20] = rng.integers(2 ** 24 - 8, 2 ** 24 + 8, (37, 4))      # int -> binary32 rounding region
+    q = np.exp(rng.uniform(np.log(1e-9), np.log(1e-2), 64)).astype(np.float32)
+    q[:4] = np.float32(2.0 ** -22)
+    ref = np_q8(Y.astype(np.float32) * q[None, :])
+    assert np.array_equal(oracle.requant_i8(Y, q), ref)
