@@ -7,6 +7,7 @@
  *
  *     Y[i][j] = sum_t X[i][t] * W[j][t]          (exact, int32)
  *     Yh[i][j] = fp16( fp32(Y[i][j]) * scale[j] ) (optional dequantisation)
+ *     Yq[i][j] = q8( fp32(Y[i][j]) * qscale[j] )  (optional requantisation)
  *
  * X is int8 [m x k] row-major (m tokens, k = in_features), W is int8 [n x k]
  * row-major (n = out_features, the layout of a PyTorch Linear weight) with at
@@ -51,6 +52,7 @@ typedef enum nm_status {
 /* Output selection bits (used by the planners and workspace queries). */
 #define NM_OUT_I32 1
 #define NM_OUT_F16 2
+#define NM_OUT_I8 4
 
 /* Physical layout of the packed weight produced by nm_compress. */
 #define NM_LAYOUT_SP42 1
@@ -215,6 +217,53 @@ nm_status nm_gemm_i8_dense(const int8_t *X, int m, const int8_t *W, int n, int k
 nm_status nm_gemm_i8_dense_ex(const int8_t *X, int m, const int8_t *W, int n, int k,
                               int32_t *Y, const float *scale, uint16_t *Yh,
                               void *ws, size_t ws_bytes, void *stream, const nm_plan *plan);
+
+/* ---------------------------------------------------------------- INT8 chaining
+ * The paper deploys the linears in INT8 end to end (Sec. 6.3).  Between two
+ * linears the int32 result must become the next linear's int8 input; the
+ * entry points below do that inside the GEMM's epilogue (requantisation) and,
+ * for the first linear, on binary16 activations (quantisation).
+ *
+ * q8(v): the binary32 value v rounded to the nearest integer, ties to even,
+ * saturated to [-127, 127]; NaN gives 0.  Products are rounded to binary32
+ * before q8, so a code is decided in binary32.  Symmetric per-tensor
+ * quantisation of the next input with scale s_y is qscale[j] = s_x * s_w[j] /
+ * s_y (per channel because the weight scales are). */
+
+/* Outputs of one GEMM: any non-empty subset.
+ *   y       device int32 [m x n]  Y = X W^T
+ *   yh      device binary16 [m x n] fp16(fp32(Y) * scale[j]), needs scale
+ *   scale   device float32 [n]
+ *   yq      device int8 [m x n]  q8(fp32(Y) * qscale[j]), needs qscale
+ *   qscale  device float32 [n]
+ * Every non-NULL pointer must be 16-byte aligned. */
+typedef struct nm_outputs {
+    int32_t *y;
+    uint16_t *yh;
+    const float *scale;
+    int8_t *yq;
+    const float *qscale;
+} nm_outputs;
+
+/* nm_spmm_ex with the outputs given by `out` (host struct, read during the
+ * call).  plan may be NULL.  Errors as nm_spmm_ex; NM_ERR_ARG also for
+ * out == NULL, no output, or an output without its multiplier array. */
+nm_status nm_spmm_out(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
+                      const nm_desc *desc, const nm_outputs *out,
+                      void *ws, size_t ws_bytes, void *stream, const nm_plan *plan);
+
+/* nm_gemm_i8_dense_ex with the outputs given by `out`. */
+nm_status nm_gemm_i8_dense_out(const int8_t *X, int m, const int8_t *W, int n, int k,
+                               const nm_outputs *out,
+                               void *ws, size_t ws_bytes, void *stream, const nm_plan *plan);
+
+/* Quantisation of binary16 activations: xq[c] = q8(fp32(x[c]) * inv_scale)
+ * for 0 <= c < count (a per-tensor scale s_x gives inv_scale = 1 / s_x).
+ * x: device binary16 bits, xq: device int8, both 16-byte aligned; count == 0
+ * is a no-op (no pointer examined).  Asynchronous on `stream`.  Errors:
+ * NM_ERR_SHAPE (count < 0), NM_ERR_ARG (NULL or misaligned pointer),
+ * NM_ERR_HIP. */
+nm_status nm_quantize_f16(const uint16_t *x, int64_t count, float inv_scale, int8_t *xq, void *stream);
 
 #ifdef __cplusplus
 }

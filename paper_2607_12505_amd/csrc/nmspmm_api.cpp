@@ -12,20 +12,33 @@ namespace {
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
-int out_mode_of(const int32_t *Y, const uint16_t *Yh) {
-    return (Y ? NM_OUT_I32 : 0) | (Yh ? NM_OUT_F16 : 0);
+int out_mode_of(const nm_outputs &o) {
+    return (o.y ? NM_OUT_I32 : 0) | (o.yh ? NM_OUT_F16 : 0) | (o.yq ? NM_OUT_I8 : 0);
+}
+
+nm_outputs outputs_of(int32_t *Y, const float *scale, uint16_t *Yh) {
+    nm_outputs o;
+    o.y = Y;
+    o.yh = Yh;
+    o.scale = scale;
+    o.yq = nullptr;
+    o.qscale = nullptr;
+    return o;
 }
 
 nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint8_t *meta, int n, int k,
-                   int k_steps, int n_frags, int32_t *Y, const float *scale, uint16_t *Yh, void *ws,
-                   size_t ws_bytes, void *stream, const nm_plan *forced) {
+                   int k_steps, int n_frags, const nm_outputs *out, void *ws, size_t ws_bytes, void *stream,
+                   const nm_plan *forced) {
     if (m < 0) return NM_ERR_SHAPE;
     if (m == 0) return NM_OK;  // nothing to compute; empty tensors may carry null pointers
+    if (!out) return NM_ERR_ARG;
+    const nm_outputs o = *out;
     if (!X || !A || (kind != NM_KIND_DENSE && !meta)) return NM_ERR_ARG;
-    if (!Y && !Yh) return NM_ERR_ARG;
-    if (Yh && !scale) return NM_ERR_ARG;
-    if (!aligned16(X) || !aligned16(A) || (meta && !aligned16(meta)) || (Y && !aligned16(Y)) ||
-        (Yh && !aligned16(Yh)) || (Yh && !aligned16(scale)))
+    if (!o.y && !o.yh && !o.yq) return NM_ERR_ARG;
+    if ((o.yh && !o.scale) || (o.yq && !o.qscale)) return NM_ERR_ARG;
+    if (!aligned16(X) || !aligned16(A) || (meta && !aligned16(meta)) || (o.y && !aligned16(o.y)) ||
+        (o.yh && !aligned16(o.yh)) || (o.yh && !aligned16(o.scale)) || (o.yq && !aligned16(o.yq)) ||
+        (o.yq && !aligned16(o.qscale)))
         return NM_ERR_ARG;
     if ((int64_t)m * n > ((int64_t)1 << 40)) return NM_ERR_SHAPE;
     nm_plan plan;
@@ -34,7 +47,7 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
         nm_status st = complete_plan(kind, m, n, k_steps, &plan);
         if (st != NM_OK) return st;
     } else {
-        nm_status st = make_plan(kind, m, n, k_steps, out_mode_of(Y, Yh), &plan);
+        nm_status st = make_plan(kind, m, n, k_steps, out_mode_of(o), &plan);
         if (st != NM_OK) return st;
     }
     const int tiles = plan.grid / plan.split_k;
@@ -45,9 +58,11 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
     a.X = X;
     a.A = A;
     a.meta = meta;
-    a.Y = Y;
-    a.Yh = Yh;
-    a.scale = scale;
+    a.Y = o.y;
+    a.Yh = o.yh;
+    a.scale = o.scale;
+    a.Yq = o.yq;
+    a.qscale = o.qscale;
     a.counters = need ? (int32_t *)ws : nullptr;
     a.partials = need ? (int32_t *)((char *)ws + kCounterBytes) : nullptr;
     a.m = m;
@@ -137,13 +152,20 @@ extern "C" nm_status nm_workspace_init(void *ws, size_t bytes, void *stream) {
     return launch_zero(ws, bytes, stream) == 0 ? NM_OK : NM_ERR_HIP;
 }
 
+extern "C" nm_status nm_spmm_out(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
+                                 const nm_desc *desc, const nm_outputs *out, void *ws, size_t ws_bytes, void *stream,
+                                 const nm_plan *plan) {
+    nm_status st = check_desc(desc);
+    if (st != NM_OK) return st;
+    return run_gemm(kind_of(desc), X, m, vals, meta, desc->n, desc->k, desc->k_steps, desc->n_frags, out, ws,
+                    ws_bytes, stream, plan);
+}
+
 extern "C" nm_status nm_spmm_ex(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
                                 const nm_desc *desc, int32_t *Y, const float *scale, uint16_t *Yh,
                                 void *ws, size_t ws_bytes, void *stream, const nm_plan *plan) {
-    nm_status st = check_desc(desc);
-    if (st != NM_OK) return st;
-    return run_gemm(kind_of(desc), X, m, vals, meta, desc->n, desc->k, desc->k_steps, desc->n_frags, Y, scale,
-                    Yh, ws, ws_bytes, stream, plan);
+    const nm_outputs o = outputs_of(Y, scale, Yh);
+    return nm_spmm_out(X, m, vals, meta, desc, &o, ws, ws_bytes, stream, plan);
 }
 
 extern "C" nm_status nm_spmm(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
@@ -152,18 +174,32 @@ extern "C" nm_status nm_spmm(const int8_t *X, int m, const int8_t *vals, const u
     return nm_spmm_ex(X, m, vals, meta, desc, Y, scale, Yh, ws, ws_bytes, stream, nullptr);
 }
 
-extern "C" nm_status nm_gemm_i8_dense_ex(const int8_t *X, int m, const int8_t *W, int n, int k,
-                                         int32_t *Y, const float *scale, uint16_t *Yh,
-                                         void *ws, size_t ws_bytes, void *stream, const nm_plan *plan) {
+extern "C" nm_status nm_gemm_i8_dense_out(const int8_t *X, int m, const int8_t *W, int n, int k,
+                                          const nm_outputs *out, void *ws, size_t ws_bytes, void *stream,
+                                          const nm_plan *plan) {
     if (n < 1 || k < 1) return NM_ERR_ARG;
     if (k % 16 != 0 || n % 4 != 0) return NM_ERR_SHAPE;
     const int k_steps = (k + kKStep - 1) / kKStep;
-    return run_gemm(NM_KIND_DENSE, X, m, W, nullptr, n, k, k_steps, (n + kFragRows - 1) / kFragRows, Y, scale,
-                    Yh, ws, ws_bytes, stream, plan);
+    return run_gemm(NM_KIND_DENSE, X, m, W, nullptr, n, k, k_steps, (n + kFragRows - 1) / kFragRows, out, ws,
+                    ws_bytes, stream, plan);
+}
+
+extern "C" nm_status nm_gemm_i8_dense_ex(const int8_t *X, int m, const int8_t *W, int n, int k,
+                                         int32_t *Y, const float *scale, uint16_t *Yh,
+                                         void *ws, size_t ws_bytes, void *stream, const nm_plan *plan) {
+    const nm_outputs o = outputs_of(Y, scale, Yh);
+    return nm_gemm_i8_dense_out(X, m, W, n, k, &o, ws, ws_bytes, stream, plan);
 }
 
 extern "C" nm_status nm_gemm_i8_dense(const int8_t *X, int m, const int8_t *W, int n, int k,
                                       int32_t *Y, const float *scale, uint16_t *Yh,
                                       void *ws, size_t ws_bytes, void *stream) {
     return nm_gemm_i8_dense_ex(X, m, W, n, k, Y, scale, Yh, ws, ws_bytes, stream, nullptr);
+}
+
+extern "C" nm_status nm_quantize_f16(const uint16_t *x, int64_t count, float inv_scale, int8_t *xq, void *stream) {
+    if (count < 0) return NM_ERR_SHAPE;
+    if (count == 0) return NM_OK;
+    if (!x || !xq || !aligned16(x) || !aligned16(xq)) return NM_ERR_ARG;
+    return launch_quantize_f16(x, count, inv_scale, xq, stream) == 0 ? NM_OK : NM_ERR_HIP;
 }

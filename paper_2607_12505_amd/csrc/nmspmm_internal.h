@@ -82,6 +82,8 @@ struct GemmArgs {
     int32_t *Y;             // [m x n] or null
     uint16_t *Yh;           // [m x n] or null
     const float *scale;     // [n] (needed with Yh)
+    int8_t *Yq;             // [m x n] or null
+    const float *qscale;    // [n] (needed with Yq)
     int32_t *counters;      // one per output tile (split_k > 1)
     int32_t *partials;      // [split_k x m x n] (split_k > 1)
     int m, n, k;
@@ -102,6 +104,7 @@ int device_cu_count();     // cached per device; 256 when no device is visible
 // Launches the kernel of (kind, tile) on the stream.  Returns a hipError_t value.
 int launch_gemm(int kind, int tile, const GemmArgs &args, int grid, void *stream);
 int launch_zero(void *ptr, size_t bytes, void *stream);
+int launch_quantize_f16(const uint16_t *x, int64_t count, float inv_scale, int8_t *xq, void *stream);
 
 // Planner shared by both GEMM families.
 nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *plan);

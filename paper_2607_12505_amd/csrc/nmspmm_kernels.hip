@@ -121,24 +121,48 @@ __device__ inline void wait_later_then_barrier(int later) {
     }
 }
 
-// Writes 4 consecutive channels of one token: int32 and/or fp16(fp32(y) * scale).
-__device__ inline void emit_out(const GemmArgs &a, int tok, int ch, const v4i &v, const v4f &sc) {
+// int8 code of a binary32 value: nearest integer (ties to even), saturated
+// to [-127, 127], NaN -> 0.
+__device__ inline int q8(float v) {
+    if (v != v) return 0;
+    const float r = __builtin_rintf(v);
+    return (int)fminf(fmaxf(r, -127.0f), 127.0f);
+}
+
+// Per-channel multipliers of the epilogue outputs for 4 consecutive channels.
+struct EpiScale {
+    v4f sc;   // dequantisation (fp16 output)
+    v4f qs;   // requantisation (int8 output)
+};
+
+// Writes 4 consecutive channels of one token: int32, fp16(fp32(y) * scale)
+// and/or the int8 code q8(fp32(y) * qscale), whichever outputs are present.
+__device__ inline void emit_out(const GemmArgs &a, int tok, int ch, const v4i &v, const EpiScale &es) {
     if (a.Y) *(v4i *)(a.Y + (size_t)tok * a.n + ch) = v;
     if (a.Yh) {
         v4u16 h;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const _Float16 x = (_Float16)((float)v[e] * sc[e]);
+            const _Float16 x = (_Float16)((float)v[e] * es.sc[e]);
             h[e] = __builtin_bit_cast(unsigned short, x);
         }
         *(v4u16 *)(a.Yh + (size_t)tok * a.n + ch) = h;
     }
+    if (a.Yq) {
+        uint32_t packed = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) packed |= (uint32_t)(q8((float)v[e] * es.qs[e]) & 0xFF) << (8 * e);
+        *(uint32_t *)(a.Yq + (size_t)tok * a.n + ch) = packed;
+    }
 }
 
-__device__ inline v4f load_scale(const GemmArgs &a, int ch) {
-    v4f sc = {0.f, 0.f, 0.f, 0.f};
-    if (a.Yh && ch < a.n) sc = *(const v4f *)(a.scale + ch);
-    return sc;
+__device__ inline EpiScale load_scale(const GemmArgs &a, int ch) {
+    EpiScale es;
+    es.sc = v4f{0.f, 0.f, 0.f, 0.f};
+    es.qs = v4f{0.f, 0.f, 0.f, 0.f};
+    if (a.Yh && ch < a.n) es.sc = *(const v4f *)(a.scale + ch);
+    if (a.Yq && ch < a.n) es.qs = *(const v4f *)(a.qscale + ch);
+    return es;
 }
 
 // Split-K partial sums: [split_k x m x n] int32 below 2 GiB (checked by the
@@ -357,7 +381,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     const int er = lane / G::CPR;                     // row offset within a read group
     const int ch = ch0 + wn * FN * 16 + ec * 4;       // first of the lane's 4 channels
     const bool ch_ok = ch < a.n;
-    const v4f sc = load_scale(a, ch);
+    const EpiScale sc = load_scale(a, ch);
     const __amdgpu_buffer_rsrc_t prsrc = partial_rsrc(a);
 
 #pragma unroll
@@ -722,7 +746,7 @@ __global__ __launch_bounds__(320) void k_gemm_rs(GemmArgs a) {
     auto epilogue = [&](int tm, int tn) {
         const int ch = tn * BN + wn * FN * 16 + ec * 4;
         const bool ch_ok = ch < a.n;
-        const v4f sc = load_scale(a, ch);
+        const EpiScale sc = load_scale(a, ch);
 #pragma unroll
         for (int j = 0; j < FM; ++j) {
 #pragma unroll
@@ -830,6 +854,50 @@ int launch_gemm(int kind, int tile, const GemmArgs &args, int grid, void *stream
         case NM_KIND_DENSE: return launch_kind<NM_KIND_DENSE>(tile, args, grid, stream);
     }
     return (int)hipErrorInvalidValue;
+}
+
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+
+// Activation quantisation: xq[c] = q8(fp32(x[c]) * inv_scale).  Each thread
+// turns 16 binary16 values (two 16-byte loads) into one 16-byte store; the
+// count % 16 tail is done one element per thread by block 0.
+__global__ __launch_bounds__(256) void k_quantize_f16(const uint16_t *__restrict__ x, size_t chunks,
+                                                      float inv_scale, int8_t *__restrict__ xq, int tail) {
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < chunks; i += stride) {
+        const v4i lo = *(const v4i *)(x + 16 * i);
+        const v4i hi = *(const v4i *)(x + 16 * i + 8);
+        const v8h hl = __builtin_bit_cast(v8h, lo), hh = __builtin_bit_cast(v8h, hi);
+        v4i out;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            uint32_t packed = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int idx = 4 * w + e;
+                const float v = (float)(idx < 8 ? hl[idx & 7] : hh[idx & 7]) * inv_scale;
+                packed |= (uint32_t)(q8(v) & 0xFF) << (8 * e);
+            }
+            out[w] = (int)packed;
+        }
+        *(v4i *)(xq + 16 * i) = out;
+    }
+    if (blockIdx.x == 0 && (int)threadIdx.x < tail) {
+        const size_t c = 16 * chunks + threadIdx.x;
+        const float v = (float)__builtin_bit_cast(_Float16, x[c]) * inv_scale;
+        xq[c] = (int8_t)q8(v);
+    }
+}
+
+int launch_quantize_f16(const uint16_t *x, int64_t count, float inv_scale, int8_t *xq, void *stream) {
+    const size_t chunks = (size_t)count / 16;
+    const int tail = (int)(count % 16);
+    size_t blocks = (chunks + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(k_quantize_f16, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, x, chunks,
+                       inv_scale, xq, tail);
+    return (int)hipGetLastError();
 }
 
 int launch_zero(void *ptr, size_t bytes, void *stream) {

@@ -90,7 +90,7 @@ static int64_t tiles_of(int t, int m, int n) {
 
 nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *plan) {
     if (!plan || m < 0 || n < 1 || k_steps < 1) return NM_ERR_ARG;
-    if ((out_mode & (NM_OUT_I32 | NM_OUT_F16)) == 0) return NM_ERR_ARG;
+    if ((out_mode & (NM_OUT_I32 | NM_OUT_F16 | NM_OUT_I8)) == 0) return NM_ERR_ARG;
     const int64_t cus = device_cu_count();
     const int mm = m > 0 ? m : 1;
     // Operands twice as heavy per k-step: dense weights and two 4:2 streams.

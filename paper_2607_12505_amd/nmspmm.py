@@ -19,7 +19,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libnmspmm.so")
 
 NM_OK, NM_ERR_ARG, NM_ERR_SHAPE, NM_ERR_PATTERN, NM_ERR_UNSUPPORTED, NM_ERR_WORKSPACE, NM_ERR_HIP = range(7)
-NM_OUT_I32, NM_OUT_F16 = 1, 2
+NM_OUT_I32, NM_OUT_F16, NM_OUT_I8 = 1, 2, 4
 NM_KIND_SP42, NM_KIND_SP42X2, NM_KIND_DENSE = 1, 2, 3
 NM_LAYOUT_SP42 = 1
 
@@ -27,7 +27,8 @@ NM_LAYOUT_SP42 = 1
 EXPORTED = (
     "nm_status_string", "nm_compress_size", "nm_compress", "nm_decompress", "nm_num_tiles",
     "nm_tile_info", "nm_plan_kernel_name", "nm_spmm_plan", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
-    "nm_spmm", "nm_spmm_ex", "nm_gemm_i8_dense", "nm_gemm_i8_dense_ex",
+    "nm_spmm", "nm_spmm_ex", "nm_gemm_i8_dense", "nm_gemm_i8_dense_ex", "nm_spmm_out", "nm_gemm_i8_dense_out",
+    "nm_quantize_f16",
 )
 
 
@@ -44,6 +45,11 @@ class NmPlan(ctypes.Structure):
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+class NmOutputs(ctypes.Structure):
+    _fields_ = [("y", ctypes.c_void_p), ("yh", ctypes.c_void_p), ("scale", ctypes.c_void_p),
+                ("yq", ctypes.c_void_p), ("qscale", ctypes.c_void_p)]
 
 
 class NmError(RuntimeError):
@@ -85,6 +91,9 @@ def lib() -> ctypes.CDLL:
             "nm_spmm_ex": ([vp, i32, vp, vp, pd, vp, vp, vp, vp, sz, vp, pp], i32),
             "nm_gemm_i8_dense": ([vp, i32, vp, i32, i32, vp, vp, vp, vp, sz, vp], i32),
             "nm_gemm_i8_dense_ex": ([vp, i32, vp, i32, i32, vp, vp, vp, vp, sz, vp, pp], i32),
+            "nm_spmm_out": ([vp, i32, vp, vp, pd, ctypes.POINTER(NmOutputs), vp, sz, vp, pp], i32),
+            "nm_gemm_i8_dense_out": ([vp, i32, vp, i32, i32, ctypes.POINTER(NmOutputs), vp, sz, vp, pp], i32),
+            "nm_quantize_f16": ([vp, ctypes.c_int64, ctypes.c_float, vp, vp], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -245,40 +254,75 @@ class DeviceWeight:
         return cls(v, m, p.desc)
 
 
+def _outputs(Y, scale, Yh, Yq, qscale) -> NmOutputs:
+    return NmOutputs(_ptr(Y), _ptr(Yh), _ptr(scale), _ptr(Yq), _ptr(qscale))
+
+
+def _out_mode(Y, Yh, Yq) -> int:
+    mode = (NM_OUT_I32 if Y is not None else 0) | (NM_OUT_F16 if Yh is not None else 0)
+    return mode | (NM_OUT_I8 if Yq is not None else 0)
+
+
 def spmm(X, w: DeviceWeight, Y=None, scale=None, Yh=None, plan: Optional[NmPlan] = None, ws=None,
-         stream=None):
-    """nm_spmm / nm_spmm_ex on torch device tensors.  Y (int32) and Yh (float16 or
-    int16 view of binary16) are written in place; returns (Y, Yh)."""
+         stream=None, Yq=None, qscale=None):
+    """Sparse GEMM on torch device tensors.  Y (int32), Yh (float16, or int16
+    view of binary16) and Yq (int8) are written in place; returns (Y, Yh), or
+    (Y, Yh, Yq) when Yq is given.  Without Yq this calls nm_spmm_ex, with it
+    nm_spmm_out."""
     m = X.shape[0]
-    out_mode = (NM_OUT_I32 if Y is not None else 0) | (NM_OUT_F16 if Yh is not None else 0)
-    p = plan if plan is not None else spmm_plan(w.desc, m, out_mode or NM_OUT_I32)
+    mode = _out_mode(Y, Yh, Yq)
+    p = plan if plan is not None else spmm_plan(w.desc, m, mode or NM_OUT_I32)
     need = workspace_size(p, m, w.desc.n)
     if ws is None:
         ws, ws_bytes = _WS.get(need, X.device)
     else:
         ws_bytes = ws.numel() * ws.element_size()
-    st = lib().nm_spmm_ex(_ptr(X), m, _ptr(w.vals), _ptr(w.meta), ctypes.byref(w.desc), _ptr(Y), _ptr(scale),
-                          _ptr(Yh), _ptr(ws), ws_bytes, _stream(stream),
-                          ctypes.byref(plan) if plan is not None else None)
-    _check(st, "nm_spmm")
-    return Y, Yh
+    pl = ctypes.byref(plan) if plan is not None else None
+    if Yq is None and qscale is None:
+        st = lib().nm_spmm_ex(_ptr(X), m, _ptr(w.vals), _ptr(w.meta), ctypes.byref(w.desc), _ptr(Y), _ptr(scale),
+                              _ptr(Yh), _ptr(ws), ws_bytes, _stream(stream), pl)
+        _check(st, "nm_spmm")
+        return Y, Yh
+    o = _outputs(Y, scale, Yh, Yq, qscale)
+    st = lib().nm_spmm_out(_ptr(X), m, _ptr(w.vals), _ptr(w.meta), ctypes.byref(w.desc), ctypes.byref(o), _ptr(ws),
+                           ws_bytes, _stream(stream), pl)
+    _check(st, "nm_spmm_out")
+    return Y, Yh, Yq
 
 
-def gemm_i8_dense(X, W, Y=None, scale=None, Yh=None, plan: Optional[NmPlan] = None, ws=None, stream=None):
-    """nm_gemm_i8_dense / nm_gemm_i8_dense_ex on torch device tensors."""
+def gemm_i8_dense(X, W, Y=None, scale=None, Yh=None, plan: Optional[NmPlan] = None, ws=None, stream=None,
+                  Yq=None, qscale=None):
+    """Dense baseline GEMM (nm_gemm_i8_dense_ex, or nm_gemm_i8_dense_out when Yq is given)."""
     m, k = X.shape
     n = W.shape[0]
-    out_mode = (NM_OUT_I32 if Y is not None else 0) | (NM_OUT_F16 if Yh is not None else 0)
-    p = plan if plan is not None else dense_plan(m, n, k, out_mode or NM_OUT_I32)
+    mode = _out_mode(Y, Yh, Yq)
+    p = plan if plan is not None else dense_plan(m, n, k, mode or NM_OUT_I32)
     need = workspace_size(p, m, n)
     if ws is None:
         ws, ws_bytes = _WS.get(need, X.device)
     else:
         ws_bytes = ws.numel() * ws.element_size()
-    st = lib().nm_gemm_i8_dense_ex(_ptr(X), m, _ptr(W), n, k, _ptr(Y), _ptr(scale), _ptr(Yh), _ptr(ws), ws_bytes,
-                                   _stream(stream), ctypes.byref(plan) if plan is not None else None)
-    _check(st, "nm_gemm_i8_dense")
-    return Y, Yh
+    pl = ctypes.byref(plan) if plan is not None else None
+    if Yq is None and qscale is None:
+        st = lib().nm_gemm_i8_dense_ex(_ptr(X), m, _ptr(W), n, k, _ptr(Y), _ptr(scale), _ptr(Yh), _ptr(ws),
+                                       ws_bytes, _stream(stream), pl)
+        _check(st, "nm_gemm_i8_dense")
+        return Y, Yh
+    o = _outputs(Y, scale, Yh, Yq, qscale)
+    st = lib().nm_gemm_i8_dense_out(_ptr(X), m, _ptr(W), n, k, ctypes.byref(o), _ptr(ws), ws_bytes,
+                                    _stream(stream), pl)
+    _check(st, "nm_gemm_i8_dense_out")
+    return Y, Yh, Yq
+
+
+def quantize_f16(x, inv_scale: float, xq=None, stream=None):
+    """nm_quantize_f16: int8 codes of a float16 (or int16-bits) device tensor."""
+    torch = _torch()
+    if xq is None:
+        xq = torch.empty(x.shape, dtype=torch.int8, device=x.device)
+    _check(lib().nm_quantize_f16(_ptr(x), x.numel(), float(inv_scale), _ptr(xq), _stream(stream)),
+           "nm_quantize_f16")
+    return xq
 
 
 def workspace_init(ws, stream=None):
