@@ -1,22 +1,27 @@
 """The C ABI library loads on a host without a GPU and exports every symbol
-that include/nmspmm.h declares (no compute call is made here)."""
+that the headers under include/ declare (no GPU compute call is made here)."""
 import ctypes
+import glob
 import os
 import re
 
-from paper_2607_12505_amd import nmspmm
+from paper_2607_12505_amd import nmsearch, nmspmm
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "nmspmm.h")
+HEADERS = sorted(glob.glob(os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                                        "*.h")))
 
 
 def declared_functions():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(nm_[a-z0-9_]+)\s*\(", src)))
+    names = set()
+    for h in HEADERS:
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(nm_[a-z0-9_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_header_declares_the_binding_names():
-    assert declared_functions() == sorted(nmspmm.EXPORTED)
+    assert len(HEADERS) == 2
+    assert declared_functions() == sorted(nmspmm.EXPORTED + nmsearch.EXPORTED)
 
 
 def test_library_exports_every_declared_symbol():
@@ -36,3 +41,6 @@ def test_struct_sizes_match_header():
     # nm_desc: 8 int32 + 2 int64 + 2 int32 = 56 bytes; nm_plan: 6 int32
     assert ctypes.sizeof(nmspmm.NmDesc) == 56
     assert ctypes.sizeof(nmspmm.NmPlan) == 24
+    # nm_outputs: 5 pointers; nm_search_params: 4 int32 + 1 uint64
+    assert ctypes.sizeof(nmspmm.NmOutputs) == 40
+    assert ctypes.sizeof(nmsearch.NmSearchParams) == 24
