@@ -300,6 +300,251 @@ def sweep(configs, torch, reps, out_path):
     return summary
 
 
+def predictor_experiment(torch, n_cal, n_test, report):
+    """Latency predictor (Sec. 5.1) and search (Sec. 5.2) on ViT-L/16 at 384 px,
+    batch 32: the LUT of every (linear shape, N:8 pattern) from this library's
+    GEMMs (mean of repeated runs), whole-chain measurements of random layer-wise
+    configurations, the NNLS calibration of Eq. 1 on some of them and its
+    prediction error on the others; then Algorithm 1 on the calibrated
+    predictor with a synthetic accuracy stand-in, and the measured latency of
+    the configurations it returns."""
+    from paper_2607_12505_amd import latency as lt
+    from paper_2607_12505_amd import nmsearch
+    shapes = lt.vit_large_layer_shapes()
+    L = len(shapes)
+    pats = list(lt.FAMILY_N8) + [(1, 4), (2, 4)]
+    t0 = time.perf_counter()
+    cb = lt.ChainBench(torch, shapes, pats, nmspmm.NM_OUT_I32, seed=4)
+    log(f"prepared {len(cb.calls)} GEMMs in {time.perf_counter() - t0:.1f} s")
+    cb.lut(reps=3, cold=False)                       # warm-up pass
+    table, lut_s = cb.lut(reps=20, cold=True)
+    hot, _ = cb.lut(reps=20, cold=False)
+    log(f"LUT of {len(table)} entries built in {lut_s:.2f} s")
+    names = {(8, 8): "dense"}
+    pname = lambda p: names.get(p, f"{p[0]}:{p[1]}")
+    family = {}
+    for shape, lin in zip(shapes[:4], ("qkv", "proj", "fc1", "fc2")):
+        m, k, n = shape
+        dense_us = table[(shape, (8, 8))]
+        family[lin] = {"m": m, "k": k, "n": n, "patterns": {
+            pname(p): {"us": round(table[(shape, p)], 2),
+                       "tops": round(2.0 * m * n * k / (table[(shape, p)] * 1e-6) / 1e12, 1),
+                       "speedup_vs_dense": round(dense_us / table[(shape, p)], 3)} for p in pats}}
+    cal = lt.random_assignments(n_cal, L, lt.FAMILY_N8, seed=1)
+    test = lt.random_assignments(n_test, L, lt.FAMILY_N8, seed=2)
+    test += [[p] * L for p in lt.FAMILY_N8]            # the uniform configurations
+    test.append(wl.vit_large_assignment())            # the layer-wise draw of the ViT-L chain workload
+    t0 = time.perf_counter()
+    T_cal = np.array([cb.measure(a) for a in cal])
+    T_test = np.array([cb.measure(a) for a in test])
+    log(f"{len(cal) + len(test)} chains measured in {time.perf_counter() - t0:.1f} s")
+    luts = {"cold": table, "hot": hot}
+    R_cal = {k: np.array([cb.layer_times(t, a) for a in cal]) for k, t in luts.items()}
+    R_test = {k: np.array([cb.layer_times(t, a) for a in test]) for k, t in luts.items()}
+    kind = np.arange(L) % 4
+
+    def fit(R, T, structure):
+        """Eq. 1 by NNLS: one gamma per layer (as written), or one per linear
+        type shared by its 24 layers (4 + 1 unknowns: better posed when few
+        configurations are measured)."""
+        if structure == "layer":
+            return nmsearch.latency_fit(R, T)
+        g, b = nmsearch.latency_fit(np.stack([R[:, kind == j].sum(axis=1) for j in range(4)], axis=1), T)
+        return g[kind], b
+
+    def errors(gamma, b, R, T):
+        pred = np.array([nmsearch.latency_predict(r, gamma, b) for r in R])
+        e = np.abs(pred - T) / T
+        return {"mean_abs_pct": round(float(e.mean() * 100), 2), "max_abs_pct": round(float(e.max() * 100), 2),
+                "within_5pct": round(float((e <= 0.05).mean()), 3)}
+
+    fits = {}
+    for lk in ("cold", "hot"):
+        fits[f"{lk} LUT, sum without calibration"] = errors(np.ones(L), 0.0, R_test[lk], T_test)
+    for lk in ("cold", "hot"):
+        for structure in ("layer", "type"):
+            for K in sorted({8, 16, 32, len(cal)}):
+                if K <= len(cal):
+                    g, b = fit(R_cal[lk][:K], T_cal[:K], structure)
+                    fits[f"{lk} LUT, gamma per {structure}, {K} configs"] = errors(g, b, R_test[lk], T_test)
+    # the predictor the search uses: the variant with the smallest 4-fold
+    # cross-validated error on the calibration configurations alone
+    folds = np.arange(len(cal)) % 4
+    cv = {}
+    for lk in ("cold", "hot"):
+        for structure in ("layer", "type"):
+            errs = []
+            for f in range(4):
+                g, b = fit(R_cal[lk][folds != f], T_cal[folds != f], structure)
+                pred = np.array([nmsearch.latency_predict(r, g, b) for r in R_cal[lk][folds == f]])
+                errs += list(np.abs(pred - T_cal[folds == f]) / T_cal[folds == f])
+            cv[(lk, structure)] = float(np.mean(errs))
+    lut_kind, structure = min(cv, key=cv.get)
+    gamma, b = fit(R_cal[lut_kind], T_cal, structure)
+    chosen = {"lut": lut_kind, "gamma": structure, "cv_mean_abs_pct": round(cv[(lut_kind, structure)] * 100, 2),
+              "test": errors(gamma, b, R_test[lut_kind], T_test)}
+    table = luts[lut_kind]
+    log(json.dumps(fits))
+    log(json.dumps(chosen))
+
+    # Algorithm 1 on the calibrated predictor (largest calibration set)
+    lut8 = np.array([[table[(shape, (N, 8))] for N in range(1, 9)] for shape in shapes])
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([5, 5])))
+    sens = rng.uniform(0.05, 1.0, L)
+    acc_tab = [[float(sens[l] * np.log(N / 8.0)) for N in range(1, 9)] for l in range(L)]
+
+    def accuracy(cfg):
+        return sum(acc_tab[l][cfg[l] - 1] for l in range(L))
+
+    lo = nmsearch.latency_predict(lut8[:, 0], gamma, b)
+    hi = nmsearch.latency_predict(lut8[:, 7], gamma, b)
+    searches = []
+    for f in (0.3, 0.6, 0.9):
+        target_speedup = 1.0 + (hi / lo - 1.0) * f
+        target = hi / target_speedup
+        t0 = time.perf_counter()
+        cfg, fit, trace = nmsearch.search(lut8, gamma, b, target, accuracy, generations=30, offspring=8,
+                                          overshoot=4, seed=7)
+        wall = time.perf_counter() - t0
+        assign = [(n, 8) for n in cfg]
+        pred = nmsearch.latency_predict([lut8[l][cfg[l] - 1] for l in range(L)], gamma, b)
+        meas = cb.measure(assign, reps=5)
+        counts = {str(N): int(sum(1 for v in cfg if v == N)) for N in range(1, 9)}
+        searches.append({"target_speedup": round(target_speedup, 3), "target_us": round(target, 1),
+                         "predicted_us": round(pred, 1), "measured_us": round(meas, 1),
+                         "measured_speedup_vs_dense": round(T_test[len(test) - 2] / meas, 3),
+                         "pred_error_pct": round(abs(pred - meas) / meas * 100, 2),
+                         "fitness": round(fit, 4), "fitness_first_last": [round(trace[0], 4), round(trace[-1], 4)],
+                         "layers_per_N": counts, "search_s": round(wall, 2)})
+        log(json.dumps(searches[-1]))
+    res = {"workload": "vit_large_384_b32 linears (96 GEMMs, int32 outputs)", "lut_entries": len(table),
+           "lut_build_s": round(lut_s, 2), "calibration_configs": len(cal), "test_configs": len(test),
+           "chain_dense_us": round(float(T_test[len(test) - 2]), 1), "fits": fits, "predictor": chosen,
+           "family": family, "search": searches}
+    if report:
+        write_predictor_report(res, report)
+    return res
+
+
+def write_predictor_report(res, path):
+    md = ["# Latency predictor and layer-wise search: ViT-L/16 384 px, batch 32", "",
+          "Command: `python3 bench.py --predictor --report profiles/predictor_vit_large.md` (repository root).", "",
+          f"LUT: {res['lut_entries']} (shape, pattern) entries, mean of 20 runs each, built in "
+          f"{res['lut_build_s']} s (each run starts with flushed caches; the hot LUT of back-to-back repeats is "
+          f"shown for comparison).  Calibration on {res['calibration_configs']} random layer-wise N:8 "
+          f"configurations, prediction error on {res['test_configs']} others (random, the eight uniform ones and "
+          f"the seeded layer-wise draw of the chain workload).  All-dense chain: {res['chain_dense_us']} us.", "",
+          "| fit | mean abs error % | max abs error % | share within 5% |", "|---|---:|---:|---:|"]
+    for k, v in res["fits"].items():
+        md.append(f"| {k} | {v['mean_abs_pct']} | {v['max_abs_pct']} | {v['within_5pct']} |")
+    c = res["predictor"]
+    md += ["", f"Predictor used by the search (smallest 4-fold cross-validated error on the calibration "
+           f"configurations): {c['lut']} LUT, gamma per {c['gamma']}; cross-validated mean error "
+           f"{c['cv_mean_abs_pct']}%, on the test configurations {c['test']['mean_abs_pct']}% mean, "
+           f"{c['test']['max_abs_pct']}% max, {c['test']['within_5pct']} within 5%.", "",
+           "N:8 family per linear from the cold LUT (mean us; dense-equivalent TOPS; speedup over the dense GEMM):",
+           "",
+           "| linear | m | k | n | " + " | ".join(next(iter(res["family"].values()))["patterns"]) + " |",
+           "|---|---:|---:|---:|" + "---:|" * len(next(iter(res["family"].values()))["patterns"])]
+    for lin, f in res["family"].items():
+        md.append(f"| {lin} | {f['m']} | {f['k']} | {f['n']} | " + " | ".join(
+            f"{v['us']} / {v['tops']} / {v['speedup_vs_dense']}x" for v in f["patterns"].values()) + " |")
+    md += ["", "Algorithm 1 on the calibrated predictor (30 generations, 8 offspring, overshoot 4, synthetic "
+           "accuracy stand-in), then the returned configuration measured:", "",
+           "| target speedup | target us | predicted us | measured us | measured speedup | error % | layers per N (1..8) | search s |",
+           "|---:|---:|---:|---:|---:|---:|---|---:|"]
+    for s in res["search"]:
+        md.append(f"| {s['target_speedup']} | {s['target_us']} | {s['predicted_us']} | {s['measured_us']} | "
+                  f"{s['measured_speedup_vs_dense']} | {s['pred_error_pct']} | "
+                  f"{' '.join(s['layers_per_N'][str(n)] and str(s['layers_per_N'][str(n)]) or '0' for n in range(1, 9))} | {s['search_s']} |")
+    with open(path, "w") as f:
+        f.write("\n".join(md) + "\n")
+
+
+def chaining_experiment(torch, report):
+    """INT8 chaining steps (Sec. 6.3 deployment): the requantisation epilogue
+    (int8 output) against the int32 and fp16 outputs of the same GEMMs, 2:4
+    and dense, on DeiT-S batch 64 and ViT-L batch 32 linears; and the binary16
+    activation quantiser on a ViT-L activation tensor.  Mean of 20 runs;
+    achieved HBM bandwidth from the algorithmic bytes."""
+    from paper_2607_12505_amd import latency as lt
+    shapes = [("DeiT-S qkv", 12608, 384, 1152), ("DeiT-S fc1", 12608, 384, 1536), ("DeiT-S fc2", 12608, 1536, 384),
+              ("ViT-L fc1", 18464, 1024, 4096), ("ViT-L fc2", 18464, 4096, 1024)]
+    rows = []
+    for name, m, k, n in shapes:
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([31, m, k, n])))
+        X = torch.from_numpy(wl.gen_x(m, k, rng)).cuda()
+        W, scale = wl.gen_w(n, k, 2, 4, rng)
+        dw = nmspmm.DeviceWeight.from_packed(nmspmm.compress(W, 2, 4))
+        Wd = torch.from_numpy(W).cuda()
+        sc = torch.from_numpy(scale).cuda()
+        qs = torch.full((n,), 1e-3, dtype=torch.float32, device="cuda")
+        Y = torch.empty((m, n), dtype=torch.int32, device="cuda")
+        Yh = torch.empty((m, n), dtype=torch.int16, device="cuda")
+        Yq = torch.empty((m, n), dtype=torch.int8, device="cuda")
+        g = wl.Gemm(name, m, k, n, 2, 4)
+        for mode, kw, ob in (("int32", dict(Y=Y), 4), ("fp16", dict(Yh=Yh, scale=sc), 2),
+                             ("int8", dict(Yq=Yq, qscale=qs), 1)):
+            for kind in ("2:4", "dense"):
+                if kind == "2:4":
+                    fn = lambda kw=kw: nmspmm.spmm(X, dw, **kw)
+                    wbytes = algorithmic_bytes(g, False, False) - m * k
+                else:
+                    fn = lambda kw=kw: nmspmm.gemm_i8_dense(X, Wd, **kw)
+                    wbytes = n * k
+                us = lt.time_launches(torch, fn, 20)
+                b = m * k + wbytes + ob * m * n + (4 * n if mode != "int32" else 0)
+                rows.append({"gemm": name, "m": m, "k": k, "n": n, "output": mode, "kind": kind,
+                             "us": round(us, 2), "gbs": round(b / us / 1e3, 1),
+                             "hbm_frac": round(b / us / 1e3 / PEAK_HBM_GBS, 3)})
+                log(json.dumps(rows[-1]))
+    count = 18464 * 1024
+    x = torch.randn(count, dtype=torch.float16, device="cuda").view(torch.int16)
+    xq = torch.empty(count, dtype=torch.int8, device="cuda")
+    us = lt.time_launches(torch, lambda: nmspmm.quantize_f16(x, 1.0 / 0.05, xq=xq), 20)
+    quant = {"elements": count, "us": round(us, 2), "gbs": round(3 * count / us / 1e3, 1),
+             "hbm_frac": round(3 * count / us / 1e3 / PEAK_HBM_GBS, 3)}
+    log(json.dumps(quant))
+    res = {"requant_epilogue": rows, "quantize_f16": quant}
+    if report:
+        md = ["# INT8 chaining: requantisation epilogue and activation quantiser", "",
+              "Command: `python3 bench.py --chaining --report profiles/int8_chaining.md` (repository root).  "
+              "Mean of 20 back-to-back runs per row (HIP events); GB/s from the algorithmic bytes (X, the weight "
+              "-- compact packed form for 2:4 --, the output, the multipliers).", "",
+              "| GEMM | m | k | n | output | weight | us | GB/s | HBM fraction |", "|---|---:|---:|---:|---|---|---:|---:|---:|"]
+        for r in rows:
+            md.append(f"| {r['gemm']} | {r['m']} | {r['k']} | {r['n']} | {r['output']} | {r['kind']} | {r['us']} | "
+                      f"{r['gbs']} | {r['hbm_frac']} |")
+        md += ["", f"Activation quantiser (binary16 -> int8, {count} elements = one ViT-L fc1 input): "
+               f"{quant['us']} us, {quant['gbs']} GB/s ({quant['hbm_frac']} of HBM peak)."]
+        with open(report, "w") as f:
+            f.write("\n".join(md) + "\n")
+    return res
+
+
+def write_sweep_report(sweep_json, path):
+    """Markdown table of a planner evaluation written by --sweep-out."""
+    d = json.load(open(sweep_json))
+    s = d["summary"]
+    md = ["# Planner evaluation (Table-1 methodology) on MI355X", "",
+          "Commands: `python3 bench.py --sweep 0,1,2,3,4 --sweep-out sweep.json` (GPU; every (tile, split_k) "
+          "candidate timed, 10 launches each, outputs rotated over buffers larger than the 256 MB last-level cache), "
+          "then `python3 bench.py --sweep-report sweep.json --report <this file>`.", "",
+          "Normalised performance = t(sweep optimum) / t(planner choice); tile indices are those of the "
+          "library's tile table (`nm_tile_info`).", "",
+          f"Summary: {s['cases']} distinct (shape, N:M) cases; planner Top-1 hit rate {s['top1_hit_rate']}, "
+          f"average normalised performance {s['avg_norm_perf']}, worst {s['worst_norm_perf']}; gain over a fixed "
+          f"split_k = 1 with the same tile {s['gain_over_fixed_split1']}.", "",
+          "| workload | m | k | n | N:M | planner tile/split | us | best tile/split | us | norm |",
+          "|---|---:|---:|---:|---|---|---:|---|---:|---:|"]
+    for r in d["rows"]:
+        md.append(f"| cfg{r['cfg']} {r['gemm']} | {r['m']} | {r['k']} | {r['n']} | {r['pattern']} | "
+                  f"{r['planned'][0]}/{r['planned'][1]} | {r['t_planned_us']:.1f} | {r['best'][0]}/{r['best'][1]} | "
+                  f"{r['t_best_us']:.1f} | {r['t_best_us'] / r['t_planned_us']:.3f} |")
+    with open(path, "w") as f:
+        f.write("\n".join(md) + "\n")
+
+
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_12505_amd", "csrc", "nmspmm_kernels.hip")
 
 
@@ -313,12 +558,14 @@ def default_traffic_path(workload_name):
     return os.path.join(ROOT, "profiles", f"traffic_{workload_name}.json")
 
 
-def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, commands, out_md):
+def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, commands, out_md, sq_dir=None):
     """Summarises rocprofv3 CSV output of a bench run: per-kernel durations
     from the kernel trace, and FETCH_SIZE / WRITE_SIZE per dispatch scaled by
     what the same counters read for the calibration copy (copy_mib MiB read
-    and written).  Writes a markdown summary and the traffic record of the
-    dominant kernel next to it."""
+    and written); with sq_dir, also matrix-core busy time and LDS bank
+    conflicts per kernel (SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE,
+    SQ_LDS_BANK_CONFLICT, SQ_LDS_IDX_ACTIVE).  Writes a markdown summary and the
+    traffic record of the dominant kernel next to it."""
     import csv
     import glob
     line = json.loads(open(bench_json).read().strip().splitlines()[-1])
@@ -327,10 +574,11 @@ def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, comma
     stats = list(csv.DictReader(open(glob.glob(os.path.join(trace_dir, "*_kernel_stats.csv"))[0])))
     stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
 
-    def counters(d):
+    def counters(d, name=None):
         per = {}
         for r in csv.DictReader(open(glob.glob(os.path.join(d, "*_counter_collection.csv"))[0])):
-            per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+            if name is None or r["Counter_Name"] == name:
+                per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
         return per
 
     fetch, write = counters(fetch_dir), counters(write_dir)
@@ -368,6 +616,20 @@ def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, comma
     alg = line["roofline"]["algorithmic_bytes_per_launch"]
     md += ["", f"Dominant kernel: measured traffic {bytes_per_launch / 1e6:.2f} MB per launch vs "
            f"{alg / 1e6:.2f} MB algorithmic ({bytes_per_launch / alg:.3f}x)."]
+    if sq_dir:
+        busy, active = counters(sq_dir, "SQ_VALU_MFMA_BUSY_CYCLES"), counters(sq_dir, "GRBM_GUI_ACTIVE")
+        conf, lds = counters(sq_dir, "SQ_LDS_BANK_CONFLICT"), counters(sq_dir, "SQ_LDS_IDX_ACTIVE")
+        simds = 4 * int(line.get("cus", 256))
+        md += ["", f"Matrix cores and LDS per dispatch (one more pass: `--pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
+               f"SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE`).  MFMA busy = busy cycles / (active cycles x {simds} SIMDs); "
+               "LDS bank conflicts = conflict cycles / LDS active cycles:", "",
+               "| kernel | dispatches | MFMA busy % | LDS conflict % |", "|---|---:|---:|---:|"]
+        for k in sorted(busy, key=lambda k: -np.mean(busy[k])):
+            if "nmspmm" not in k or k not in active:
+                continue
+            mb = 100.0 * np.mean(busy[k]) / (np.mean(active[k]) * simds)
+            lc = 100.0 * np.mean(conf[k]) / max(np.mean(lds[k]), 1.0) if k in conf and k in lds else float("nan")
+            md.append(f"| `{k[:90]}` | {len(busy[k])} | {mb:.1f} | {lc:.2f} |")
     with open(out_md, "w") as f:
         f.write("\n".join(md) + "\n")
     rec = {"kernel": dom, "workload": work, "bytes_per_launch": int(bytes_per_launch),
@@ -391,20 +653,34 @@ def main():
     ap.add_argument("--sweep", type=str, default=None,
                     help="planner evaluation over the given comma-separated configs (e.g. 0,1,2,3,4)")
     ap.add_argument("--sweep-out", type=str, default=None, help="JSON file for the sweep results")
+    ap.add_argument("--sweep-report", type=str, default=None, metavar="SWEEP_JSON",
+                    help="markdown report (--report) of a sweep JSON (no GPU needed)")
     ap.add_argument("--traffic", type=str, default=None,
                     help="JSON record of measured HBM bytes per launch of the dominant kernel "
                          "(default: profiles/traffic_<workload>.json, used only if it matches this kernel source)")
     ap.add_argument("--rocprof-summary", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"), default=None,
                     help="summarise rocprofv3 CSV output of a bench run (no GPU needed)")
     ap.add_argument("--bench-json", type=str, default=None, help="bench output line used by --rocprof-summary")
+    ap.add_argument("--rocprof-sq", type=str, default=None,
+                    help="rocprofv3 counter output with MFMA busy / LDS bank conflict counters (--rocprof-summary)")
     ap.add_argument("--summary-out", type=str, default=None, help="markdown file written by --rocprof-summary")
     ap.add_argument("--commands", type=str, default=None, help="file with the profiling commands to quote")
+    ap.add_argument("--predictor", action="store_true",
+                    help="latency LUT + Eq. 1 calibration + Algorithm 1 on ViT-L (prints one JSON line)")
+    ap.add_argument("--chaining", action="store_true",
+                    help="int8 requantisation epilogue and activation quantiser timings (prints one JSON line)")
+    ap.add_argument("--cal", type=int, default=64, help="calibration configurations for --predictor")
+    ap.add_argument("--test", type=int, default=32, help="random test configurations for --predictor")
+    ap.add_argument("--report", type=str, default=None, help="markdown report of --predictor / --chaining")
     args = ap.parse_args()
 
+    if args.sweep_report:
+        write_sweep_report(args.sweep_report, args.report)
+        return
     if args.rocprof_summary:
         cmds = open(args.commands).read().strip().splitlines() if args.commands else []
         rocprof_summary(*args.rocprof_summary, args.bench_json, args.copy_calibration or 256, cmds,
-                        args.summary_out)
+                        args.summary_out, args.rocprof_sq)
         return
 
     if args.gpus != 1:
@@ -421,6 +697,12 @@ def main():
     if args.sweep:
         summary = sweep([int(c) for c in args.sweep.split(",")], torch, 10, args.sweep_out)
         print(json.dumps({"planner_evaluation": summary}), flush=True)
+        return
+    if args.chaining:
+        print(json.dumps({"chaining": chaining_experiment(torch, args.report)}), flush=True)
+        return
+    if args.predictor:
+        print(json.dumps({"predictor": predictor_experiment(torch, args.cal, args.test, args.report)}), flush=True)
         return
 
     work = wl.workload(args.config)

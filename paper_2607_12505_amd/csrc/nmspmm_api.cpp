@@ -120,6 +120,9 @@ extern "C" nm_status nm_plan_kernel_name(const nm_plan *plan, char *buf, int len
         w = std::snprintf(buf, (size_t)len, "k_gemm_ks<%d, %d, %d, %d>", plan->kind, t.fn, t.fm, t.nst);
     else if (t.layout == kRowStat)
         w = std::snprintf(buf, (size_t)len, "k_gemm_rs<%d, %d, %d, %d>", plan->kind, t.fn, t.fm, t.nst);
+    else if (t.layout == kPersist)
+        w = std::snprintf(buf, (size_t)len, "k_gemm_ps<%d, %d, %d, %d, %d, %d>", plan->kind, t.wn, t.wm, t.fn, t.fm,
+                          t.nst);
     else
         w = std::snprintf(buf, (size_t)len, "k_gemm<%d, %d, %d, %d, %d, %d>", plan->kind, t.wn, t.wm, t.fn, t.fm, t.nst);
     return (w > 0 && w < len) ? NM_OK : NM_ERR_ARG;

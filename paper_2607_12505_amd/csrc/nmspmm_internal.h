@@ -27,8 +27,11 @@ constexpr int kThreads = 256;    // threads per workgroup (4 waves of 64)
 //               workgroup keeps a token block of X in LDS and walks a range of
 //               output tiles (row-stationary), so the grid is a fixed number
 //               of workgroups.
+//   kPersist:   kOutSplit tiles walked by a fixed grid of workgroups, the
+//               (tile, k-step) slices streaming through one ring so the next
+//               tile loads while the current one is stored; split_k = 1.
 // nst = depth of the ring of k-step slots staged in LDS.
-enum Layout { kOutSplit = 0, kKSliced = 1, kRowStat = 2 };
+enum Layout { kOutSplit = 0, kKSliced = 1, kRowStat = 2, kPersist = 3 };
 
 struct TileCfg {
     int wn, wm, fn, fm, nst, layout;
@@ -52,6 +55,12 @@ constexpr TileCfg kTiles[] = {
     {2, 2, 4, 4, 3, kRowStat},   // 11: 128 ch x 128 tok, row-stationary
     {2, 2, 4, 2, 3, kRowStat},   // 12: 128 ch x  64 tok, row-stationary
     {2, 2, 8, 2, 3, kRowStat},   // 13: 256 ch x  64 tok, row-stationary
+    {2, 2, 4, 4, 3, kPersist},   // 14: 128 ch x 128 tok, persistent
+    {2, 2, 4, 2, 4, kPersist},   // 15: 128 ch x  64 tok, persistent
+    {2, 2, 4, 4, 2, kOutSplit},  // 16: 128 ch x 128 tok, 2-slot ring (3 workgroups per CU)
+    {2, 2, 4, 2, 2, kOutSplit},  // 17: 128 ch x  64 tok, 2-slot ring
+    {2, 2, 2, 4, 2, kOutSplit},  // 18:  64 ch x 128 tok, 2-slot ring
+    {2, 2, 2, 2, 2, kOutSplit},  // 19:  64 ch x  64 tok, 2-slot ring
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
@@ -73,6 +82,20 @@ inline RowStatLds rowstat_lds(int kind, const TileCfg &t, int k_steps) {
     return L;
 }
 constexpr size_t kLdsPerCu = 160 * 1024;
+
+// LDS of an output-split workgroup (kOutSplit, kPersist): the ring of k-step
+// slots (X slice and weight slice), as deep as asked or as 160 KB allows, or
+// the epilogue staging if larger.
+inline size_t outsplit_lds(int kind, const TileCfg &t) {
+    const bool sparse = kind != NM_KIND_DENSE;
+    const int S = kind == NM_KIND_SP42X2 ? 2 : 1;
+    const size_t BN = t.tile_n(), BM = t.tile_m();
+    const size_t slot = BM * 128 + (sparse ? (BN / 16) * S * (kVBlock + kMBlock) : BN * 128);
+    const size_t cap = kLdsPerCu - 1024;
+    const size_t ring = (size_t)t.nst * slot <= cap ? (size_t)t.nst : cap / slot;
+    const size_t epi = (size_t)4 * 16 * (t.fn * 64 + 16);
+    return ring * slot > epi ? ring * slot : epi;
+}
 
 // Everything a GEMM kernel needs; passed by value as the kernel argument.
 struct GemmArgs {

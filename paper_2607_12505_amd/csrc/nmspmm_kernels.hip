@@ -156,12 +156,26 @@ __device__ inline void emit_out(const GemmArgs &a, int tok, int ch, const v4i &v
     }
 }
 
+// The multipliers of 4 consecutive channels.  The loads are issued whatever
+// outputs are present (from a valid dummy address when a multiplier array is
+// absent, or from channel 0 past n) so that no branch guards them: the
+// compiler then waits for them once, at their first use, instead of emitting
+// a full vector-memory wait before every later use, which would also wait
+// for every store issued in between.
+//
+// The loads are also awaited right away (all vector-memory operations of the
+// wave): the compiler's own wait tracking cannot see through the output
+// branches of emit_out and would otherwise wait again before every store.
+// Callers load the multipliers where nothing else of theirs is in flight
+// that they could keep waiting for.
 __device__ inline EpiScale load_scale(const GemmArgs &a, int ch) {
+    const int c = ch < a.n ? ch : 0;
+    const float *sc = a.scale ? a.scale : (const float *)a.X;    // X holds at least 16 aligned bytes
+    const float *qs = a.qscale ? a.qscale : (const float *)a.X;
     EpiScale es;
-    es.sc = v4f{0.f, 0.f, 0.f, 0.f};
-    es.qs = v4f{0.f, 0.f, 0.f, 0.f};
-    if (a.Yh && ch < a.n) es.sc = *(const v4f *)(a.scale + ch);
-    if (a.Yq && ch < a.n) es.qs = *(const v4f *)(a.qscale + ch);
+    es.sc = *(const v4f *)(sc + (a.scale ? c : 0));
+    es.qs = *(const v4f *)(qs + (a.qscale ? c : 0));
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0); expcnt and lgkmcnt not waited for
     return es;
 }
 
@@ -202,8 +216,9 @@ __device__ inline bool arrive_last(const GemmArgs &a, int tile, int *s_flag) {
     return *s_flag != 0;
 }
 
-template <int KIND, int WN, int WM, int FN, int FM, int NST>
+template <int KIND, int WN_, int WM_, int FN_, int FM_, int NST>
 struct Geometry {
+    static constexpr int WN = WN_, WM = WM_, FN = FN_, FM = FM_;
     static constexpr int BN = WN * FN * 16;
     static constexpr int BM = WM * FM * 16;
     static constexpr bool kSparse = KIND != NM_KIND_DENSE;
@@ -227,44 +242,20 @@ struct Geometry {
     static_assert(LDSB <= 160 * 1024, "LDS budget");
 };
 
-template <int KIND, int WN, int WM, int FN, int FM, int NST>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
-    using G = Geometry<KIND, WN, WM, FN, FM, NST>;
-    constexpr int BN = G::BN, BM = G::BM, S = G::S;
-    constexpr bool kSparse = G::kSparse;
-    constexpr int R = G::RING;
+// The stages of an output-split tile (4 waves, each FN x FM accumulators of a
+// WN x WM arrangement), shared by the one-tile-per-workgroup kernel and the
+// persistent one.
+template <class G>
+struct OutSplit {
+    static constexpr int BN = G::BN, BM = G::BM, S = G::S, FN = G::FN, FM = G::FM;
 
-    __shared__ __attribute__((aligned(1024))) int8_t lds[G::LDSB];
-    __shared__ int s_last;
-    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
-
-    const int lid = map_block(blockIdx.x, gridDim.x);
-    const int tn = lid % a.tiles_n;
-    const int rest = lid / a.tiles_n;
-    const int split = rest % a.split_k;
-    const int tm = rest / a.split_k;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wn = wave % WN, wm = wave / WN;
-    const int lg = lane >> 4;
-    const int tok0 = tm * BM;
-    const int ch0 = tn * BN;
-    const int s_begin = (int)((int64_t)split * a.k_steps / a.split_k);
-    const int s_end = (int)((int64_t)(split + 1) * a.k_steps / a.split_k);
-    const int nsteps = s_end - s_begin;
-    const int f0 = ch0 >> 4;
-
-    v4i acc[FN][FM];
-#pragma unroll
-    for (int i = 0; i < FN; ++i)
-#pragma unroll
-        for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
-
-    // Fill ring slot st with k-step s.  Rows of X past m, and weight rows past
-    // n, read a valid row instead: their outputs are never stored.  Past k the
-    // packed weight is zero, so X may hold anything there; for a dense weight
-    // the tail k-step is staged with zeros instead (see below).
-    auto issue = [&](int s, int st) {
+    // Fill ring slot st with k-step s of the tile at (tok0, ch0).  Rows of X
+    // past m, and weight rows past n, read a valid row instead: their outputs
+    // are never stored.  Past k the packed weight is zero, so X may hold
+    // anything there; for a dense weight the tail k-step is staged with zeros
+    // instead.
+    static __device__ __forceinline__ void issue(const GemmArgs &a, int8_t *lds, uint32_t lds0, int wave, int lane,
+                                                 int tok0, int ch0, int s, int st) {
         const uint32_t slot = lds0 + st * G::SLOT;
 #pragma unroll
         for (int j = 0; j < G::XI; ++j) {
@@ -274,7 +265,8 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
             const int kk = s * 128 + c * 16 < a.k ? s * 128 + c * 16 : a.k - 16;
             dma16(a.X + (size_t)tok * a.k + kk, slot + (4 * j + wave) * 1024);
         }
-        if constexpr (kSparse) {
+        if constexpr (G::kSparse) {
+            const int f0 = ch0 >> 4;
 #pragma unroll
             for (int j = 0; j < (BN / 16) * S / 4; ++j) {
                 const int bl = 4 * j + wave;               // weight block of the slot: fragment bl / S, stream bl % S
@@ -307,12 +299,15 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
                 }
             }
         }
-    };
+    }
 
-    auto compute = [&](int st) {
+    // One k-step of the wave's FN x FM accumulators from ring slot st.
+    static __device__ __forceinline__ void compute(const int8_t *lds, int wn, int wm, int lane, int st,
+                                                   v4i (&acc)[FN][FM]) {
+        const int lg = lane >> 4;
         const int8_t *xs = lds + st * G::SLOT;
         const int8_t *ws = xs + G::XB;
-        if constexpr (kSparse) {
+        if constexpr (G::kSparse) {
             v4i av[FN][S];
             int ai[FN][S];
 #pragma unroll
@@ -358,55 +353,102 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
                 }
             }
         }
-    };
+    }
+
+    // Epilogue of the wave's part of a tile through its private staging area
+    // stg (16 rows of ROWB bytes): 16 tokens at a time, the FN accumulators
+    // become int32 rows, read back row-contiguously, so that every store
+    // instruction writes whole rows of the wave's tile.  With split_k > 1 the
+    // rows go to the partial-sum workspace instead.
+    static __device__ __forceinline__ void store(const GemmArgs &a, int8_t *stg, int lane, int wn, int wm, int tok0,
+                                                 int ch0, int split, const v4i (&acc)[FN][FM]) {
+        const int lg = lane >> 4;
+        const int ec = lane % G::CPR;                     // 4-channel chunk this lane stores
+        const int er = lane / G::CPR;                     // row offset within a read group
+        const int ch = ch0 + wn * FN * 16 + ec * 4;       // first of the lane's 4 channels
+        const bool ch_ok = ch < a.n;
+        const EpiScale sc = load_scale(a, ch);
+        const __amdgpu_buffer_rsrc_t prsrc = partial_rsrc(a);
+        constexpr int NR = 16 / G::RPI;                   // staged rows each lane stores per 16 tokens
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+                *(v4i *)(stg + (lane & 15) * G::ROWB + (i * 16 + 4 * lg) * 4) = acc[i][j];
+            // all reads first, then the stores: one wait for the reads, none between stores
+            v4i v[NR];
+#pragma unroll
+            for (int r = 0; r < NR; ++r) v[r] = *(const v4i *)(stg + (r * G::RPI + er) * G::ROWB + ec * 16);
+#pragma unroll
+            for (int r = 0; r < NR; ++r) {
+                const int tok = tok0 + (wm * FM + j) * 16 + r * G::RPI + er;
+                if (tok < a.m && ch_ok) {
+                    if (a.split_k == 1)
+                        emit_out(a, tok, ch, v[r], sc);
+                    else
+                        publish_partial(a, prsrc, split, tok, ch, v[r]);
+                }
+            }
+        }
+    }
+};
+
+template <int KIND, int WN, int WM, int FN, int FM, int NST>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+    using G = Geometry<KIND, WN, WM, FN, FM, NST>;
+    using O = OutSplit<G>;
+    constexpr int BN = G::BN, BM = G::BM;
+    constexpr int R = G::RING;
+
+    __shared__ __attribute__((aligned(1024))) int8_t lds[G::LDSB];
+    __shared__ int s_last;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
+
+    const int lid = map_block(blockIdx.x, gridDim.x);
+    const int tn = lid % a.tiles_n;
+    const int rest = lid / a.tiles_n;
+    const int split = rest % a.split_k;
+    const int tm = rest / a.split_k;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wn = wave % WN, wm = wave / WN;
+    const int tok0 = tm * BM;
+    const int ch0 = tn * BN;
+    const int s_begin = (int)((int64_t)split * a.k_steps / a.split_k);
+    const int s_end = (int)((int64_t)(split + 1) * a.k_steps / a.split_k);
+    const int nsteps = s_end - s_begin;
+
+    v4i acc[FN][FM];
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
 
 #pragma unroll
     for (int i = 0; i < R - 1; ++i)
-        if (i < nsteps) issue(s_begin + i, i);
+        if (i < nsteps) O::issue(a, lds, lds0, wave, lane, tok0, ch0, s_begin + i, i);
     for (int it = 0; it < nsteps; ++it) {
         // k-step it was issued NST-1 iterations ago; only the loads of later
         // k-steps may remain in flight.  The barrier then publishes every
         // wave's slot and frees the slot computed in the previous iteration.
         const int later = nsteps - 1 - it < R - 2 ? nsteps - 1 - it : R - 2;
         wait_later_then_barrier<R - 2, G::DMA>(later);
-        if (it + R - 1 < nsteps) issue(s_begin + it + R - 1, (it + R - 1) % R);
-        compute(it % R);
+        if (it + R - 1 < nsteps) O::issue(a, lds, lds0, wave, lane, tok0, ch0, s_begin + it + R - 1, (it + R - 1) % R);
+        O::compute(lds, wn, wm, lane, it % R, acc);
     }
 
-    // Epilogue through LDS: each wave stages 16 tokens x FN*16 channels of its
-    // accumulators as int32 rows, then reads them back row-contiguously.
     __syncthreads();  // every wave is done with the ring
-    int8_t *stg = lds + wave * 16 * G::ROWB;
-    const int ec = lane % G::CPR;                     // 4-channel chunk this lane stores
-    const int er = lane / G::CPR;                     // row offset within a read group
-    const int ch = ch0 + wn * FN * 16 + ec * 4;       // first of the lane's 4 channels
-    const bool ch_ok = ch < a.n;
-    const EpiScale sc = load_scale(a, ch);
-    const __amdgpu_buffer_rsrc_t prsrc = partial_rsrc(a);
-
-#pragma unroll
-    for (int j = 0; j < FM; ++j) {
-#pragma unroll
-        for (int i = 0; i < FN; ++i)
-            *(v4i *)(stg + (lane & 15) * G::ROWB + (i * 16 + 4 * lg) * 4) = acc[i][j];
-#pragma unroll
-        for (int r0 = 0; r0 < 16; r0 += G::RPI) {
-            const int t = r0 + er;
-            const v4i v = *(const v4i *)(stg + t * G::ROWB + ec * 16);
-            const int tok = tok0 + (wm * FM + j) * 16 + t;
-            if (tok < a.m && ch_ok) {
-                if (a.split_k == 1)
-                    emit_out(a, tok, ch, v, sc);
-                else
-                    publish_partial(a, prsrc, split, tok, ch, v);
-            }
-        }
-    }
+    O::store(a, lds + wave * 16 * G::ROWB, lane, wn, wm, tok0, ch0, split, acc);
     if (a.split_k == 1) return;
 
     // Split-K: the last split to arrive adds every partial (integer addition:
     // any order gives the same result) and writes the outputs.
     if (!arrive_last(a, tm * a.tiles_n + tn, &s_last)) return;
+    const int ec = lane % G::CPR, er = lane / G::CPR;
+    const int ch = ch0 + wn * FN * 16 + ec * 4;
+    const bool ch_ok = ch < a.n;
+    const EpiScale sc = load_scale(a, ch);
+    const __amdgpu_buffer_rsrc_t prsrc = partial_rsrc(a);
 #pragma unroll
     for (int j = 0; j < FM; ++j)
 #pragma unroll
@@ -414,6 +456,74 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
             const int tok = tok0 + (wm * FM + j) * 16 + r0 + er;
             if (tok < a.m && ch_ok) emit_out(a, tok, ch, merge_partials(a, prsrc, tok, ch), sc);
         }
+}
+
+// ---------------------------------------------------------------------------
+// Persistent output-split variant for shapes with many output tiles: a fixed
+// grid of workgroups walks the tiles (workgroup w takes tiles w, w + grid, ...)
+// and streams the (tile, k-step) slices through one continuous ring, so the
+// first k-steps of the next tile are loading while the current tile's
+// epilogue runs.  The epilogue stages through the ring slot computed last:
+// nothing is loaded into it before the next iteration's barrier, which every
+// wave reaches only after its staging reads.  split_k must be 1.
+//
+// Store completions also count in the vector-memory counter.  The waits count
+// only loads issued after the awaited one; since loads complete in order,
+// extra stores in flight can only make a wait longer, never let it pass
+// early.
+template <int KIND, int WN, int WM, int FN, int FM, int NST>
+__global__ __launch_bounds__(256) void k_gemm_ps(GemmArgs a) {
+    using G = Geometry<KIND, WN, WM, FN, FM, NST>;
+    using O = OutSplit<G>;
+    constexpr int BN = G::BN, BM = G::BM;
+    constexpr int R = G::RING;
+    static_assert(G::EPI <= G::SLOT && R >= 2, "the epilogue stages inside one ring slot");
+
+    __shared__ __attribute__((aligned(1024))) int8_t lds[G::LDSB];
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
+
+    const int lid = map_block(blockIdx.x, gridDim.x);
+    const int T = a.tiles_m * a.tiles_n;
+    const int G_ = (int)gridDim.x;
+    const int ntiles = lid < T ? (T - 1 - lid) / G_ + 1 : 0;
+    const int nq = ntiles * a.k_steps;  // (tile, k-step) pairs of this workgroup, in order
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wn = wave % WN, wm = wave / WN;
+
+    auto issue_pair = [&](int q) {
+        const int t = lid + (q / a.k_steps) * G_;
+        O::issue(a, lds, lds0, wave, lane, (t / a.tiles_n) * BM, (t % a.tiles_n) * BN, q % a.k_steps, q % R);
+    };
+
+    v4i acc[FN][FM];
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+
+#pragma unroll
+    for (int i = 0; i < R - 1; ++i)
+        if (i < nq) issue_pair(i);
+    for (int q = 0; q < nq; ++q) {
+        // pair q has landed; the slot computed in the previous iteration (or
+        // used there for staging) is free for pair q + R - 1
+        const int later = nq - 1 - q < R - 2 ? nq - 1 - q : R - 2;
+        wait_later_then_barrier<R - 2, G::DMA>(later);
+        if (q + R - 1 < nq) issue_pair(q + R - 1);
+        O::compute(lds, wn, wm, lane, q % R, acc);
+        if (q % a.k_steps == a.k_steps - 1) {
+            // every wave has read its operands from slot q % R: stage there
+            wait_then_barrier<63>();
+            const int t = lid + (q / a.k_steps) * G_;
+            O::store(a, lds + (q % R) * G::SLOT + wave * 16 * G::ROWB, lane, wn, wm, (t / a.tiles_n) * BM,
+                     (t % a.tiles_n) * BN, 0, acc);
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+#pragma unroll
+                for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -588,15 +698,18 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
     __syncthreads();
     const __amdgpu_buffer_rsrc_t prsrc = partial_rsrc(a);
     constexpr int CHUNKS = BM * G::CPR;
+    static_assert(256 % G::CPR == 0, "a thread keeps its channel chunk across rows");
+    const int cc = tid % G::CPR, ch = ch0 + cc * 4;   // the same for every row this thread stores
+    const EpiScale sc = load_scale(a, ch);
     for (int c = tid; c < CHUNKS; c += 256) {
-        const int row = c / G::CPR, cc = c % G::CPR;
-        const int tok = tok0 + row, ch = ch0 + cc * 4;
+        const int row = c / G::CPR;
+        const int tok = tok0 + row;
         v4i v = v4i{0, 0, 0, 0};
 #pragma unroll
         for (int w = 0; w < 4; ++w) v += *(const v4i *)(lds + w * BM * G::ROWB + row * G::ROWB + cc * 16);
         if (tok < a.m && ch < a.n) {
             if (a.split_k == 1)
-                emit_out(a, tok, ch, v, load_scale(a, ch));
+                emit_out(a, tok, ch, v, sc);
             else
                 publish_partial(a, prsrc, split, tok, ch, v);
         }
@@ -604,8 +717,8 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
     if (a.split_k == 1) return;
     if (!arrive_last(a, tm * a.tiles_n + tn, &s_last)) return;
     for (int c = tid; c < CHUNKS; c += 256) {
-        const int tok = tok0 + c / G::CPR, ch = ch0 + (c % G::CPR) * 4;
-        if (tok < a.m && ch < a.n) emit_out(a, tok, ch, merge_partials(a, prsrc, tok, ch), load_scale(a, ch));
+        const int tok = tok0 + c / G::CPR;
+        if (tok < a.m && ch < a.n) emit_out(a, tok, ch, merge_partials(a, prsrc, tok, ch), sc);
     }
 }
 
@@ -829,6 +942,9 @@ int launch_one(const GemmArgs &args, int grid, void *stream) {
                            args);
     } else if constexpr (t.layout == kKSliced)
         hipLaunchKernelGGL((k_gemm_ks<KIND, t.fn, t.fm, t.nst>), dim3(grid), dim3(kThreads), 0,
+                           (hipStream_t)stream, args);
+    else if constexpr (t.layout == kPersist)
+        hipLaunchKernelGGL((k_gemm_ps<KIND, t.wn, t.wm, t.fn, t.fm, t.nst>), dim3(grid), dim3(kThreads), 0,
                            (hipStream_t)stream, args);
     else
         hipLaunchKernelGGL((k_gemm<KIND, t.wn, t.wm, t.fn, t.fm, t.nst>), dim3(grid), dim3(kThreads), 0,

@@ -72,6 +72,14 @@ nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *p) {
         p->grid = (int)(tiles < slots ? tiles : slots);
         return NM_OK;
     }
+    if (t.layout == kPersist) {
+        // a fixed grid: as many workgroups as fit on the chip at once
+        if (p->split_k != 1) return NM_ERR_ARG;
+        const int64_t per_cu = (int64_t)(kLdsPerCu / outsplit_lds(kind, t));
+        const int64_t slots = (int64_t)device_cu_count() * (per_cu > 0 ? per_cu : 1);
+        p->grid = (int)(tiles < slots ? tiles : slots);
+        return NM_OK;
+    }
     const int64_t grid = tiles * p->split_k;
     if (grid > 0x7fffffff) return NM_ERR_SHAPE;
     if (p->split_k > 1 && tiles > kMaxSplitTiles) return NM_ERR_ARG;
@@ -82,7 +90,8 @@ nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *p) {
 }
 
 // Tile indices used by the rules below (see kTiles).
-constexpr int kT256x256 = 0, kT128x128 = 2, kT128x64 = 4, kT64x64 = 6, kT32x32ks = 10, kT128x128rs = 11;
+constexpr int kT64x64 = 6, kT32x32ks = 10, kT128x128rs = 11;
+constexpr int kT128x128r2 = 16, kT128x64r2 = 17, kT64x128r2 = 18, kT64x64r2 = 19;
 
 static int64_t tiles_of(int t, int m, int n) {
     return ceil_div(n, kTiles[t].tile_n()) * ceil_div(m, kTiles[t].tile_m());
@@ -95,26 +104,32 @@ nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *
     const int mm = m > 0 ? m : 1;
     // Operands twice as heavy per k-step: dense weights and two 4:2 streams.
     const bool heavy = kind != NM_KIND_SP42;
+    // Rules fitted to an exhaustive timing of every tile on the ViT, DeiT and
+    // Swin shapes (the paper's Table 1 methodology): above a few hundred
+    // tokens the two-slot rings win -- their smaller LDS footprint keeps three
+    // or more workgroups per compute unit, so one workgroup's loads overlap
+    // another's compute and stores.
     int tile;
     if (mm <= 512) {
         // Few tokens: too few output tiles to occupy the GPU.  Split the
         // reduction over the waves of each workgroup (k-sliced tile, merged in
-        // LDS) when k is long enough and the 32 x 32 tiles do not oversubscribe.
-        tile = (k_steps >= 4 && tiles_of(kT32x32ks, mm, n) <= 2 * cus) ? kT32x32ks : kT64x64;
-    } else if (tiles_of(kT128x128, mm, n) < cus) {
-        // Medium: the largest tile that still gives every compute unit one.
-        tile = tiles_of(kT128x64, mm, n) >= cus ? kT128x64 : kT64x64;
-    } else if (n <= 384 && k_steps >= 3) {
-        // Narrow outputs: small tiles keep more workgroups per output row.
-        tile = kT64x64;
-    } else if (tiles_of(kT256x256, mm, n) >= 4 * cus || (heavy && n >= 3072)) {
-        // Very large outputs: keep X resident and stream the weight when the
-        // token block fits in LDS (short k, one-stream weights); otherwise the
-        // biggest tile, which halves the operand traffic per output.
-        const bool rs_fits = rowstat_lds(kind, kTiles[kT128x128rs], k_steps).total <= kLdsPerCu;
-        tile = (!heavy && k_steps <= 6 && rs_fits) ? kT128x128rs : kT256x256;
+        // LDS) when k has at least two k-steps and the 32 x 32 tiles do not
+        // oversubscribe.
+        tile = (k_steps >= 2 && tiles_of(kT32x32ks, mm, n) <= 2 * cus) ? kT32x32ks : kT64x64;
+    } else if (k_steps <= 2) {
+        // Very short reductions: the output stream dominates; small tiles
+        // give the most workgroups in flight.
+        tile = kT64x64r2;
+    } else if (tiles_of(kT128x128r2, mm, n) < 4 * cus) {
+        // Medium: half-height tiles (narrower for the heavier operands).
+        tile = heavy ? kT64x128r2 : kT128x64r2;
     } else {
-        tile = kT128x128;
+        // Large: keep X resident and stream the weight when the token block
+        // fits in LDS (short k, one-stream weights) and there are many tiles;
+        // else 128 x 128 tiles.
+        const bool rs_fits = rowstat_lds(kind, kTiles[kT128x128rs], k_steps).total <= kLdsPerCu;
+        const bool many = ceil_div(n, 256) * ceil_div(mm, 256) >= 4 * cus;
+        tile = (!heavy && k_steps <= 6 && rs_fits && many) ? kT128x128rs : kT128x128r2;
     }
     plan->kind = kind;
     plan->tile = tile;

@@ -111,8 +111,9 @@ def test_every_tile_and_split_is_bit_identical(kind):
             plan = nmspmm.make_plan(kind, tile, split)
             try:
                 nmspmm.workspace_size(plan, m, n)
-                if "k_gemm_rs" in nmspmm.plan_kernel_name(plan) and split > 1:
-                    continue  # the row-stationary layout takes split_k = 1 only
+                name = nmspmm.plan_kernel_name(plan)
+                if ("k_gemm_rs" in name or "k_gemm_ps" in name) and split > 1:
+                    continue  # the row-stationary and persistent layouts take split_k = 1 only
             except nmspmm.NmError:
                 continue
             print(f"kind {kind} tile {tile} split {split}", flush=True)
@@ -127,6 +128,32 @@ def test_every_tile_and_split_is_bit_identical(kind):
                 continue
             assert np.array_equal(Y, ref), (tile, split)
             gu.assert_f16_close(Yh, ref_h)
+
+
+@pytest.mark.parametrize("kind", [nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_SP42X2, nmspmm.NM_KIND_DENSE])
+@pytest.mark.parametrize("m,n,k", [(16500, 1028, 256), (20000, 516, 208), (300, 132, 384)])
+def test_persistent_tiles(kind, m, n, k):
+    # a fixed grid walking several tiles each (more tiles than workgroups for
+    # the first two shapes), ragged m and n, a dense k tail (k = 208)
+    N, M = {nmspmm.NM_KIND_SP42: (1, 4), nmspmm.NM_KIND_SP42X2: (3, 8), nmspmm.NM_KIND_DENSE: (8, 8)}[kind]
+    X, W, scale = _case(m, n, k, N, M, seed=kind * 5 + m)
+    ref = oracle.matmul_i8(X, W)
+    ref_h = oracle.dequant_f16(ref, scale)
+    packed = nmspmm.compress(W, N, M)
+    ran = 0
+    for tile in range(nmspmm.num_tiles()):
+        plan = nmspmm.make_plan(kind, tile, 1)
+        if "k_gemm_ps" not in nmspmm.plan_kernel_name(plan):
+            continue
+        print(f"persistent kind {kind} tile {tile} m={m} n={n} k={k}", flush=True)
+        if kind == nmspmm.NM_KIND_DENSE:
+            Y, Yh = gu.run_dense(X, W, scale, True, True, plan=plan)
+        else:
+            Y, Yh = gu.run_sparse(X, packed, scale, True, True, plan=plan)
+        assert np.array_equal(Y, ref), tile
+        gu.assert_f16_close(Yh, ref_h)
+        ran += 1
+    assert ran >= 2
 
 
 @pytest.mark.parametrize("kind", [nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_SP42X2, nmspmm.NM_KIND_DENSE])

@@ -53,8 +53,12 @@ def test_small_token_counts_split_the_reduction_inside_workgroups():
     d = nmspmm.compress_size(768, 3072, 2, 4)
     p = nmspmm.spmm_plan(d, 197, nmspmm.NM_OUT_I32)
     assert (p.tile_n, p.tile_m) == (32, 32) and p.split_k == 1 and p.grid >= 128
-    # ... but not when k is too short for four slices (DeiT-Tiny fc1, k = 192)
+    # ... and with two k-steps too (DeiT-Tiny fc1, k = 192)
     d = nmspmm.compress_size(768, 192, 2, 4)
+    p = nmspmm.spmm_plan(d, 197, nmspmm.NM_OUT_I32)
+    assert (p.tile_n, p.tile_m) == (32, 32)
+    # but not when 32 x 32 tiles would oversubscribe (DeiT-Base fc1 at batch 1)
+    d = nmspmm.compress_size(3072, 768, 2, 4)
     p = nmspmm.spmm_plan(d, 197, nmspmm.NM_OUT_I32)
     assert (p.tile_n, p.tile_m) == (64, 64)
 
@@ -65,10 +69,18 @@ def test_large_shapes_use_large_tiles():
     assert nmspmm.plan_kernel_name(p).startswith("k_gemm_rs")   # X resident, weight streamed
     d = nmspmm.compress_size(4096, 1024, 4, 8)
     p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)    # ViT-L fc1, two-stream weight
-    assert (p.tile_n, p.tile_m) == (256, 256)
+    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 2, 2, 4, 4, 2>"
     d = nmspmm.compress_size(768, 3072, 2, 4)
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # fc2 at batch 128
     assert (p.tile_n, p.tile_m) == (128, 128)
+    # medium token counts: half-height tiles, narrower for two-stream weights
+    d = nmspmm.compress_size(1152, 384, 2, 4)
+    assert (nmspmm.spmm_plan(d, 12608, 1).tile_n, nmspmm.spmm_plan(d, 12608, 1).tile_m) == (128, 64)
+    d = nmspmm.compress_size(1152, 384, 4, 8)
+    assert (nmspmm.spmm_plan(d, 12608, 1).tile_n, nmspmm.spmm_plan(d, 12608, 1).tile_m) == (64, 128)
+    # one or two k-steps: 64 x 64 tiles (Swin-B stage 1, k = 128)
+    d = nmspmm.compress_size(384, 128, 2, 4)
+    assert (nmspmm.spmm_plan(d, 100352, 1).tile_n, nmspmm.spmm_plan(d, 100352, 1).tile_m) == (64, 64)
 
 
 def test_forced_plan_validation():
