@@ -619,15 +619,16 @@ def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, comma
     if sq_dir:
         busy, active = counters(sq_dir, "SQ_VALU_MFMA_BUSY_CYCLES"), counters(sq_dir, "GRBM_GUI_ACTIVE")
         conf, lds = counters(sq_dir, "SQ_LDS_BANK_CONFLICT"), counters(sq_dir, "SQ_LDS_IDX_ACTIVE")
-        simds = 4 * int(line.get("cus", 256))
-        md += ["", f"Matrix cores and LDS per dispatch (one more pass: `--pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
-               f"SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE`).  MFMA busy = busy cycles / (active cycles x {simds} SIMDs); "
-               "LDS bank conflicts = conflict cycles / LDS active cycles:", "",
+        simds, xcds = 1024, 8   # MI355X: 256 CUs x 4 SIMDs, in 8 XCDs
+        md += ["", "Matrix cores and LDS per dispatch (one more pass: `--pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
+               "SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE`).  GRBM_GUI_ACTIVE is reported summed over the 8 XCDs, so "
+               f"MFMA busy = busy cycles / (GRBM_GUI_ACTIVE / {xcds} x {simds} SIMDs), the definition of rocprofv3's "
+               "MfmaUtil; LDS bank conflicts = conflict cycles / LDS active cycles:", "",
                "| kernel | dispatches | MFMA busy % | LDS conflict % |", "|---|---:|---:|---:|"]
         for k in sorted(busy, key=lambda k: -np.mean(busy[k])):
             if "nmspmm" not in k or k not in active:
                 continue
-            mb = 100.0 * np.mean(busy[k]) / (np.mean(active[k]) * simds)
+            mb = 100.0 * np.mean(busy[k]) / (np.mean(active[k]) / xcds * simds)
             lc = 100.0 * np.mean(conf[k]) / max(np.mean(lds[k]), 1.0) if k in conf and k in lds else float("nan")
             md.append(f"| `{k[:90]}` | {len(busy[k])} | {mb:.1f} | {lc:.2f} |")
     with open(out_md, "w") as f:

@@ -7,7 +7,7 @@ import oracle
 from paper_2607_12505_amd import nmspmm
 from paper_2607_12505_amd import workloads as wl
 
-PATTERNS = [(1, 4), (2, 4), (3, 4), (4, 4), (1, 8), (2, 8), (3, 8), (4, 8), (6, 8), (8, 8)]
+PATTERNS = [(1, 4), (2, 4), (3, 4), (4, 4)] + [(n, 8) for n in range(1, 9)]
 
 
 def decode_documented(vals, meta, d):

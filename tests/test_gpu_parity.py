@@ -17,7 +17,8 @@ import gpu_util as gu
 
 pytestmark = pytest.mark.gpu
 
-ALL_PATTERNS = [(1, 4), (2, 4), (3, 4), (4, 4), (1, 8), (2, 8), (3, 8), (4, 8), (5, 8), (8, 8)]
+# every N:4 and the whole N:8 family the layer-wise search draws from (N = 1 .. 8)
+ALL_PATTERNS = [(1, 4), (2, 4), (3, 4), (4, 4)] + [(n, 8) for n in range(1, 9)]
 
 
 @pytest.fixture(scope="module", autouse=True)
