@@ -245,7 +245,10 @@ def sweep(configs, torch, reps, out_path):
             Yhs = [torch.empty((g.m, g.n), dtype=torch.int16, device="cuda") if out & 2 else None for _ in range(nsets)]
             ws = torch.zeros(64 << 20, dtype=torch.uint8, device="cuda")
             times = {}
-            for tile in range(nmspmm.num_tiles()):
+            # two passes over the candidates, keeping each one's faster mean:
+            # a candidate slowed once by a transient (clock, co-runner) is not
+            # mistaken for a slow schedule
+            for tile in list(range(nmspmm.num_tiles())) * 2:
                 tn_, tm_ = nmspmm.tile_info(tile)
                 tiles = -(-g.n // tn_) * -(-g.m // tm_)
                 for split in (1, 2, 4, 8):
@@ -271,7 +274,8 @@ def sweep(configs, torch, reps, out_path):
                         run(r % nsets)
                     e1.record()
                     torch.cuda.synchronize()
-                    times[(tile, split)] = e0.elapsed_time(e1) / reps * 1e3
+                    t_us = e0.elapsed_time(e1) / reps * 1e3
+                    times[(tile, split)] = min(t_us, times.get((tile, split), t_us))
             best = min(times, key=times.get)
             chosen = (planned.tile, planned.split_k)
             t_plan = times.get(chosen)
@@ -528,7 +532,8 @@ def write_sweep_report(sweep_json, path):
     s = d["summary"]
     md = ["# Planner evaluation (Table-1 methodology) on MI355X", "",
           "Commands: `python3 bench.py --sweep 0,1,2,3,4 --sweep-out sweep.json` (GPU; every (tile, split_k) "
-          "candidate timed, 10 launches each, outputs rotated over buffers larger than the 256 MB last-level cache), "
+          "candidate timed in two passes of 10 launches each, the faster pass kept, outputs rotated over buffers "
+          "larger than the 256 MB last-level cache), "
           "then `python3 bench.py --sweep-report sweep.json --report <this file>`.", "",
           "Normalised performance = t(sweep optimum) / t(planner choice); tile indices are those of the "
           "library's tile table (`nm_tile_info`).", "",

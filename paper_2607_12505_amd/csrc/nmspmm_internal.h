@@ -18,9 +18,9 @@ constexpr int kMBlock = 256;     // packed position bytes per (fragment, k-step,
 constexpr int kThreads = 256;    // threads per workgroup (4 waves of 64)
 
 // Kernel layouts of a workgroup tile.
-//   kOutSplit:  WN x WM waves, each owning FN x FM fragments of 16 x 16
-//               outputs (tile_n = WN * FN * 16 channels, tile_m = WM * FM * 16
-//               tokens); one output tile per workgroup.
+//   kOutSplit:  WN x WM waves (4 or 8), each owning FN x FM fragments of
+//               16 x 16 outputs (tile_n = WN * FN * 16 channels, tile_m = WM *
+//               FM * 16 tokens); one output tile per workgroup.
 //   kKSliced:   every wave computes the whole FN x FM-fragment tile over a
 //               quarter of the k-steps (wn = wm = 1); one tile per workgroup.
 //   kRowStat:   2 x 2 consumer waves as kOutSplit plus one producer wave; the
@@ -61,6 +61,8 @@ constexpr TileCfg kTiles[] = {
     {2, 2, 4, 2, 2, kOutSplit},  // 17: 128 ch x  64 tok, 2-slot ring
     {2, 2, 2, 4, 2, kOutSplit},  // 18:  64 ch x 128 tok, 2-slot ring
     {2, 2, 2, 2, 2, kOutSplit},  // 19:  64 ch x  64 tok, 2-slot ring
+    {2, 4, 8, 4, 3, kOutSplit},  // 20: 256 ch x 256 tok, 8 waves (2 x 4), 3-slot ring
+    {2, 4, 8, 2, 2, kOutSplit},  // 21: 256 ch x 128 tok, 8 waves, 2-slot ring
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
@@ -93,7 +95,7 @@ inline size_t outsplit_lds(int kind, const TileCfg &t) {
     const size_t slot = BM * 128 + (sparse ? (BN / 16) * S * (kVBlock + kMBlock) : BN * 128);
     const size_t cap = kLdsPerCu - 1024;
     const size_t ring = (size_t)t.nst * slot <= cap ? (size_t)t.nst : cap / slot;
-    const size_t epi = (size_t)4 * 16 * (t.fn * 64 + 16);
+    const size_t epi = (size_t)t.wn * t.wm * 16 * (t.fn * 64 + 16);
     return ring * slot > epi ? ring * slot : epi;
 }
 

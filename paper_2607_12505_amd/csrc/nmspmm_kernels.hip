@@ -219,6 +219,7 @@ __device__ inline bool arrive_last(const GemmArgs &a, int tile, int *s_flag) {
 template <int KIND, int WN_, int WM_, int FN_, int FM_, int NST>
 struct Geometry {
     static constexpr int WN = WN_, WM = WM_, FN = FN_, FM = FM_;
+    static constexpr int NW = WN * WM;                               // waves per workgroup (4 or 8)
     static constexpr int BN = WN * FN * 16;
     static constexpr int BM = WM * FM * 16;
     static constexpr bool kSparse = KIND != NM_KIND_DENSE;
@@ -227,27 +228,27 @@ struct Geometry {
     static constexpr int WVB = kSparse ? (BN / 16) * S * kVBlock : BN * 128;  // weight value bytes
     static constexpr int WMB = kSparse ? (BN / 16) * S * kMBlock : 0;         // weight position bytes
     static constexpr int SLOT = XB + WVB + WMB;
-    static constexpr int XI = BM / 32;                               // X loads per wave per k-step
-    static constexpr int WI = kSparse ? (BN / 16) * S / 4 * 2 : BN / 32;      // weight loads per wave
+    static constexpr int XI = BM / (8 * NW);                         // X loads per wave per k-step
+    static constexpr int WI = kSparse ? (BN / 16) * S / NW * 2 : BN / (8 * NW);  // weight loads per wave
     static constexpr int DMA = XI + WI;
     static constexpr int CPR = FN * 4;                               // 4-channel chunks per staged row
     static constexpr int RPI = 64 / CPR;                             // staged rows read per instruction
     static constexpr int ROWB = FN * 64 + 16;                        // padded bytes per staged int32 row
-    static constexpr int EPI = 4 * 16 * ROWB;
+    static constexpr int EPI = NW * 16 * ROWB;
     // ring depth: as asked, or as deep as 160 KB of LDS allows
     static constexpr int RING = NST * SLOT <= 160 * 1024 - 1024 ? NST : (160 * 1024 - 1024) / SLOT;
     static constexpr int LDSB = RING * SLOT > EPI ? RING * SLOT : EPI;
-    static_assert(WN * WM == 4 && RING >= 2 && 64 % CPR == 0 && BM % 32 == 0, "tile shape");
-    static_assert(!kSparse || ((BN / 16) * S) % 4 == 0, "weight blocks split evenly over 4 waves");
+    static_assert((NW == 4 || NW == 8) && RING >= 2 && 64 % CPR == 0 && BM % (8 * NW) == 0, "tile shape");
+    static_assert(kSparse ? ((BN / 16) * S) % NW == 0 : BN % (8 * NW) == 0, "weight loads split evenly over the waves");
     static_assert(LDSB <= 160 * 1024, "LDS budget");
 };
 
-// The stages of an output-split tile (4 waves, each FN x FM accumulators of a
-// WN x WM arrangement), shared by the one-tile-per-workgroup kernel and the
+// The stages of an output-split tile (WN x WM waves, each FN x FM
+// accumulators), shared by the one-tile-per-workgroup kernel and the
 // persistent one.
 template <class G>
 struct OutSplit {
-    static constexpr int BN = G::BN, BM = G::BM, S = G::S, FN = G::FN, FM = G::FM;
+    static constexpr int BN = G::BN, BM = G::BM, S = G::S, FN = G::FN, FM = G::FM, NW = G::NW;
 
     // Fill ring slot st with k-step s of the tile at (tok0, ch0).  Rows of X
     // past m, and weight rows past n, read a valid row instead: their outputs
@@ -259,17 +260,17 @@ struct OutSplit {
         const uint32_t slot = lds0 + st * G::SLOT;
 #pragma unroll
         for (int j = 0; j < G::XI; ++j) {
-            const int r = 8 * (4 * j + wave) + (lane >> 3);
+            const int r = 8 * (NW * j + wave) + (lane >> 3);
             const int c = (lane & 7) ^ (r & 7);
             const int tok = tok0 + r < a.m ? tok0 + r : a.m - 1;
             const int kk = s * 128 + c * 16 < a.k ? s * 128 + c * 16 : a.k - 16;
-            dma16(a.X + (size_t)tok * a.k + kk, slot + (4 * j + wave) * 1024);
+            dma16(a.X + (size_t)tok * a.k + kk, slot + (NW * j + wave) * 1024);
         }
         if constexpr (G::kSparse) {
             const int f0 = ch0 >> 4;
 #pragma unroll
-            for (int j = 0; j < (BN / 16) * S / 4; ++j) {
-                const int bl = 4 * j + wave;               // weight block of the slot: fragment bl / S, stream bl % S
+            for (int j = 0; j < (BN / 16) * S / NW; ++j) {
+                const int bl = NW * j + wave;              // weight block of the slot: fragment bl / S, stream bl % S
                 int f = f0 + bl / S;
                 f = f < a.n_frags ? f : a.n_frags - 1;
                 const size_t b = ((size_t)f * a.k_steps + s) * S + bl % S;
@@ -279,23 +280,23 @@ struct OutSplit {
         } else {
             if (s * 128 + 128 <= a.k) {
 #pragma unroll
-                for (int j = 0; j < BN / 32; ++j) {
-                    const int r = 8 * (4 * j + wave) + (lane >> 3);
+                for (int j = 0; j < BN / (8 * NW); ++j) {
+                    const int r = 8 * (NW * j + wave) + (lane >> 3);
                     const int c = (lane & 7) ^ (r & 7);
                     const int row = ch0 + r < a.n ? ch0 + r : a.n - 1;
-                    dma16(a.A + (size_t)row * a.k + s * 128 + c * 16, slot + G::XB + (4 * j + wave) * 1024);
+                    dma16(a.A + (size_t)row * a.k + s * 128 + c * 16, slot + G::XB + (NW * j + wave) * 1024);
                 }
             } else {
                 // tail k-step of a dense weight: plain loads, zeros past k
 #pragma unroll
-                for (int j = 0; j < BN / 32; ++j) {
-                    const int r = 8 * (4 * j + wave) + (lane >> 3);
+                for (int j = 0; j < BN / (8 * NW); ++j) {
+                    const int r = 8 * (NW * j + wave) + (lane >> 3);
                     const int c = (lane & 7) ^ (r & 7);
                     const int row = ch0 + r < a.n ? ch0 + r : a.n - 1;
                     const int kk = s * 128 + c * 16;
                     v4i v = v4i{0, 0, 0, 0};
                     if (kk < a.k) v = *(const v4i *)(a.A + (size_t)row * a.k + kk);
-                    *(v4i *)(lds + st * G::SLOT + G::XB + (4 * j + wave) * 1024 + lane * 16) = v;
+                    *(v4i *)(lds + st * G::SLOT + G::XB + (NW * j + wave) * 1024 + lane * 16) = v;
                 }
             }
         }
@@ -394,7 +395,7 @@ struct OutSplit {
 };
 
 template <int KIND, int WN, int WM, int FN, int FM, int NST>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+__global__ __launch_bounds__(64 * WN * WM) void k_gemm(GemmArgs a) {
     using G = Geometry<KIND, WN, WM, FN, FM, NST>;
     using O = OutSplit<G>;
     constexpr int BN = G::BN, BM = G::BM;
@@ -472,7 +473,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 // extra stores in flight can only make a wait longer, never let it pass
 // early.
 template <int KIND, int WN, int WM, int FN, int FM, int NST>
-__global__ __launch_bounds__(256) void k_gemm_ps(GemmArgs a) {
+__global__ __launch_bounds__(64 * WN * WM) void k_gemm_ps(GemmArgs a) {
     using G = Geometry<KIND, WN, WM, FN, FM, NST>;
     using O = OutSplit<G>;
     constexpr int BN = G::BN, BM = G::BM;
@@ -944,10 +945,10 @@ int launch_one(const GemmArgs &args, int grid, void *stream) {
         hipLaunchKernelGGL((k_gemm_ks<KIND, t.fn, t.fm, t.nst>), dim3(grid), dim3(kThreads), 0,
                            (hipStream_t)stream, args);
     else if constexpr (t.layout == kPersist)
-        hipLaunchKernelGGL((k_gemm_ps<KIND, t.wn, t.wm, t.fn, t.fm, t.nst>), dim3(grid), dim3(kThreads), 0,
+        hipLaunchKernelGGL((k_gemm_ps<KIND, t.wn, t.wm, t.fn, t.fm, t.nst>), dim3(grid), dim3(64 * t.wn * t.wm), 0,
                            (hipStream_t)stream, args);
     else
-        hipLaunchKernelGGL((k_gemm<KIND, t.wn, t.wm, t.fn, t.fm, t.nst>), dim3(grid), dim3(kThreads), 0,
+        hipLaunchKernelGGL((k_gemm<KIND, t.wn, t.wm, t.fn, t.fm, t.nst>), dim3(grid), dim3(64 * t.wn * t.wm), 0,
                            (hipStream_t)stream, args);
     return (int)hipGetLastError();
 }

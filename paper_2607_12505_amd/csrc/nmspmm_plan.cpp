@@ -90,8 +90,8 @@ nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *p) {
 }
 
 // Tile indices used by the rules below (see kTiles).
-constexpr int kT64x64 = 6, kT32x32ks = 10, kT128x128rs = 11;
-constexpr int kT128x128r2 = 16, kT128x64r2 = 17, kT64x128r2 = 18, kT64x64r2 = 19;
+constexpr int kT64x64 = 6, kT32x32ks = 10;
+constexpr int kT128x128r2 = 16, kT128x64r2 = 17, kT64x128r2 = 18, kT64x64r2 = 19, kT256x256w8 = 20;
 
 static int64_t tiles_of(int t, int m, int n) {
     return ceil_div(n, kTiles[t].tile_n()) * ceil_div(m, kTiles[t].tile_m());
@@ -123,13 +123,13 @@ nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *
     } else if (tiles_of(kT128x128r2, mm, n) < 4 * cus) {
         // Medium: half-height tiles (narrower for the heavier operands).
         tile = heavy ? kT64x128r2 : kT128x64r2;
+    } else if (tiles_of(kT256x256w8, mm, n) >= 4 * cus && k_steps <= 8) {
+        // Large outputs with a short reduction: 256 x 256 tiles on 8 waves
+        // halve the operand traffic per output and keep enough waves per CU
+        // to read the operands from LDS fast enough.
+        tile = kT256x256w8;
     } else {
-        // Large: keep X resident and stream the weight when the token block
-        // fits in LDS (short k, one-stream weights) and there are many tiles;
-        // else 128 x 128 tiles.
-        const bool rs_fits = rowstat_lds(kind, kTiles[kT128x128rs], k_steps).total <= kLdsPerCu;
-        const bool many = ceil_div(n, 256) * ceil_div(mm, 256) >= 4 * cus;
-        tile = (!heavy && k_steps <= 6 && rs_fits && many) ? kT128x128rs : kT128x128r2;
+        tile = kT128x128r2;
     }
     plan->kind = kind;
     plan->tile = tile;

@@ -66,10 +66,10 @@ def test_small_token_counts_split_the_reduction_inside_workgroups():
 def test_large_shapes_use_large_tiles():
     d = nmspmm.compress_size(3072, 768, 2, 4)
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # DeiT-Base fc1 at batch 128
-    assert nmspmm.plan_kernel_name(p).startswith("k_gemm_rs")   # X resident, weight streamed
+    assert nmspmm.plan_kernel_name(p) == "k_gemm<1, 2, 4, 8, 4, 3>"   # 256 x 256 on 8 waves
     d = nmspmm.compress_size(4096, 1024, 4, 8)
     p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)    # ViT-L fc1, two-stream weight
-    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 2, 2, 4, 4, 2>"
+    assert (p.tile_n, p.tile_m) == (256, 256) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 2, 4, 8, 4, 3>"
     d = nmspmm.compress_size(768, 3072, 2, 4)
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # fc2 at batch 128
     assert (p.tile_n, p.tile_m) == (128, 128)
