@@ -180,6 +180,34 @@ def time_each(preps, torch, reps=5):
     return out
 
 
+def secondary_workload(cfg, steps, warmup, torch):
+    """Speedup over the dense baseline per (token count, N:M) on another
+    workload (same protocol as the main measurement, fewer steps); reported
+    beside the main line, never folded into its value."""
+    work = wl.workload(cfg)
+    xd, xh = {}, {}
+    preps = [Prepared(cfg, g, xd, xh, work.out_int32, work.out_f16, torch, use_dense_kernel=(g.N == g.M))
+             for g in work.gemms]
+    torch.cuda.synchronize()
+    sleep_cycles = int(2.4e9 * 25e-6 * len(preps) * 2)
+    groups = launch_groups(preps)
+    time_steps(preps, groups, max(1, warmup), torch, sleep_cycles)
+    each = np.zeros((len(preps), 2))
+    for _ in range(steps):
+        each += time_each(preps, torch, reps=3)
+    each /= steps
+    out = {}
+    for key in sorted({(p.g.m, pattern_name(p.g)) for p in preps}):
+        sel = [i for i, p in enumerate(preps) if (p.g.m, pattern_name(p.g)) == key]
+        ops = sum(preps[i].g.dense_eq_ops for i in sel)
+        ts, td = each[sel, 0].sum(), each[sel, 1].sum()
+        out[f"m={key[0]} {key[1]}"] = {"tops": round(ops / (ts * 1e-3) / 1e12, 1),
+                                        "speedup_vs_dense": round(float(td / ts), 3)}
+    del preps
+    torch.cuda.empty_cache()
+    return {"workload": work.name, "outputs": "int32", "per_batch_pattern": out}
+
+
 def cpu_baseline(preps, budget_s, check):
     """The oracle (plain C, all host threads) on the first rows of every GEMM
     of the workload; the row fraction is sized to about budget_s seconds."""
@@ -654,6 +682,8 @@ def main():
     ap.add_argument("--config", type=int, default=1, help="0..4 (default 1: DeiT-Small linears, batch 64)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the DeiT-Base per-batch speedups reported beside the main line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after timing, run one plain device copy of MIB MiB (profiler counter calibration)")
     ap.add_argument("--sweep", type=str, default=None,
@@ -825,6 +855,9 @@ def main():
         "dense_ms_per_step": round(float(dense_ms), 4),
         "roofline": roofline,
     }
+    if not args.no_secondary and args.config != 2:
+        line["deit_base_speedups"] = secondary_workload(2, 3, 2, torch)
+        log(json.dumps(line["deit_base_speedups"]))
     if args.copy_calibration:
         # a plain elementwise pass that reads and writes exactly MIB MiB each
         n = args.copy_calibration * (1 << 20) // 4
