@@ -40,7 +40,8 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
         (o.yh && !aligned16(o.yh)) || (o.yh && !aligned16(o.scale)) || (o.yq && !aligned16(o.yq)) ||
         (o.yq && !aligned16(o.qscale)))
         return NM_ERR_ARG;
-    if ((int64_t)m * n > ((int64_t)1 << 40)) return NM_ERR_SHAPE;
+    // outputs are addressed with 32-bit byte offsets (int32: 4 bytes per element)
+    if ((int64_t)m * n >= ((int64_t)1 << 29)) return NM_ERR_SHAPE;
     nm_plan plan;
     if (forced) {
         plan = *forced;

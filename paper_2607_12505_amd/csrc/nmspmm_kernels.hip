@@ -135,24 +135,38 @@ struct EpiScale {
     v4f qs;   // requantisation (int8 output)
 };
 
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
 // Writes 4 consecutive channels of one token: int32, fp16(fp32(y) * scale)
 // and/or the int8 code q8(fp32(y) * qscale), whichever outputs are present.
+// Buffer stores with a 32-bit element offset (outputs hold fewer than 2^29
+// elements, checked on the host): the per-lane address is one 32-bit
+// multiply-add instead of 64-bit pointer arithmetic, and the hardware drops
+// any write past the end of an output.
 __device__ inline void emit_out(const GemmArgs &a, int tok, int ch, const v4i &v, const EpiScale &es) {
-    if (a.Y) *(v4i *)(a.Y + (size_t)tok * a.n + ch) = v;
+    const uint32_t e = (uint32_t)tok * (uint32_t)a.n + (uint32_t)ch;
+    const uint32_t elems = (uint32_t)a.m * (uint32_t)a.n;
+    if (a.Y) {
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(a.Y, 0, (int)(elems * 4), kBufferFlags);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, v), r, (int)(e * 4), 0, 0);
+    }
     if (a.Yh) {
         v4u16 h;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const _Float16 x = (_Float16)((float)v[e] * es.sc[e]);
-            h[e] = __builtin_bit_cast(unsigned short, x);
+        for (int i = 0; i < 4; ++i) {
+            const _Float16 x = (_Float16)((float)v[i] * es.sc[i]);
+            h[i] = __builtin_bit_cast(unsigned short, x);
         }
-        *(v4u16 *)(a.Yh + (size_t)tok * a.n + ch) = h;
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(a.Yh, 0, (int)(elems * 2), kBufferFlags);
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u, h), r, (int)(e * 2), 0, 0);
     }
     if (a.Yq) {
         uint32_t packed = 0;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) packed |= (uint32_t)(q8((float)v[e] * es.qs[e]) & 0xFF) << (8 * e);
-        *(uint32_t *)(a.Yq + (size_t)tok * a.n + ch) = packed;
+        for (int i = 0; i < 4; ++i) packed |= (uint32_t)(q8((float)v[i] * es.qs[i]) & 0xFF) << (8 * i);
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(a.Yq, 0, (int)elems, kBufferFlags);
+        __builtin_amdgcn_raw_buffer_store_b32(packed, r, (int)e, 0, 0);
     }
 }
 
