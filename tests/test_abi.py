@@ -44,3 +44,27 @@ def test_struct_sizes_match_header():
     # nm_outputs: 5 pointers; nm_search_params: 4 int32 + 1 uint64
     assert ctypes.sizeof(nmspmm.NmOutputs) == 40
     assert ctypes.sizeof(nmsearch.NmSearchParams) == 24
+
+
+def test_host_side_argument_checks_need_no_gpu():
+    # These calls are rejected before any HIP call, so fake (aligned, non-null)
+    # pointers are never dereferenced.
+    L = nmspmm.lib()
+    fake = ctypes.c_void_p(1 << 20)
+    nul = ctypes.c_void_p(0)
+    args = lambda m, n, Y, Yh: (fake, m, fake, n, 128, Y, fake, Yh, nul, 0, nul, None)
+    assert L.nm_gemm_i8_dense_ex(*args(-1, 64, fake, nul)) == nmspmm.NM_ERR_SHAPE
+    assert L.nm_gemm_i8_dense_ex(*args(0, 64, nul, nul)) == nmspmm.NM_OK           # m == 0: nothing examined
+    assert L.nm_gemm_i8_dense_ex(*args(64, 64, nul, nul)) == nmspmm.NM_ERR_ARG     # no output
+    assert L.nm_gemm_i8_dense_ex(*args(64, 66, fake, nul)) == nmspmm.NM_ERR_SHAPE  # n % 4 != 0
+    # outputs are addressed with 32-bit byte offsets: m * n must stay below 2^29
+    assert L.nm_gemm_i8_dense_ex(*args(1 << 20, 512, fake, nul)) == nmspmm.NM_ERR_SHAPE
+    misaligned = ctypes.c_void_p((1 << 20) + 4)
+    assert L.nm_gemm_i8_dense_ex(fake, 64, fake, 64, 128, misaligned, fake, nul, nul, 0, nul, None) == \
+        nmspmm.NM_ERR_ARG
+    o = nmspmm.NmOutputs(None, None, None, (1 << 20), None)                         # int8 output without qscale
+    d = nmspmm.compress_size(64, 128, 2, 4)
+    assert L.nm_spmm_out(fake, 64, fake, fake, ctypes.byref(d), ctypes.byref(o), nul, 0, nul, None) == \
+        nmspmm.NM_ERR_ARG
+    assert L.nm_quantize_f16(fake, -1, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_SHAPE
+    assert L.nm_quantize_f16(misaligned, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_ARG
