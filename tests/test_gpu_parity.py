@@ -223,6 +223,33 @@ def test_workspace_shared_by_plans_of_growing_size():
 
 # ---------------------------------------------------------------- edge cases and errors
 
+@pytest.mark.parametrize("m,n,k", [(1, 4, 16), (3, 8, 32), (2, 20, 48), (5, 4, 4096)])
+@pytest.mark.parametrize("N,M", [(1, 4), (2, 4), (4, 8), (7, 8), (8, 8)])
+def test_smallest_shapes(m, n, k, N, M):
+    # the smallest legal n (4) and k (16), one-token inputs, a single output
+    # fragment padded from 4 rows, and a long reduction onto 4 channels
+    print(f"smallest {N}:{M} m={m} n={n} k={k}", flush=True)
+    X, W, scale = _case(m, n, k, N, M, seed=m + n + k + N)
+    ref = oracle.matmul_i8(X, W)
+    if N == M:
+        Y, Yh = gu.run_dense(X, W, scale, True, True)
+    else:
+        Y, Yh = gu.run_sparse(X, nmspmm.compress(W, N, M), scale, True, True)
+    assert np.array_equal(Y, ref)
+    gu.assert_f16_close(Yh, oracle.dequant_f16(ref, scale))
+
+
+def test_all_zero_weight_and_input():
+    # degenerate operands: every window empty, or every activation zero
+    m, n, k = 130, 72, 256
+    X, W, scale = _case(m, n, k, 2, 8, seed=9)
+    Wz = np.zeros_like(W)
+    Y, _ = gu.run_sparse(X, nmspmm.compress(Wz, 2, 8), scale, True, False)
+    assert (Y == 0).all()
+    Y, _ = gu.run_sparse(np.zeros_like(X), nmspmm.compress(W, 2, 8), scale, True, False)
+    assert (Y == 0).all()
+
+
 def test_zero_tokens_is_a_noop():
     torch = gu.torch()
     packed = nmspmm.compress(np.zeros((16, 128), np.int8), 2, 4)
