@@ -554,6 +554,63 @@ def chaining_experiment(torch, report):
     return res
 
 
+def paper_grid(torch, report):
+    """The paper's kernel benchmark grid (Sec. 6.1): tokens m in {64, 128, 256,
+    512}, n and k in {128, 256, 512, 1024}, sparsity 50 / 75 / 87.5 % (2:4 and
+    4:8 / 1:4 and 2:8 / 1:8).  Each case: this library's sparse GEMM, its dense
+    MFMA GEMM, and the vendor dense INT8 GEMM (hipBLASLt through
+    torch._int_mm, a measured reference only), int32 output, mean of 50
+    back-to-back runs."""
+    from paper_2607_12505_amd import latency as lt
+    sizes = (128, 256, 512, 1024)
+    rows = []
+    for m in (64, 128, 256, 512):
+        for n in sizes:
+            for k in sizes:
+                rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([6, m, n, k])))
+                X = torch.from_numpy(wl.gen_x(m, k, rng)).cuda()
+                Y = torch.empty((m, n), dtype=torch.int32, device="cuda")
+                Wd_host, _ = wl.gen_w(n, k, 8, 8, rng)
+                Wd = torch.from_numpy(Wd_host).cuda()
+                WdT = Wd.t().contiguous()
+                t_dense = lt.time_launches(torch, lambda: nmspmm.gemm_i8_dense(X, Wd, Y=Y), 50)
+                t_vendor = lt.time_launches(torch, lambda: torch._int_mm(X, WdT), 50)
+                for (N, M), spars in (((2, 4), 50), ((4, 8), 50), ((1, 4), 75), ((2, 8), 75), ((1, 8), 87.5)):
+                    W, _ = wl.gen_w(n, k, N, M, rng)
+                    dw = nmspmm.DeviceWeight.from_packed(nmspmm.compress(W, N, M))
+                    t_sp = lt.time_launches(torch, lambda: nmspmm.spmm(X, dw, Y=Y), 50)
+                    rows.append({"m": m, "n": n, "k": k, "pattern": f"{N}:{M}", "sparsity": spars,
+                                 "sparse_us": round(t_sp, 2), "dense_us": round(t_dense, 2),
+                                 "vendor_us": round(t_vendor, 2)})
+        log(f"grid m={m} done")
+    summary = {}
+    for key in ("50", "75", "87.5", "all"):
+        sel = [r for r in rows if key == "all" or float(r["sparsity"]) == float(key)]
+        summary[key] = {
+            "cases": len(sel),
+            "mean_speedup_vs_own_dense": round(float(np.mean([r["dense_us"] / r["sparse_us"] for r in sel])), 3),
+            "mean_speedup_vs_vendor_dense": round(float(np.mean([r["vendor_us"] / r["sparse_us"] for r in sel])), 3),
+        }
+    log(json.dumps(summary))
+    if report:
+        md = ["# The paper's kernel benchmark grid on MI355X", "",
+              "Command: `python3 bench.py --paper-grid --report profiles/paper_grid.md` (repository root).  Tokens m in "
+              "{64, 128, 256, 512}, n and k in {128, 256, 512, 1024}; 50 % = 2:4 and 4:8, 75 % = 1:4 and 2:8, 87.5 % "
+              "= 1:8; int32 output; mean of 50 back-to-back runs with inputs resident (HIP events).  \"vendor\" = the "
+              "dense INT8 GEMM of hipBLASLt through torch._int_mm, timed as a reference.", "",
+              "| sparsity | cases | mean speedup vs this library's dense MFMA GEMM | mean speedup vs the vendor dense GEMM |",
+              "|---|---:|---:|---:|"]
+        for key, v in summary.items():
+            md.append(f"| {key} | {v['cases']} | {v['mean_speedup_vs_own_dense']} | {v['mean_speedup_vs_vendor_dense']} |")
+        md += ["", "| m | n | k | pattern | sparse us | dense us | vendor dense us |", "|---:|---:|---:|---|---:|---:|---:|"]
+        for r in rows:
+            md.append(f"| {r['m']} | {r['n']} | {r['k']} | {r['pattern']} | {r['sparse_us']} | {r['dense_us']} | "
+                      f"{r['vendor_us']} |")
+        with open(report, "w") as f:
+            f.write("\n".join(md) + "\n")
+    return {"summary": summary, "rows": len(rows)}
+
+
 def write_sweep_report(sweep_json, path):
     """Markdown table of a planner evaluation written by --sweep-out."""
     d = json.load(open(sweep_json))
@@ -703,6 +760,8 @@ def main():
     ap.add_argument("--commands", type=str, default=None, help="file with the profiling commands to quote")
     ap.add_argument("--predictor", action="store_true",
                     help="latency LUT + Eq. 1 calibration + Algorithm 1 on ViT-L (prints one JSON line)")
+    ap.add_argument("--paper-grid", action="store_true",
+                    help="the paper's kernel benchmark grid vs the dense GEMMs (prints one JSON line)")
     ap.add_argument("--chaining", action="store_true",
                     help="int8 requantisation epilogue and activation quantiser timings (prints one JSON line)")
     ap.add_argument("--cal", type=int, default=64, help="calibration configurations for --predictor")
@@ -736,6 +795,9 @@ def main():
         return
     if args.chaining:
         print(json.dumps({"chaining": chaining_experiment(torch, args.report)}), flush=True)
+        return
+    if args.paper_grid:
+        print(json.dumps({"paper_grid": paper_grid(torch, args.report)}), flush=True)
         return
     if args.predictor:
         print(json.dumps({"predictor": predictor_experiment(torch, args.cal, args.test, args.report)}), flush=True)
