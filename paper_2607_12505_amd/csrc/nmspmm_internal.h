@@ -15,7 +15,7 @@ constexpr int kFragRows = 16;    // rows (output channels) per MFMA fragment
 constexpr int kKStep = 128;      // dense-equivalent k per structured-sparse MFMA
 constexpr int kVBlock = 1024;    // packed value bytes per (fragment, k-step, stream)
 constexpr int kMBlock = 256;     // packed position bytes per (fragment, k-step, stream)
-constexpr int kThreads = 256;    // threads per workgroup (4 waves of 64)
+constexpr int kThreads = 256;    // threads of a k-sliced workgroup (4 waves of 64)
 
 // Kernel layouts of a workgroup tile.
 //   kOutSplit:  WN x WM waves (4 or 8), each owning FN x FM fragments of

@@ -1,14 +1,15 @@
 // GEMM kernels of libnmspmm for gfx950 (CDNA4): Y = X W^T in int8 with int32
-// accumulation, optional per-channel fp16 dequantisation.
+// accumulation, optional per-channel fp16 dequantisation and int8
+// requantisation; and the binary16 -> int8 activation quantiser.
 //
 // Orientation: the weight is the A operand and the activations the B operand
 // of the matrix instruction, so a 16 x 16 accumulator holds 16 output channels
 // x 16 tokens.  This orientation is forced by the structured-sparse
 // instruction, whose sparse operand is A.
 //
-// Dataflow of one workgroup (4 waves) over its k range, one 128-wide k-step at
-// a time (paper Sec. 4.2: sparse handling confined to packed loading, the
-// compute stage purely matrix-instruction based):
+// Dataflow of one workgroup (4 or 8 waves) over its k range, one 128-wide
+// k-step at a time (paper Sec. 4.2: sparse handling confined to packed
+// loading, the compute stage purely matrix-instruction based):
 //   - every operand byte reaches LDS through the direct-to-LDS 16-byte (and
 //     4-byte) loads of gfx950, into a ring of NST k-step slots filled NST-1
 //     steps ahead of the compute: the tile_m x 128 slice of X, and the weight
@@ -26,7 +27,7 @@
 //     reused by all FN weight fragments;
 //   - the epilogue goes back through LDS, 16 tokens at a time, so that every
 //     store instruction writes whole rows of the wave's tile: 16 lanes cover
-//     256 contiguous bytes of int32 (128 of fp16) per token;
+//     256 contiguous bytes of int32 (128 of fp16, 64 of int8) per token;
 //   - split-K (Sec. 4.3): every split runs the same code on its k range and
 //     stores its int32 partial tile; the last split to arrive at a tile
 //     (atomic counter) adds the partials and runs the epilogue, so merging
