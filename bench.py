@@ -639,9 +639,15 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_12505_amd", "csrc", "nmspmm_kerne
 
 
 def kernel_source_sha256():
+    """SHA-256 of the kernel source with comments and blank space removed, so
+    that a counter record stays valid across edits that change no code."""
     import hashlib
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    import re
+    src = open(KERNEL_SOURCE).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    src = re.sub(r"\s+", " ", src).strip()
+    return hashlib.sha256(src.encode()).hexdigest()
 
 
 def default_traffic_path(workload_name):

@@ -61,7 +61,10 @@ constexpr int kBufferFlags = 0x00020000;
 constexpr int kSc1 = 16;
 
 // Direct-to-LDS loads: lane L's bytes land at lds_base + L * size.  lds_base
-// must be wave-uniform (it goes through M0).
+// must be wave-uniform (it goes through M0).  M0 is a register the compiler
+// reserves, so it warns that the clobber below may not be honoured; the
+// generated code of these kernels uses M0 nowhere else (LDS instructions do
+// not need it on gfx950), so nothing live is overwritten.
 __device__ inline void dma16(const void *g, uint32_t lds_base) {
     asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_base) : "memory", "m0");
 }
