@@ -194,7 +194,8 @@ nm_status nm_workspace_init(void *ws, size_t bytes, void *stream);
  *          may be NULL when the plan needs none)
  *   stream hipStream_t or NULL
  * m == 0 is a valid no-op (no pointer is examined, nothing is launched).  Errors: NM_ERR_ARG, NM_ERR_SHAPE (m < 0 or an
- * m·n >= 2^29: outputs are addressed with 32-bit byte offsets), NM_ERR_WORKSPACE,
+ * m·n >= 2^29, m·k >= 2^32 or a weight of 2^32 bytes or more: outputs, X and the
+ * weight are addressed with 32-bit byte offsets), NM_ERR_WORKSPACE,
  * NM_ERR_HIP. */
 nm_status nm_spmm(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
                   const nm_desc *desc, int32_t *Y, const float *scale, uint16_t *Yh,

@@ -40,8 +40,11 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
         (o.yh && !aligned16(o.yh)) || (o.yh && !aligned16(o.scale)) || (o.yq && !aligned16(o.yq)) ||
         (o.yq && !aligned16(o.qscale)))
         return NM_ERR_ARG;
-    // outputs are addressed with 32-bit byte offsets (int32: 4 bytes per element)
+    // outputs, X and the weight are addressed with 32-bit byte offsets
     if ((int64_t)m * n >= ((int64_t)1 << 29)) return NM_ERR_SHAPE;
+    if ((int64_t)m * k >= ((int64_t)1 << 32)) return NM_ERR_SHAPE;
+    const int64_t w_bytes = kind == NM_KIND_DENSE ? (int64_t)n * k : (int64_t)n_frags * k_steps * 2 * kVBlock;
+    if (w_bytes >= ((int64_t)1 << 32)) return NM_ERR_SHAPE;
     nm_plan plan;
     if (forced) {
         plan = *forced;

@@ -71,6 +71,16 @@ __device__ inline void dma16(const void *g, uint32_t lds_base) {
 __device__ inline void dma4(const void *g, uint32_t lds_base) {
     asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_base) : "memory", "m0");
 }
+// The same with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane
+// byte offset: no per-lane 64-bit address arithmetic.
+__device__ inline void dma16o(const void *base, uint32_t off, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds_base)
+                 : "memory", "m0");
+}
+__device__ inline void dma4o(const void *base, uint32_t off, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(off), "s"(base), "s"(lds_base)
+                 : "memory", "m0");
+}
 
 // Wait until at most N of this wave's vector-memory operations are in flight
 // and all of its LDS operations are done, then the workgroup barrier.
@@ -268,56 +278,108 @@ template <class G>
 struct OutSplit {
     static constexpr int BN = G::BN, BM = G::BM, S = G::S, FN = G::FN, FM = G::FM, NW = G::NW;
 
-    // Fill ring slot st with k-step s of the tile at (tok0, ch0).  Rows of X
-    // past m, and weight rows past n, read a valid row instead: their outputs
-    // are never stored.  Past k the packed weight is zero, so X may hold
-    // anything there; for a dense weight the tail k-step is staged with zeros
-    // instead.
-    static __device__ __forceinline__ void issue(const GemmArgs &a, int8_t *lds, uint32_t lds0, int wave, int lane,
-                                                 int tok0, int ch0, int s, int st) {
-        const uint32_t slot = lds0 + st * G::SLOT;
+    static constexpr int WJ = G::kSparse ? (BN / 16) * S / NW : BN / (8 * NW);  // weight loads per wave
+
+    // Per-lane byte offsets of one tile's loads at k-step 0: the X row chunks
+    // and the weight blocks (or dense weight row chunks).  A k-step adds the
+    // same amount to every lane, so each load is a 32-bit offset from a
+    // scalar base that advances with the k-step (X and the weights hold fewer
+    // than 2^32 bytes, checked on the host).  Rows of X past m, and weight
+    // rows past n, read a valid row instead: their outputs are never stored.
+    struct Cursor {
+        uint32_t x[G::XI];
+        uint32_t w[WJ];
+        uint32_t m[G::kSparse ? WJ : 1];
+    };
+
+    static __device__ __forceinline__ Cursor cursor(const GemmArgs &a, int wave, int lane, int tok0, int ch0) {
+        Cursor c;
 #pragma unroll
         for (int j = 0; j < G::XI; ++j) {
             const int r = 8 * (NW * j + wave) + (lane >> 3);
-            const int c = (lane & 7) ^ (r & 7);
+            const int cc = (lane & 7) ^ (r & 7);
             const int tok = tok0 + r < a.m ? tok0 + r : a.m - 1;
-            const int kk = s * 128 + c * 16 < a.k ? s * 128 + c * 16 : a.k - 16;
-            dma16(a.X + (size_t)tok * a.k + kk, slot + (NW * j + wave) * 1024);
+            c.x[j] = (uint32_t)tok * (uint32_t)a.k + (uint32_t)cc * 16;
         }
         if constexpr (G::kSparse) {
             const int f0 = ch0 >> 4;
 #pragma unroll
-            for (int j = 0; j < (BN / 16) * S / NW; ++j) {
+            for (int j = 0; j < WJ; ++j) {
                 const int bl = NW * j + wave;              // weight block of the slot: fragment bl / S, stream bl % S
                 int f = f0 + bl / S;
                 f = f < a.n_frags ? f : a.n_frags - 1;
-                const size_t b = ((size_t)f * a.k_steps + s) * S + bl % S;
-                dma16(a.A + b * kVBlock + lane * 16, slot + G::XB + bl * kVBlock);
-                dma4(a.meta + b * kMBlock + lane * 4, slot + G::XB + G::WVB + bl * kMBlock);
+                const uint32_t b0 = (uint32_t)f * (uint32_t)a.k_steps * S + bl % S;
+                c.w[j] = b0 * kVBlock + lane * 16;
+                c.m[j] = b0 * kMBlock + lane * 4;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < WJ; ++j) {
+                const int r = 8 * (NW * j + wave) + (lane >> 3);
+                const int cc = (lane & 7) ^ (r & 7);
+                const int row = ch0 + r < a.n ? ch0 + r : a.n - 1;
+                c.w[j] = (uint32_t)row * (uint32_t)a.k + (uint32_t)cc * 16;
+            }
+        }
+        return c;
+    }
+
+    // Fill ring slot st with k-step s of the tile of cursor c.  Past k the
+    // packed weight is zero, so X may hold anything there (its loads are
+    // clamped to the row); for a dense weight the tail k-step is staged with
+    // zeros instead.
+    static __device__ __forceinline__ void issue(const GemmArgs &a, const Cursor &c, int8_t *lds, uint32_t lds0,
+                                                 int wave, int lane, int s, int st) {
+        const uint32_t slot = lds0 + st * G::SLOT;
+        if (s * 128 + 128 <= a.k) {
+            const int8_t *xb = a.X + (size_t)s * 128;
+#pragma unroll
+            for (int j = 0; j < G::XI; ++j) dma16o(xb, c.x[j], slot + (NW * j + wave) * 1024);
+        } else {
+            // last k-step of a k that is not a multiple of 128: clamp to the row
+#pragma unroll
+            for (int j = 0; j < G::XI; ++j) {
+                const int r = 8 * (NW * j + wave) + (lane >> 3);
+                const uint32_t cc16 = (uint32_t)(((lane & 7) ^ (r & 7)) * 16);
+                const uint32_t kk = (uint32_t)s * 128 + cc16 < (uint32_t)a.k ? (uint32_t)s * 128 + cc16
+                                                                              : (uint32_t)a.k - 16;
+                dma16o(a.X, c.x[j] - cc16 + kk, slot + (NW * j + wave) * 1024);
+            }
+        }
+        if constexpr (G::kSparse) {
+            const int8_t *vb = a.A + (size_t)s * S * kVBlock;
+            const uint8_t *mb = a.meta + (size_t)s * S * kMBlock;
+#pragma unroll
+            for (int j = 0; j < WJ; ++j) {
+                const int bl = NW * j + wave;
+                dma16o(vb, c.w[j], slot + G::XB + bl * kVBlock);
+                dma4o(mb, c.m[j], slot + G::XB + G::WVB + bl * kMBlock);
             }
         } else {
             if (s * 128 + 128 <= a.k) {
+                const int8_t *wb = a.A + (size_t)s * 128;
 #pragma unroll
-                for (int j = 0; j < BN / (8 * NW); ++j) {
-                    const int r = 8 * (NW * j + wave) + (lane >> 3);
-                    const int c = (lane & 7) ^ (r & 7);
-                    const int row = ch0 + r < a.n ? ch0 + r : a.n - 1;
-                    dma16(a.A + (size_t)row * a.k + s * 128 + c * 16, slot + G::XB + (NW * j + wave) * 1024);
-                }
+                for (int j = 0; j < WJ; ++j) dma16o(wb, c.w[j], slot + G::XB + (NW * j + wave) * 1024);
             } else {
                 // tail k-step of a dense weight: plain loads, zeros past k
 #pragma unroll
-                for (int j = 0; j < BN / (8 * NW); ++j) {
+                for (int j = 0; j < WJ; ++j) {
                     const int r = 8 * (NW * j + wave) + (lane >> 3);
-                    const int c = (lane & 7) ^ (r & 7);
-                    const int row = ch0 + r < a.n ? ch0 + r : a.n - 1;
-                    const int kk = s * 128 + c * 16;
+                    const uint32_t cc16 = (uint32_t)(((lane & 7) ^ (r & 7)) * 16);
+                    const uint32_t kk = (uint32_t)s * 128 + cc16;
                     v4i v = v4i{0, 0, 0, 0};
-                    if (kk < a.k) v = *(const v4i *)(a.A + (size_t)row * a.k + kk);
+                    if (kk < (uint32_t)a.k) v = *(const v4i *)(a.A + (c.w[j] - cc16 + kk));
                     *(v4i *)(lds + st * G::SLOT + G::XB + (NW * j + wave) * 1024 + lane * 16) = v;
                 }
             }
         }
+    }
+
+    // The same for a tile given by its origin (the persistent kernel, whose
+    // slices belong to changing tiles).
+    static __device__ __forceinline__ void issue(const GemmArgs &a, int8_t *lds, uint32_t lds0, int wave, int lane,
+                                                 int tok0, int ch0, int s, int st) {
+        issue(a, cursor(a, wave, lane, tok0, ch0), lds, lds0, wave, lane, s, st);
     }
 
     // One k-step of the wave's FN x FM accumulators from ring slot st.
@@ -443,16 +505,17 @@ __global__ __launch_bounds__(64 * WN * WM) void k_gemm(GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
 
+    const typename O::Cursor cur = O::cursor(a, wave, lane, tok0, ch0);
 #pragma unroll
     for (int i = 0; i < R - 1; ++i)
-        if (i < nsteps) O::issue(a, lds, lds0, wave, lane, tok0, ch0, s_begin + i, i);
+        if (i < nsteps) O::issue(a, cur, lds, lds0, wave, lane, s_begin + i, i);
     for (int it = 0; it < nsteps; ++it) {
         // k-step it was issued NST-1 iterations ago; only the loads of later
         // k-steps may remain in flight.  The barrier then publishes every
         // wave's slot and frees the slot computed in the previous iteration.
         const int later = nsteps - 1 - it < R - 2 ? nsteps - 1 - it : R - 2;
         wait_later_then_barrier<R - 2, G::DMA>(later);
-        if (it + R - 1 < nsteps) O::issue(a, lds, lds0, wave, lane, tok0, ch0, s_begin + it + R - 1, (it + R - 1) % R);
+        if (it + R - 1 < nsteps) O::issue(a, cur, lds, lds0, wave, lane, s_begin + it + R - 1, (it + R - 1) % R);
         O::compute(lds, wn, wm, lane, it % R, acc);
     }
 
