@@ -737,6 +737,38 @@ def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, comma
     print("\n".join(md))
 
 
+def mfma_ceiling(torch, iters: int = 4000, reps: int = 3) -> dict:
+    """Matrix-instruction rate this GPU sustains (nm_probe_mfma_rate), in
+    dense-equivalent POPS, on uniform random int8 operands and on zeros: the
+    practical compute ceiling beside the data-sheet peak (random operands make
+    the chip lower its clock)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    g = torch.Generator().manual_seed(2607)
+    rnd = torch.randint(-2 ** 31, 2 ** 31, (nmspmm.NM_PROBE_WORDS,), generator=g, dtype=torch.int64)
+    rnd = rnd.to(torch.int32).cuda()
+    zero = torch.zeros_like(rnd)
+    wgs = 4 * cus
+    out = torch.empty(wgs * 256, dtype=torch.int32, device="cuda")
+    res = {}
+    for kind, name, macs in ((nmspmm.NM_KIND_SP42, "smfmac_i32_16x16x128_i8", 16 * 16 * 128),
+                             (nmspmm.NM_KIND_DENSE, "mfma_i32_16x16x64_i8", 16 * 16 * 64)):
+        for tname, tab in (("random", rnd), ("zero", zero)):
+            nmspmm.probe_mfma_rate(kind, tab, 16, out)
+            best = float("inf")
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                nmspmm.probe_mfma_rate(kind, tab, iters, out)
+                e1.record()
+                torch.cuda.synchronize()
+                best = min(best, e0.elapsed_time(e1))
+            ops = wgs * 4 * iters * 8 * 2 * macs
+            res[f"{name}_{tname}_pops"] = round(ops / (best * 1e-3) / 1e15, 3)
+    res["setup"] = (f"{wgs} workgroups x 4 waves, 8 independent instructions per wave per iteration, {iters} "
+                    "iterations; operands uniform random int8 bytes or all zeros")
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -747,6 +779,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true",
                     help="skip the DeiT-Base per-batch speedups reported beside the main line")
+    ap.add_argument("--no-mfma-ceiling", action="store_true",
+                    help="skip the measured matrix-instruction rate reported beside the main line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after timing, run one plain device copy of MIB MiB (profiler counter calibration)")
     ap.add_argument("--sweep", type=str, default=None,
@@ -927,6 +961,9 @@ def main():
         "dense_ms_per_step": round(float(dense_ms), 4),
         "roofline": roofline,
     }
+    if not args.no_mfma_ceiling:
+        line["mfma_measured"] = mfma_ceiling(torch)
+        log(json.dumps(line["mfma_measured"]))
     if not args.no_secondary and args.config != 2:
         line["deit_base_speedups"] = secondary_workload(2, 3, 2, torch)
         log(json.dumps(line["deit_base_speedups"]))

@@ -1,0 +1,44 @@
+/* nmprobe.h -- measurement aid of libnmspmm (not part of the method).
+ *
+ * The matrix-instruction rate this GPU sustains on given operand values: the
+ * practical ceiling beside the data-sheet peak.  Under random int8 operands
+ * the chip lowers its clock (power), so a structured-sparse or dense int8
+ * matrix instruction stream runs below the peak derived from the nominal
+ * clock; the GEMM kernels' compute-bound throughput is compared with this.
+ */
+#ifndef NMPROBE_H
+#define NMPROBE_H
+
+#include <stdint.h>
+
+#include "nmspmm.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Operand table of the rate loop: NM_PROBE_WORDS int32 words in device memory.
+ *   words [0, 2048):    A operands, 8 fragments x 64 lanes x 4 words
+ *   words [2048, 4096): B operands, 4 fragments x 64 lanes x 8 words
+ * (the structured-sparse position words are fixed valid patterns). */
+#define NM_PROBE_WORDS 4096
+
+/* Launches `workgroups` workgroups of 4 waves; each wave loads its operands
+ * from `operands` and issues iters x 8 independent matrix instructions of
+ * `kind`:
+ *   NM_KIND_SP42  -- v_smfmac_i32_16x16x128_i8, 2*16*16*128 dense-equivalent
+ *                    ops each (half of them on stored zeros)
+ *   NM_KIND_DENSE -- v_mfma_i32_16x16x64_i8, 2*16*16*64 ops each
+ * and writes one int32 per thread to out[workgroups x 256] (so the loop is
+ * not removed).  Asynchronous on `stream` (a hipStream_t, NULL = default);
+ * time it with events on that stream.  The caller owns both buffers.
+ * Errors: NM_ERR_ARG for a NULL pointer, another kind, iters < 1 or
+ * workgroups < 1; NM_ERR_HIP if the launch fails. */
+nm_status nm_probe_mfma_rate(int kind, const int32_t *operands, int iters, int workgroups, int32_t *out,
+                             void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NMPROBE_H */

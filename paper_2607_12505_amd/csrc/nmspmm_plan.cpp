@@ -121,8 +121,10 @@ nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *
         // give the most workgroups in flight.
         tile = kT64x64r2;
     } else if (tiles_of(kT128x128r2, mm, n) < 4 * cus) {
-        // Medium: half-height tiles (narrower for the heavier operands).
+        // Medium: half-height tiles (narrower for the heavier operands), or
+        // 64 x 64 when those would leave compute units without a tile.
         tile = heavy ? kT64x128r2 : kT128x64r2;
+        if (tiles_of(tile, mm, n) < cus) tile = kT64x64r2;
     } else if (tiles_of(kT256x256w8, mm, n) >= 4 * cus && k_steps <= 8) {
         // Large outputs with a short reduction: 256 x 256 tiles on 8 waves
         // halve the operand traffic per output and keep enough waves per CU

@@ -20,7 +20,7 @@ def declared_functions():
 
 
 def test_header_declares_the_binding_names():
-    assert len(HEADERS) == 2
+    assert len(HEADERS) == 3
     assert declared_functions() == sorted(nmspmm.EXPORTED + nmsearch.EXPORTED)
 
 
@@ -68,3 +68,7 @@ def test_host_side_argument_checks_need_no_gpu():
         nmspmm.NM_ERR_ARG
     assert L.nm_quantize_f16(fake, -1, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_SHAPE
     assert L.nm_quantize_f16(misaligned, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, nul, 1, 1, fake, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42X2, fake, 1, 1, fake, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 0, 1, fake, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 1, 0, fake, nul) == nmspmm.NM_ERR_ARG

@@ -78,6 +78,11 @@ def test_large_shapes_use_large_tiles():
     assert (nmspmm.spmm_plan(d, 12608, 1).tile_n, nmspmm.spmm_plan(d, 12608, 1).tile_m) == (128, 64)
     d = nmspmm.compress_size(1152, 384, 4, 8)
     assert (nmspmm.spmm_plan(d, 12608, 1).tile_n, nmspmm.spmm_plan(d, 12608, 1).tile_m) == (64, 128)
+    # ... or 64 x 64 when half-height tiles would leave compute units idle
+    # (DeiT-Base fc2 at batch 8: 150 tiles of 128 x 64 on 256 compute units)
+    d = nmspmm.compress_size(768, 3072, 2, 4)
+    assert (nmspmm.spmm_plan(d, 1576, 1).tile_n, nmspmm.spmm_plan(d, 1576, 1).tile_m) == (64, 64)
+    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 1576, 1)) == "k_gemm<1, 2, 2, 2, 2, 2>"
     # one or two k-steps: 64 x 64 tiles (Swin-B stage 1, k = 128)
     d = nmspmm.compress_size(384, 128, 2, 4)
     assert (nmspmm.spmm_plan(d, 100352, 1).tile_n, nmspmm.spmm_plan(d, 100352, 1).tile_m) == (64, 64)
