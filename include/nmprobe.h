@@ -37,6 +37,21 @@ extern "C" {
 nm_status nm_probe_mfma_rate(int kind, const int32_t *operands, int iters, int workgroups, int32_t *out,
                              void *stream);
 
+/* One matrix instruction on one wave (64 lanes), operands given per lane, so
+ * a test can pin the (lane, register byte) <-> (row, k, column) maps that the
+ * packed weight layout and the GEMM kernels rely on.  Device buffers, caller
+ * owned, int32 words, lane-major:
+ *   kind NM_KIND_SP42 (v_smfmac_i32_16x16x128_i8):
+ *     a[64 x 4] (16 value bytes per lane), b[64 x 8] (32 bytes per lane),
+ *     pos[64] (one position word per lane), d[64 x 4]
+ *   kind NM_KIND_DENSE (v_mfma_i32_16x16x64_i8):
+ *     a[64 x 4], b[64 x 4], pos unused (may be NULL), d[64 x 4]
+ * d receives the lane's four accumulator words of D = A x B (C = 0).
+ * Asynchronous on `stream`.  Errors: NM_ERR_ARG for a NULL buffer or another
+ * kind; NM_ERR_HIP if the launch fails. */
+nm_status nm_probe_mfma_layout(int kind, const int32_t *a, const int32_t *b, const int32_t *pos, int32_t *d,
+                               void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,4 +1,5 @@
-// Matrix-instruction rate loop (measurement aid, declared in nmprobe.h).
+// Matrix-instruction rate loop and single-instruction layout probe (measurement
+// and test aids, declared in nmprobe.h).
 #include <hip/hip_runtime.h>
 
 #include "../../include/nmprobe.h"
@@ -44,7 +45,38 @@ __global__ __launch_bounds__(256) void k_mfma_rate(const int32_t *__restrict__ o
     out[blockIdx.x * 256 + threadIdx.x] = s;
 }
 
+// One instruction of KIND on one wave; operands and results lane-major.
+template <int KIND>
+__global__ __launch_bounds__(64) void k_mfma_layout(const int32_t *__restrict__ a, const int32_t *__restrict__ b,
+                                                    const int32_t *__restrict__ pos, int32_t *d) {
+    const int lane = threadIdx.x;
+    const v4i av = *(const v4i *)(a + lane * 4);
+    v4i acc = v4i{0, 0, 0, 0};
+    if constexpr (KIND == NM_KIND_SP42) {
+        const v8i bv = *(const v8i *)(b + lane * 8);
+        acc = __builtin_amdgcn_smfmac_i32_16x16x128_i8(av, bv, acc, pos[lane], 0, 0);
+    } else {
+        const v4i bv = *(const v4i *)(b + lane * 4);
+        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bv, acc, 0, 0, 0);
+    }
+    *(v4i *)(d + lane * 4) = acc;
+}
+
 }  // namespace
+
+extern "C" nm_status nm_probe_mfma_layout(int kind, const int32_t *a, const int32_t *b, const int32_t *pos,
+                                          int32_t *d, void *stream) {
+    if (!a || !b || !d) return NM_ERR_ARG;
+    if (kind == NM_KIND_SP42) {
+        if (!pos) return NM_ERR_ARG;
+        hipLaunchKernelGGL(k_mfma_layout<NM_KIND_SP42>, dim3(1), dim3(64), 0, (hipStream_t)stream, a, b, pos, d);
+    } else if (kind == NM_KIND_DENSE) {
+        hipLaunchKernelGGL(k_mfma_layout<NM_KIND_DENSE>, dim3(1), dim3(64), 0, (hipStream_t)stream, a, b, pos, d);
+    } else {
+        return NM_ERR_ARG;
+    }
+    return hipGetLastError() == hipSuccess ? NM_OK : NM_ERR_HIP;
+}
 
 extern "C" nm_status nm_probe_mfma_rate(int kind, const int32_t *operands, int iters, int workgroups, int32_t *out,
                                         void *stream) {

@@ -28,7 +28,7 @@ EXPORTED = (
     "nm_status_string", "nm_compress_size", "nm_compress", "nm_decompress", "nm_num_tiles",
     "nm_tile_info", "nm_plan_kernel_name", "nm_spmm_plan", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
     "nm_spmm", "nm_spmm_ex", "nm_gemm_i8_dense", "nm_gemm_i8_dense_ex", "nm_spmm_out", "nm_gemm_i8_dense_out",
-    "nm_quantize_f16", "nm_probe_mfma_rate",
+    "nm_quantize_f16", "nm_probe_mfma_rate", "nm_probe_mfma_layout",
 )
 NM_PROBE_WORDS = 4096
 
@@ -96,6 +96,7 @@ def lib() -> ctypes.CDLL:
             "nm_gemm_i8_dense_out": ([vp, i32, vp, i32, i32, ctypes.POINTER(NmOutputs), vp, sz, vp, pp], i32),
             "nm_quantize_f16": ([vp, ctypes.c_int64, ctypes.c_float, vp, vp], i32),
             "nm_probe_mfma_rate": ([i32, vp, i32, i32, vp, vp], i32),
+            "nm_probe_mfma_layout": ([i32, vp, vp, vp, vp, vp], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -336,6 +337,19 @@ def probe_mfma_rate(kind: int, operands, iters: int, out, stream=None):
         raise ValueError("operands needs NM_PROBE_WORDS words and out a multiple of 256")
     _check(lib().nm_probe_mfma_rate(int(kind), _ptr(operands), int(iters), out.numel() // 256, _ptr(out),
                                     _stream(stream)), "nm_probe_mfma_rate")
+
+
+def probe_mfma_layout(kind: int, a, b, pos, d, stream=None):
+    """nm_probe_mfma_layout: one matrix instruction on one wave (nmprobe.h).
+
+    a, d: int32 device tensors of 256 words; b: 512 words (NM_KIND_SP42) or
+    256 (NM_KIND_DENSE); pos: 64 words (NM_KIND_SP42) or None."""
+    nb = 512 if kind == NM_KIND_SP42 else 256
+    if a.numel() < 256 or d.numel() < 256 or b.numel() < nb or (kind == NM_KIND_SP42 and
+                                                                 (pos is None or pos.numel() < 64)):
+        raise ValueError("operand buffers smaller than the instruction needs")
+    _check(lib().nm_probe_mfma_layout(int(kind), _ptr(a), _ptr(b), _ptr(pos), _ptr(d), _stream(stream)),
+           "nm_probe_mfma_layout")
 
 
 def workspace_init(ws, stream=None):

@@ -72,3 +72,33 @@ def test_host_side_argument_checks_need_no_gpu():
     assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42X2, fake, 1, 1, fake, nul) == nmspmm.NM_ERR_ARG
     assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 0, 1, fake, nul) == nmspmm.NM_ERR_ARG
     assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 1, 0, fake, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, nul, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, fake, fake, nul, fake, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42X2, fake, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
+
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.device_count() > 0
+    except Exception:  # pragma: no cover - torch is part of the image
+        return False
+
+
+def test_launch_failures_report_nm_err_hip():
+    # Without a device every launch fails: each entry point must turn that into
+    # NM_ERR_HIP (never a crash or NM_OK).  Skipped where a GPU is visible, since
+    # the fake pointers below would then reach a real kernel.
+    if _gpu_visible():
+        import pytest
+        pytest.skip("a GPU is visible: fake device pointers must not be launched")
+    L = nmspmm.lib()
+    fake, nul = ctypes.c_void_p(1 << 20), None
+    d = nmspmm.compress_size(64, 128, 2, 4)
+    assert L.nm_spmm_ex(fake, 64, fake, fake, ctypes.byref(d), fake, nul, nul, nul, 0, nul, None) == \
+        nmspmm.NM_ERR_HIP
+    assert L.nm_gemm_i8_dense_ex(fake, 64, fake, 64, 128, fake, nul, nul, nul, 0, nul, None) == nmspmm.NM_ERR_HIP
+    assert L.nm_quantize_f16(fake, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_HIP
+    assert L.nm_workspace_init(fake, 64, nul) == nmspmm.NM_ERR_HIP
+    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, fake, 1, 1, fake, nul) == nmspmm.NM_ERR_HIP
+    assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_DENSE, fake, fake, nul, fake, nul) == nmspmm.NM_ERR_HIP
