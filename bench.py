@@ -611,6 +611,80 @@ def paper_grid(torch, report):
     return {"summary": summary, "rows": len(rows)}
 
 
+def shape_report(torch, report, cfgs=(0, 1, 2, 3, 4)):
+    """Per-shape roofline of every workload GEMM (distinct shape and pattern):
+    sparse and dense time, the compute and HBM fractions against the data-sheet
+    peaks, the compute fraction against the matrix-instruction rate measured in
+    the same run on random operands, and the roofline fraction (the binding
+    one).  Times: mean of 5 back-to-back launches, inputs resident."""
+    ceil = mfma_ceiling(torch)
+    sp_rate = ceil["smfmac_i32_16x16x128_i8_random_pops"] * 1e3       # dense-equivalent TOPS
+    dn_rate = ceil["mfma_i32_16x16x64_i8_random_pops"] * 1e3
+    rows = []
+    for cfg in cfgs:
+        work = wl.workload(cfg)
+        seen, gemms = set(), []
+        for g in work.gemms:
+            key = (g.m, g.k, g.n, g.N, g.M)
+            if key not in seen:
+                seen.add(key)
+                gemms.append(g)
+        xd, xh = {}, {}
+        preps = [Prepared(cfg, g, xd, xh, work.out_int32, work.out_f16, torch, use_dense_kernel=(g.N == g.M))
+                 for g in gemms]
+        torch.cuda.synchronize()
+        each = time_each(preps, torch)
+        outs = ("int32" if work.out_int32 else "") + ("+fp16" if work.out_f16 else "")
+        for p, (ts, td) in zip(preps, each):
+            g, kind = p.g, p.splan.kind
+            ops = g.dense_eq_ops
+            peak = PEAK_SPARSE_TOPS if kind == nmspmm.NM_KIND_SP42 else PEAK_INT8_TOPS
+            rate = sp_rate if kind == nmspmm.NM_KIND_SP42 else sp_rate / 2 if kind == nmspmm.NM_KIND_SP42X2 \
+                else dn_rate
+            b = algorithmic_bytes(g, work.out_int32, work.out_f16, sparse=p.sparse_kernel)
+            bd = algorithmic_bytes(g, work.out_int32, work.out_f16, sparse=False)
+            t_mfma, t_hbm = ops / (peak * 1e9), b / (PEAK_HBM_GBS * 1e6)      # ms
+            td_mfma, td_hbm = ops / (PEAK_INT8_TOPS * 1e9), bd / (PEAK_HBM_GBS * 1e6)
+            rows.append({"workload": work.name, "gemm": g.name, "m": g.m, "k": g.k, "n": g.n, "pattern": pattern_name(g),
+                         "outputs": outs, "kernel": p.kernel_name(p.splan), "sparse_us": ts * 1e3, "dense_us": td * 1e3,
+                         "speedup": td / ts, "tops": ops / (ts * 1e-3) / 1e12,
+                         "bound": "mfma" if t_mfma > t_hbm else "hbm",
+                         "mfma_frac": t_mfma / ts, "mfma_frac_measured": ops / (rate * 1e9) / ts,
+                         "hbm_gbs": b / (ts * 1e-3) / 1e9, "hbm_frac": t_hbm / ts, "roofline_frac": max(t_mfma, t_hbm) / ts,
+                         "dense_roofline_frac": max(td_mfma, td_hbm) / td})
+        log(f"shape report: {work.name} done ({len(preps)} shapes)")
+        del preps
+        torch.cuda.empty_cache()
+    if report:
+        md = ["# Per-shape roofline of the workload GEMMs", "",
+              "Command: `python3 bench.py --shape-report --report profiles/per_shape_roofline.md` (repository root).  "
+              "Every distinct (shape, N:M) of the five workloads; mean of 5 back-to-back launches with inputs resident "
+              "(HIP events).  Peaks: HBM 8 TB/s; matrix cores 10.07 dense-equivalent POPS for one 4:2 stream "
+              "(smfmac), 5.03 POPS for two streams and dense.  \"MFMA frac (meas.)\" divides by the rate measured "
+              f"in the same run on random int8 operands: smfmac {ceil['smfmac_i32_16x16x128_i8_random_pops']} "
+              f"dense-equivalent POPS (two streams: half), dense {ceil['mfma_i32_16x16x64_i8_random_pops']} POPS "
+              f"(on zeros: {ceil['smfmac_i32_16x16x128_i8_zero_pops']} and {ceil['mfma_i32_16x16x64_i8_zero_pops']}).  "
+              "Roofline fraction = max(compute time at peak, algorithmic bytes at 8 TB/s) / measured time; "
+              "algorithmic bytes count the compact packed weight (N/M of the values plus ceil(log2 M) bits per value).  "
+              "Each row has its own input and output buffers; the dense time of one shape, measured again in every "
+              "pattern row, shows the run-to-run spread (largest on the biggest outputs).", "",
+              "| workload | GEMM | m | k | n | N:M | out | sparse kernel | sparse us | dense us | speedup | TOPS | bound | "
+              "MFMA frac | MFMA frac (meas.) | GB/s | HBM frac | roofline frac | dense roofline frac |",
+              "|---|---|---:|---:|---:|---|---|---|---:|---:|---:|---:|---|---:|---:|---:|---:|---:|---:|"]
+        for r in rows:
+            md.append(f"| {r['workload']} | {r['gemm']} | {r['m']} | {r['k']} | {r['n']} | {r['pattern']} | {r['outputs']} "
+                      f"| `{r['kernel']}` | {r['sparse_us']:.1f} | {r['dense_us']:.1f} | {r['speedup']:.2f} | "
+                      f"{r['tops']:.0f} | {r['bound']} | {r['mfma_frac']:.3f} | {r['mfma_frac_measured']:.3f} | "
+                      f"{r['hbm_gbs']:.0f} | {r['hbm_frac']:.3f} | {r['roofline_frac']:.3f} | "
+                      f"{r['dense_roofline_frac']:.3f} |")
+        with open(report, "w") as f:
+            f.write("\n".join(md) + "\n")
+    fr = np.array([r["roofline_frac"] for r in rows])
+    return {"shapes": len(rows), "roofline_frac_median": round(float(np.median(fr)), 3),
+            "roofline_frac_min": round(float(fr.min()), 3), "roofline_frac_max": round(float(fr.max()), 3),
+            "mfma_measured": ceil}
+
+
 def write_sweep_report(sweep_json, path):
     """Markdown table of a planner evaluation written by --sweep-out."""
     d = json.load(open(sweep_json))
@@ -804,6 +878,8 @@ def main():
                     help="the paper's kernel benchmark grid vs the dense GEMMs (prints one JSON line)")
     ap.add_argument("--chaining", action="store_true",
                     help="int8 requantisation epilogue and activation quantiser timings (prints one JSON line)")
+    ap.add_argument("--shape-report", action="store_true",
+                    help="per-shape roofline of every workload GEMM (prints one JSON line; --report for markdown)")
     ap.add_argument("--cal", type=int, default=64, help="calibration configurations for --predictor")
     ap.add_argument("--test", type=int, default=32, help="random test configurations for --predictor")
     ap.add_argument("--report", type=str, default=None, help="markdown report of --predictor / --chaining")
@@ -841,6 +917,9 @@ def main():
         return
     if args.predictor:
         print(json.dumps({"predictor": predictor_experiment(torch, args.cal, args.test, args.report)}), flush=True)
+        return
+    if args.shape_report:
+        print(json.dumps({"shape_report": shape_report(torch, args.report)}), flush=True)
         return
 
     work = wl.workload(args.config)
