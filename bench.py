@@ -896,7 +896,7 @@ def main():
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the method is a "
-              "single-GPU kernel; see the sharding notes in DESIGN.md)", file=sys.stderr)
+              "single-GPU kernel; how it would shard is a design note, not a measured path)", file=sys.stderr)
         sys.exit(2)
 
     import torch
