@@ -823,23 +823,30 @@ def mfma_ceiling(torch, iters: int = 4000, reps: int = 3) -> dict:
     zero = torch.zeros_like(rnd)
     wgs = 4 * cus
     out = torch.empty(wgs * 256, dtype=torch.int32, device="cuda")
+    ticks = torch.zeros(2 * wgs, dtype=torch.int64, device="cuda")
+    wall_hz = nmspmm.wall_clock_khz() * 1e3
     res = {}
     for kind, name, macs in ((nmspmm.NM_KIND_SP42, "smfmac_i32_16x16x128_i8", 16 * 16 * 128),
                              (nmspmm.NM_KIND_DENSE, "mfma_i32_16x16x64_i8", 16 * 16 * 64)):
         for tname, tab in (("random", rnd), ("zero", zero)):
             nmspmm.probe_mfma_rate(kind, tab, 16, out)
-            best = float("inf")
+            best, mhz = float("inf"), 0.0
             for _ in range(reps):
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 e0.record()
-                nmspmm.probe_mfma_rate(kind, tab, iters, out)
+                nmspmm.probe_mfma_rate(kind, tab, iters, out, ticks)
                 e1.record()
                 torch.cuda.synchronize()
-                best = min(best, e0.elapsed_time(e1))
+                ms = e0.elapsed_time(e1)
+                if ms < best:
+                    t = ticks.cpu().numpy().reshape(-1, 2).astype(np.float64)
+                    best, mhz = ms, t[:, 0].sum() / (t[:, 1].sum() / wall_hz) / 1e6
             ops = wgs * 4 * iters * 8 * 2 * macs
             res[f"{name}_{tname}_pops"] = round(ops / (best * 1e-3) / 1e15, 3)
+            res[f"{name}_{tname}_clock_mhz"] = round(float(mhz))
     res["setup"] = (f"{wgs} workgroups x 4 waves, 8 independent instructions per wave per iteration, {iters} "
-                    "iterations; operands uniform random int8 bytes or all zeros")
+                    "iterations; operands uniform random int8 bytes or all zeros; clock = shader cycles over "
+                    "real-time counter ticks during the loop")
     return res
 
 

@@ -25,17 +25,26 @@ extern "C" {
 
 /* Launches `workgroups` workgroups of 4 waves; each wave loads its operands
  * from `operands` and issues iters x 8 independent matrix instructions of
- * `kind`:
+ * `kind` (four of the dense ones being the second k-half of the other four,
+ * as in the dense GEMM):
  *   NM_KIND_SP42  -- v_smfmac_i32_16x16x128_i8, 2*16*16*128 dense-equivalent
  *                    ops each (half of them on stored zeros)
  *   NM_KIND_DENSE -- v_mfma_i32_16x16x64_i8, 2*16*16*64 ops each
  * and writes one int32 per thread to out[workgroups x 256] (so the loop is
- * not removed).  Asynchronous on `stream` (a hipStream_t, NULL = default);
- * time it with events on that stream.  The caller owns both buffers.
- * Errors: NM_ERR_ARG for a NULL pointer, another kind, iters < 1 or
+ * not removed).  If `ticks` is not NULL, wave 0 of workgroup w writes
+ * ticks[2w] = shader-clock cycles and ticks[2w + 1] = real-time counter
+ * ticks spent in its loop (the real-time counter runs at nm_wall_clock_khz),
+ * from which the shader clock during the loop follows.  Asynchronous on
+ * `stream` (a hipStream_t, NULL = default); time it with events on that
+ * stream.  The caller owns the buffers (device memory).
+ * Errors: NM_ERR_ARG for a NULL operands/out, another kind, iters < 1 or
  * workgroups < 1; NM_ERR_HIP if the launch fails. */
 nm_status nm_probe_mfma_rate(int kind, const int32_t *operands, int iters, int workgroups, int32_t *out,
-                             void *stream);
+                             int64_t *ticks, void *stream);
+
+/* Rate of the real-time counter of the current device in kHz (host query).
+ * Errors: NM_ERR_ARG for NULL; NM_ERR_HIP if the device query fails. */
+nm_status nm_wall_clock_khz(int32_t *khz);
 
 /* One matrix instruction on one wave (64 lanes), operands given per lane, so
  * a test can pin the (lane, register byte) <-> (row, k, column) maps that the

@@ -13,7 +13,8 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 // and cycles through them, so consecutive instructions are independent and
 // read different registers, as in the GEMM kernels' inner loop.
 template <int KIND>
-__global__ __launch_bounds__(256) void k_mfma_rate(const int32_t *__restrict__ ops, int iters, int32_t *out) {
+__global__ __launch_bounds__(256) void k_mfma_rate(const int32_t *__restrict__ ops, int iters, int32_t *out,
+                                                   int64_t *ticks) {
     const int lane = threadIdx.x & 63;
     v4i a[8], acc[8];
     v8i b[4];
@@ -24,6 +25,7 @@ __global__ __launch_bounds__(256) void k_mfma_rate(const int32_t *__restrict__ o
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) b[j] = *(const v8i *)(ops + 2048 + (j * 64 + lane) * 8);
+    const int64_t c0 = clock64(), r0 = wall_clock64();
     for (int it = 0; it < iters; ++it) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
@@ -39,10 +41,15 @@ __global__ __launch_bounds__(256) void k_mfma_rate(const int32_t *__restrict__ o
             }
         }
     }
+    const int64_t c1 = clock64(), r1 = wall_clock64();
     int s = 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) s += acc[i][0] ^ acc[i][1] ^ acc[i][2] ^ acc[i][3];
     out[blockIdx.x * 256 + threadIdx.x] = s;
+    if (ticks && threadIdx.x == 0) {
+        ticks[2 * blockIdx.x] = c1 - c0;
+        ticks[2 * blockIdx.x + 1] = r1 - r0;
+    }
 }
 
 // One instruction of KIND on one wave; operands and results lane-major.
@@ -78,15 +85,27 @@ extern "C" nm_status nm_probe_mfma_layout(int kind, const int32_t *a, const int3
     return hipGetLastError() == hipSuccess ? NM_OK : NM_ERR_HIP;
 }
 
+extern "C" nm_status nm_wall_clock_khz(int32_t *khz) {
+    if (!khz) return NM_ERR_ARG;
+    int dev = 0, rate = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&rate, hipDeviceAttributeWallClockRate, dev) !=
+                                                 hipSuccess) {
+        (void)hipGetLastError();
+        return NM_ERR_HIP;
+    }
+    *khz = rate;
+    return NM_OK;
+}
+
 extern "C" nm_status nm_probe_mfma_rate(int kind, const int32_t *operands, int iters, int workgroups, int32_t *out,
-                                        void *stream) {
+                                        int64_t *ticks, void *stream) {
     if (!operands || !out || iters < 1 || workgroups < 1) return NM_ERR_ARG;
     if (kind == NM_KIND_SP42)
         hipLaunchKernelGGL(k_mfma_rate<NM_KIND_SP42>, dim3(workgroups), dim3(256), 0, (hipStream_t)stream, operands,
-                           iters, out);
+                           iters, out, ticks);
     else if (kind == NM_KIND_DENSE)
         hipLaunchKernelGGL(k_mfma_rate<NM_KIND_DENSE>, dim3(workgroups), dim3(256), 0, (hipStream_t)stream,
-                           operands, iters, out);
+                           operands, iters, out, ticks);
     else
         return NM_ERR_ARG;
     return hipGetLastError() == hipSuccess ? NM_OK : NM_ERR_HIP;

@@ -68,10 +68,11 @@ def test_host_side_argument_checks_need_no_gpu():
         nmspmm.NM_ERR_ARG
     assert L.nm_quantize_f16(fake, -1, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_SHAPE
     assert L.nm_quantize_f16(misaligned, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, nul, 1, 1, fake, nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42X2, fake, 1, 1, fake, nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 0, 1, fake, nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 1, 0, fake, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, nul, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42X2, fake, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 0, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 1, 0, fake, nul, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_wall_clock_khz(None) == nmspmm.NM_ERR_ARG
     assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, nul, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
     assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, fake, fake, nul, fake, nul) == nmspmm.NM_ERR_ARG
     assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42X2, fake, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
@@ -100,5 +101,7 @@ def test_launch_failures_report_nm_err_hip():
     assert L.nm_gemm_i8_dense_ex(fake, 64, fake, 64, 128, fake, nul, nul, nul, 0, nul, None) == nmspmm.NM_ERR_HIP
     assert L.nm_quantize_f16(fake, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_HIP
     assert L.nm_workspace_init(fake, 64, nul) == nmspmm.NM_ERR_HIP
-    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, fake, 1, 1, fake, nul) == nmspmm.NM_ERR_HIP
+    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, fake, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_HIP
+    khz = ctypes.c_int32(0)
+    assert L.nm_wall_clock_khz(ctypes.byref(khz)) == nmspmm.NM_ERR_HIP
     assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_DENSE, fake, fake, nul, fake, nul) == nmspmm.NM_ERR_HIP

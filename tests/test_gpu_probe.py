@@ -29,10 +29,25 @@ def test_rate_loop_runs_and_is_deterministic():
     assert int(out.abs().sum()) == 0
 
 
+def test_loop_ticks_give_a_plausible_clock():
+    import torch
+    khz = nmspmm.wall_clock_khz()
+    assert khz > 0
+    tab = torch.zeros(nmspmm.NM_PROBE_WORDS, dtype=torch.int32, device="cuda")
+    out = torch.empty(4 * 256, dtype=torch.int32, device="cuda")
+    ticks = torch.zeros(8, dtype=torch.int64, device="cuda")
+    nmspmm.probe_mfma_rate(nmspmm.NM_KIND_DENSE, tab, 2000, out, ticks)
+    torch.cuda.synchronize()
+    t = ticks.cpu().numpy().reshape(-1, 2)
+    assert (t > 0).all()
+    mhz = t[:, 0] / (t[:, 1] / (khz * 1e3)) / 1e6
+    assert ((mhz > 50) & (mhz < 5000)).all()
+
+
 def test_bench_reports_positive_rates():
     import torch
     import bench
     res = bench.mfma_ceiling(torch, iters=64, reps=1)
-    for key in ("smfmac_i32_16x16x128_i8_random_pops", "mfma_i32_16x16x64_i8_random_pops",
-                "smfmac_i32_16x16x128_i8_zero_pops", "mfma_i32_16x16x64_i8_zero_pops"):
-        assert res[key] > 0
+    for key in ("smfmac_i32_16x16x128_i8_random", "mfma_i32_16x16x64_i8_random",
+                "smfmac_i32_16x16x128_i8_zero", "mfma_i32_16x16x64_i8_zero"):
+        assert res[key + "_pops"] > 0 and res[key + "_clock_mhz"] > 0
