@@ -11,8 +11,9 @@ device memory, the stream and HIP events.
 from __future__ import annotations
 
 import ctypes
+import json
 import time
-from typing import Dict, List, Sequence, Tuple
+from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
@@ -177,3 +178,46 @@ def random_assignments(count: int, layers: int, patterns: Sequence[Pattern], see
     """Configurations with one uniform pattern draw per layer."""
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 4242])))
     return [[patterns[int(i)] for i in rng.integers(0, len(patterns), layers)] for _ in range(count)]
+
+
+# ---------------------------------------------------------------------------
+# Persistence: the table is built once offline and reused by every search, so
+# it is kept as JSON together with the calibration of Eq. 1 (gamma, b) and a
+# free-form record of where it was measured.
+
+LUT_FORMAT = "nmspmm-lut/1"
+
+
+def save_lut(path: str, table: Dict[Tuple[Shape, Pattern], float], gamma: Optional[Sequence[float]] = None,
+             b: Optional[float] = None, info: Optional[dict] = None) -> None:
+    """Writes the table (and, if given, the calibrated gamma and b) as JSON."""
+    entries = [{"m": m, "k": k, "n": n, "N": N, "M": M, "us": float(t)}
+               for ((m, k, n), (N, M)), t in sorted(table.items())]
+    doc = {"format": LUT_FORMAT, "entries": entries, "info": info or {}}
+    if gamma is not None:
+        doc["gamma"] = [float(g) for g in gamma]
+        doc["b"] = float(b if b is not None else 0.0)
+    with open(path, "w") as f:
+        json.dump(doc, f, indent=1)
+
+
+def load_lut(path: str) -> Tuple[Dict[Tuple[Shape, Pattern], float], Optional[List[float]], Optional[float], dict]:
+    """Reads a file written by save_lut: (table, gamma or None, b or None, info).
+    Raises ValueError on another format, a duplicate key or a latency that is
+    not a finite non-negative number."""
+    with open(path) as f:
+        doc = json.load(f)
+    if doc.get("format") != LUT_FORMAT:
+        raise ValueError(f"{path}: not a {LUT_FORMAT} file")
+    table: Dict[Tuple[Shape, Pattern], float] = {}
+    for e in doc["entries"]:
+        key = ((int(e["m"]), int(e["k"]), int(e["n"])), (int(e["N"]), int(e["M"])))
+        t = float(e["us"])
+        if key in table:
+            raise ValueError(f"{path}: duplicate entry {key}")
+        if not np.isfinite(t) or t < 0:
+            raise ValueError(f"{path}: bad latency {t} for {key}")
+        table[key] = t
+    gamma = [float(g) for g in doc["gamma"]] if "gamma" in doc else None
+    b = float(doc["b"]) if "b" in doc else None
+    return table, gamma, b, doc.get("info", {})

@@ -10,7 +10,9 @@ from __future__ import annotations
 import ctypes
 import dataclasses
 import os
+import struct
 import threading
+import zlib
 from typing import Optional
 
 import numpy as np
@@ -124,6 +126,57 @@ class Packed:
     vals: np.ndarray
     meta: np.ndarray
     desc: NmDesc
+
+
+# ---------------------------------------------------------------------------
+# Packed-weight files: nm_compress runs once offline, so its output is kept on
+# disk.  Layout (little-endian): 8-byte magic, u32 version, u32 header bytes,
+# the descriptor's fields (8 x i32: n, k, nm_n, nm_m, streams, layout,
+# n_frags, k_steps; 2 x i64: vals_bytes, meta_bytes), CRC-32 of the values
+# and of the positions (2 x u32), then the values and the positions.
+
+PACKED_MAGIC = b"NMSPMM\x00\x01"
+PACKED_VERSION = 1
+_PACKED_HEAD = struct.Struct("<8sII8i2q2I")
+
+
+def save_packed(path: str, p: "Packed") -> None:
+    d = p.desc
+    vals, meta = np.ascontiguousarray(p.vals).view(np.uint8), np.ascontiguousarray(p.meta).view(np.uint8)
+    if vals.size != d.vals_bytes or meta.size != d.meta_bytes:
+        raise ValueError("packed arrays do not match their descriptor")
+    head = _PACKED_HEAD.pack(PACKED_MAGIC, PACKED_VERSION, _PACKED_HEAD.size, d.n, d.k, d.nm_n, d.nm_m, d.streams,
+                             d.layout, d.n_frags, d.k_steps, d.vals_bytes, d.meta_bytes,
+                             zlib.crc32(vals.tobytes()), zlib.crc32(meta.tobytes()))
+    with open(path, "wb") as f:
+        f.write(head)
+        f.write(vals.tobytes())
+        f.write(meta.tobytes())
+
+
+def load_packed(path: str) -> "Packed":
+    """Reads a file written by save_packed.  The descriptor is checked against
+    the library's own nm_compress_size of (n, k, N, M) and both checksums are
+    verified; any mismatch raises ValueError."""
+    with open(path, "rb") as f:
+        raw = f.read()
+    if len(raw) < _PACKED_HEAD.size:
+        raise ValueError(f"{path}: truncated header")
+    (magic, version, hsize, n, k, nm_n, nm_m, streams, layout, n_frags, k_steps, vb, mb, cv,
+     cm) = _PACKED_HEAD.unpack_from(raw)
+    if magic != PACKED_MAGIC or version != PACKED_VERSION or hsize != _PACKED_HEAD.size:
+        raise ValueError(f"{path}: not a packed-weight file of version {PACKED_VERSION}")
+    want = compress_size(n, k, nm_n, nm_m)
+    got = (streams, layout, n_frags, k_steps, vb, mb)
+    if got != (want.streams, want.layout, want.n_frags, want.k_steps, want.vals_bytes, want.meta_bytes):
+        raise ValueError(f"{path}: descriptor does not match nm_compress_size({n}, {k}, {nm_n}, {nm_m})")
+    if len(raw) != hsize + vb + mb:
+        raise ValueError(f"{path}: {len(raw)} bytes, expected {hsize + vb + mb}")
+    vals = np.frombuffer(raw, dtype=np.int8, count=vb, offset=hsize).copy()
+    meta = np.frombuffer(raw, dtype=np.uint8, count=mb, offset=hsize + vb).copy()
+    if zlib.crc32(vals.view(np.uint8).tobytes()) != cv or zlib.crc32(meta.tobytes()) != cm:
+        raise ValueError(f"{path}: checksum mismatch")
+    return Packed(vals, meta, want)
 
 
 def compress_size(n: int, k: int, N: int, M: int) -> NmDesc:
