@@ -811,6 +811,27 @@ def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, comma
     print("\n".join(md))
 
 
+def cache_state(preps) -> str:
+    """What the caches hold when a GEMM of the timed steps starts: every step
+    reuses the same buffers, but the distinct bytes one step touches (inputs,
+    weights and outputs of every sparse and dense GEMM) decide whether the
+    previous step left them in the 256 MB MALL and the 8 x 4 MB of L2."""
+    seen, total = set(), 0
+    for p in preps:
+        tensors = [p.Xd, p.Wd, p.Y, p.Yh, p.Yd, p.Yhd, p.scale]
+        if p.sparse_kernel:
+            tensors += [p.dw.vals, p.dw.meta]
+        for t in tensors:
+            if t is not None and t.data_ptr() not in seen:
+                seen.add(t.data_ptr())
+                total += t.numel() * t.element_size()
+    caches = 256e6 + 32e6
+    if total > caches:
+        return (f"same buffers every step; one step touches {total / 1e9:.2f} GB, over the 288 MB of MALL and L2, "
+                "so the caches cannot keep a step's inputs until the next step")
+    return f"same buffers every step; one step touches {total / 1e6:.0f} MB, so inputs can stay cache-resident"
+
+
 def mfma_ceiling(torch, iters: int = 4000, reps: int = 3) -> dict:
     """Matrix-instruction rate this GPU sustains (nm_probe_mfma_rate), in
     dense-equivalent POPS, on uniform random int8 operands and on zeros: the
@@ -1043,7 +1064,7 @@ def main():
         # per-step totals: the mean above (the paper averages repeated runs); the median is robust to outliers
         "sparse_ms_per_step_median": round(float(np.median(t[:, [gi for gi, ((sd, _), _) in enumerate(groups)
                                                                   if sd == "sparse"]].sum(axis=1))), 4),
-        "cache_state": "hot: the same input and output buffers every step (inputs stay resident)",
+        "cache_state": cache_state(preps),
         "dense_ms_per_step": round(float(dense_ms), 4),
         "roofline": roofline,
     }
