@@ -685,6 +685,57 @@ def shape_report(torch, report, cfgs=(0, 1, 2, 3, 4)):
             "mfma_measured": ceil}
 
 
+def graph_layer(torch, reps: int = 200) -> dict:
+    """One DeiT-Base layer's four linears (qkv, proj, fc1, fc2; 2:4, int32
+    output) at batch 1 and 8, launched from Python one call at a time as an
+    application would (no pre-queued sleep), against the same four calls
+    captured once in a HIP graph and replayed: mean microseconds per layer."""
+    res = {}
+    E = torch.cuda.Event
+    for batch in (1, 8):
+        m = 197 * batch
+        rng = np.random.default_rng(batch)
+        calls = []
+        for k, n in ((768, 2304), (768, 768), (768, 3072), (3072, 768)):
+            X = torch.from_numpy(wl.gen_x(m, k, rng)).cuda()
+            W, _ = wl.gen_w(n, k, 2, 4, rng)
+            dw = nmspmm.DeviceWeight.from_packed(nmspmm.compress(W, 2, 4))
+            Y = torch.empty((m, n), dtype=torch.int32, device="cuda")
+            calls.append(lambda X=X, dw=dw, Y=Y: nmspmm.spmm(X, dw, Y=Y))
+
+        def layer():
+            for c in calls:
+                c()
+        for _ in range(3):
+            layer()
+        torch.cuda.synchronize()
+        e0, e1 = E(enable_timing=True), E(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            layer()
+        e1.record()
+        torch.cuda.synchronize()
+        eager_us = e0.elapsed_time(e1) * 1e3 / reps
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            layer()
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            layer()
+        g.replay()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        graph_us = e0.elapsed_time(e1) * 1e3 / reps
+        res[f"b{batch}"] = {"m": m, "eager_us_per_layer": round(eager_us, 2), "graph_us_per_layer": round(graph_us, 2)}
+    return res
+
+
 def write_sweep_report(sweep_json, path):
     """Markdown table of a planner evaluation written by --sweep-out."""
     d = json.load(open(sweep_json))
@@ -906,6 +957,8 @@ def main():
                     help="the paper's kernel benchmark grid vs the dense GEMMs (prints one JSON line)")
     ap.add_argument("--chaining", action="store_true",
                     help="int8 requantisation epilogue and activation quantiser timings (prints one JSON line)")
+    ap.add_argument("--graph-layer", action="store_true",
+                    help="DeiT-Base layer at batch 1 and 8: Python launches vs one HIP graph replay (one JSON line)")
     ap.add_argument("--shape-report", action="store_true",
                     help="per-shape roofline of every workload GEMM (prints one JSON line; --report for markdown)")
     ap.add_argument("--cal", type=int, default=64, help="calibration configurations for --predictor")
@@ -948,6 +1001,9 @@ def main():
         return
     if args.shape_report:
         print(json.dumps({"shape_report": shape_report(torch, args.report)}), flush=True)
+        return
+    if args.graph_layer:
+        print(json.dumps({"graph_layer": graph_layer(torch)}), flush=True)
         return
 
     work = wl.workload(args.config)
