@@ -617,6 +617,7 @@ def shape_report(torch, report, cfgs=(0, 1, 2, 3, 4)):
     peaks, the compute fraction against the matrix-instruction rate measured in
     the same run on random operands, and the roofline fraction (the binding
     one).  Times: mean of 5 back-to-back launches, inputs resident."""
+    from paper_2607_12505_amd import latency as lt
     ceil = mfma_ceiling(torch)
     sp_rate = ceil["smfmac_i32_16x16x128_i8_random_pops"] * 1e3       # dense-equivalent TOPS
     dn_rate = ceil["mfma_i32_16x16x64_i8_random_pops"] * 1e3
@@ -635,7 +636,20 @@ def shape_report(torch, report, cfgs=(0, 1, 2, 3, 4)):
         torch.cuda.synchronize()
         each = time_each(preps, torch)
         outs = ("int32" if work.out_int32 else "") + ("+fp16" if work.out_f16 else "")
-        for p, (ts, td) in zip(preps, each):
+        # the vendor dense INT8 GEMM (hipBLASLt through torch._int_mm, int32
+        # output) beside ours, where the outputs are the same (int32 only)
+        vendor = []
+        for p in preps:
+            if work.out_f16 or not work.out_int32:
+                vendor.append(None)
+                continue
+            WdT = p.Wd.t().contiguous()
+            try:
+                vendor.append(lt.time_launches(torch, lambda: torch._int_mm(p.Xd, WdT), 5) * 1e-3)
+            except RuntimeError:
+                vendor.append(None)
+            del WdT
+        for p, (ts, td), tv in zip(preps, each, vendor):
             g, kind = p.g, p.splan.kind
             ops = g.dense_eq_ops
             peak = PEAK_SPARSE_TOPS if kind == nmspmm.NM_KIND_SP42 else PEAK_INT8_TOPS
@@ -651,7 +665,8 @@ def shape_report(torch, report, cfgs=(0, 1, 2, 3, 4)):
                          "bound": "mfma" if t_mfma > t_hbm else "hbm",
                          "mfma_frac": t_mfma / ts, "mfma_frac_measured": ops / (rate * 1e9) / ts,
                          "hbm_gbs": b / (ts * 1e-3) / 1e9, "hbm_frac": t_hbm / ts, "roofline_frac": max(t_mfma, t_hbm) / ts,
-                         "dense_roofline_frac": max(td_mfma, td_hbm) / td})
+                         "dense_roofline_frac": max(td_mfma, td_hbm) / td,
+                         "vendor_us": tv * 1e3 if tv is not None else None})
         log(f"shape report: {work.name} done ({len(preps)} shapes)")
         del preps
         torch.cuda.empty_cache()
@@ -667,20 +682,25 @@ def shape_report(torch, report, cfgs=(0, 1, 2, 3, 4)):
               "Roofline fraction = max(compute time at peak, algorithmic bytes at 8 TB/s) / measured time; "
               "algorithmic bytes count the compact packed weight (N/M of the values plus ceil(log2 M) bits per value).  "
               "Each row has its own input and output buffers; the dense time of one shape, measured again in every "
-              "pattern row, shows the run-to-run spread (largest on the biggest outputs).", "",
+              "pattern row, shows the run-to-run spread (largest on the biggest outputs).  \"vendor dense\": the dense "
+              "INT8 GEMM of hipBLASLt through torch._int_mm (int32 output, so only for the int32-only workloads), "
+              "timed beside ours as a reference for the dense baseline.", "",
               "| workload | GEMM | m | k | n | N:M | out | sparse kernel | sparse us | dense us | speedup | TOPS | bound | "
-              "MFMA frac | MFMA frac (meas.) | GB/s | HBM frac | roofline frac | dense roofline frac |",
-              "|---|---|---:|---:|---:|---|---|---|---:|---:|---:|---:|---|---:|---:|---:|---:|---:|---:|"]
+              "MFMA frac | MFMA frac (meas.) | GB/s | HBM frac | roofline frac | dense roofline frac | vendor dense us |",
+              "|---|---|---:|---:|---:|---|---|---|---:|---:|---:|---:|---|---:|---:|---:|---:|---:|---:|---:|"]
         for r in rows:
             md.append(f"| {r['workload']} | {r['gemm']} | {r['m']} | {r['k']} | {r['n']} | {r['pattern']} | {r['outputs']} "
                       f"| `{r['kernel']}` | {r['sparse_us']:.1f} | {r['dense_us']:.1f} | {r['speedup']:.2f} | "
                       f"{r['tops']:.0f} | {r['bound']} | {r['mfma_frac']:.3f} | {r['mfma_frac_measured']:.3f} | "
                       f"{r['hbm_gbs']:.0f} | {r['hbm_frac']:.3f} | {r['roofline_frac']:.3f} | "
-                      f"{r['dense_roofline_frac']:.3f} |")
+                      f"{r['dense_roofline_frac']:.3f} | "
+                      f"{'—' if r['vendor_us'] is None else format(r['vendor_us'], '.1f')} |")
         with open(report, "w") as f:
             f.write("\n".join(md) + "\n")
     fr = np.array([r["roofline_frac"] for r in rows])
+    vd = [(r["vendor_us"], r["dense_us"]) for r in rows if r["vendor_us"] is not None]
     return {"shapes": len(rows), "roofline_frac_median": round(float(np.median(fr)), 3),
+            "dense_vs_vendor_median": round(float(np.median([v / d for v, d in vd])), 3) if vd else None,
             "roofline_frac_min": round(float(fr.min()), 3), "roofline_frac_max": round(float(fr.max()), 3),
             "mfma_measured": ceil}
 
