@@ -231,11 +231,20 @@ def cpu_baseline(preps, budget_s, check):
         if check and p.Y is not None:
             mism += int((p.Y[:r].cpu().numpy() != Yc).sum())
     dt = time.perf_counter() - t0
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
+    from oracle import build as oracle_build
     return {
         "value": ops / dt / 1e12,
         "unit": "TOPS (dense-equivalent INT8)",
         "cores": threads,
         "kind": "oracle",
+        "cpu_model": model,
+        "compiler": "gcc " + " ".join(oracle_build.CFLAGS),
         "sample": f"first {frac * 100:.2f}% of the rows of each of the {len(preps)} GEMMs "
                   f"({ops / 1e9:.1f} dense-eq GOP in {dt:.1f} s)",
     }, mism
