@@ -1,0 +1,31 @@
+"""bench.py end to end on every workload configuration (one short step each,
+in this process): the JSON line carries the contract's fields with sane
+values, and the roofline object names the dominant kernel."""
+import json
+import sys
+
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+KEYS = ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better", "scaling",
+        "vs_baseline", "dtype", "data", "config", "roofline", "cpu_baseline", "speedup_vs_dense", "per_pattern")
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_bench_config_line(cfg, capsys, monkeypatch):
+    import bench
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--config", str(cfg), "--steps", "1", "--warmup", "1",
+                                      "--no-cpu-baseline", "--no-secondary", "--no-mfma-ceiling"])
+    bench.main()
+    line = json.loads(capsys.readouterr().out.strip().splitlines()[-1])
+    for k in KEYS:
+        assert k in line, k
+    assert line["n_gpus"] == 1 and line["steps"] == 1 and line["higher_is_better"] is True
+    assert line["value"] > 0 and line["ms_per_step"] > 0 and line["speedup_vs_dense"] > 0
+    assert line["dtype"] == "int8" and line["vs_baseline"] is None and line["cpu_baseline"] is None
+    r = line["roofline"]
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert 0 < r["frac"] <= 1 and r["kernel"].startswith("k_gemm")
+    assert abs(r["achieved"] / r["peak"] - r["frac"]) < 1e-3
+    assert line["config"]["workload"]
