@@ -59,6 +59,12 @@ __device__ inline int map_block(int bid, int nwg) {
 // that makes a buffer access coherent at agent scope (sc1).
 constexpr int kBufferFlags = 0x00020000;
 constexpr int kSc1 = 16;
+// Cache policy of the output stores: non-temporal.  Timed inside whole
+// workload steps (every GEMM's buffers evicted by the others' traffic before
+// it runs again), streaming the outputs past L2 and the last-level cache beat
+// the default and the device-scope (sc1) policies on every workload, by up to
+// a third on outputs larger than the 256 MB last-level cache.
+constexpr int kStoreNT = 2;
 
 // Direct-to-LDS loads: lane L's bytes land at lds_base + L * size.  lds_base
 // must be wave-uniform (it goes through M0).  M0 is a register the compiler
@@ -163,7 +169,7 @@ __device__ inline void emit_out(const GemmArgs &a, int tok, int ch, const v4i &v
     const uint32_t elems = (uint32_t)a.m * (uint32_t)a.n;
     if (a.Y) {
         const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(a.Y, 0, (int)(elems * 4), kBufferFlags);
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, v), r, (int)(e * 4), 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, v), r, (int)(e * 4), 0, kStoreNT);
     }
     if (a.Yh) {
         v4u16 h;
@@ -173,14 +179,14 @@ __device__ inline void emit_out(const GemmArgs &a, int tok, int ch, const v4i &v
             h[i] = __builtin_bit_cast(unsigned short, x);
         }
         const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(a.Yh, 0, (int)(elems * 2), kBufferFlags);
-        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u, h), r, (int)(e * 2), 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u, h), r, (int)(e * 2), 0, kStoreNT);
     }
     if (a.Yq) {
         uint32_t packed = 0;
 #pragma unroll
         for (int i = 0; i < 4; ++i) packed |= (uint32_t)(q8((float)v[i] * es.qs[i]) & 0xFF) << (8 * i);
         const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(a.Yq, 0, (int)elems, kBufferFlags);
-        __builtin_amdgcn_raw_buffer_store_b32(packed, r, (int)e, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(packed, r, (int)e, 0, kStoreNT);
     }
 }
 
