@@ -19,6 +19,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import dataclasses
 import json
 import os
 import sys
@@ -250,6 +251,23 @@ def cpu_baseline(preps, budget_s, check):
     }, mism
 
 
+def sweep_summary(rows):
+    """Table-1 figures of a set of sweep rows: the planner's Top-1 hit rate, its
+    average and worst time normalised to the sweep optimum, and the gain over a
+    fixed split_k = 1 with the planner's tile."""
+    if not rows:
+        return None
+    norm = np.array([r["t_best_us"] / r["t_planned_us"] for r in rows])
+    fixed = np.array([r["t_fixed_split1_us"] / r["t_planned_us"] for r in rows if r["t_fixed_split1_us"]])
+    return {
+        "cases": len(rows),
+        "top1_hit_rate": round(float(np.mean([r["planned"] == r["best"] for r in rows])), 3),
+        "avg_norm_perf": round(float(norm.mean()), 3),
+        "worst_norm_perf": round(float(norm.min()), 3),
+        "gain_over_fixed_split1": round(float(fixed.mean()), 3) if len(fixed) else None,
+    }
+
+
 def sweep(configs, torch, reps, out_path):
     """Planner evaluation in the manner of the paper's Table 1: for every
     distinct (shape, N:M) of the workloads, time every (tile, split_k)
@@ -262,8 +280,16 @@ def sweep(configs, torch, reps, out_path):
     for cfg in configs:
         work = wl.workload(cfg)
         out = (nmspmm.NM_OUT_I32 if work.out_int32 else 0) | (nmspmm.NM_OUT_F16 if work.out_f16 else 0)
+        cases = []
         for g in work.gemms:
-            key = (g.m, g.k, g.n, g.N, g.M, out)
+            cases.append(g)
+            if g.N < g.M:
+                # the dense baseline of the same shape, whose plan is the
+                # denominator of every speedup
+                base = " ".join(t for t in g.name.split() if ":" not in t)
+                cases.append(dataclasses.replace(g, name="dense " + base, N=8, M=8))
+        for g in cases:
+            key = (g.m, g.k, g.n, g.N == g.M or (g.N, g.M), out)
             if key in seen:
                 continue
             seen.add(key)
@@ -277,15 +303,22 @@ def sweep(configs, torch, reps, out_path):
             else:
                 Wd = torch.from_numpy(W).cuda()
                 planned = nmspmm.dense_plan(g.m, g.n, g.k, out)
-            nsets = max(1, min(4, int(400e6 // (6 * g.m * g.n))))
+            # rotate the outputs over at least two buffers and 512 MB in all
+            # (twice the last-level cache), as a network's consecutive layers
+            # write fresh buffers
+            out_bytes = g.m * g.n * ((4 if out & 1 else 0) + (2 if out & 2 else 0))
+            nsets = int(min(64, max(2, -(-512e6 // out_bytes))))
             Ys = [torch.empty((g.m, g.n), dtype=torch.int32, device="cuda") if out & 1 else None for _ in range(nsets)]
             Yhs = [torch.empty((g.m, g.n), dtype=torch.int16, device="cuda") if out & 2 else None for _ in range(nsets)]
             ws = torch.zeros(64 << 20, dtype=torch.uint8, device="cuda")
             times = {}
-            # two passes over the candidates, keeping each one's faster mean:
-            # a candidate slowed once by a transient (clock, co-runner) is not
-            # mistaken for a slow schedule
-            for tile in list(range(nmspmm.num_tiles())) * 2:
+            cursor = 0  # the next output buffer in the rotation
+            # two passes over the candidates, the second in reverse order,
+            # keeping each one's faster mean: a candidate slowed once by a
+            # transient (clock or power state left by the kernels before it)
+            # is not mistaken for a slow schedule
+            order = list(range(nmspmm.num_tiles()))
+            for tile in order + order[::-1]:
                 tn_, tm_ = nmspmm.tile_info(tile)
                 tiles = -(-g.n // tn_) * -(-g.m // tm_)
                 for split in (1, 2, 4, 8):
@@ -304,11 +337,14 @@ def sweep(configs, torch, reps, out_path):
                     except nmspmm.NmError:
                         continue
                     torch.cuda.synchronize()
-                    torch.cuda._sleep(int(2.4e9 * 20e-6 * reps))
+                    # queue the launches behind a 1 ms spin, which also lets
+                    # the clock recover from the previous candidate
+                    torch.cuda._sleep(int(2.4e9 * 100e-6 * reps))
                     e0, e1 = E(enable_timing=True), E(enable_timing=True)
                     e0.record()
                     for r in range(reps):
-                        run(r % nsets)
+                        run(cursor % nsets)
+                        cursor += 1
                     e1.record()
                     torch.cuda.synchronize()
                     t_us = e0.elapsed_time(e1) / reps * 1e3
@@ -325,19 +361,12 @@ def sweep(configs, torch, reps, out_path):
             log(f"cfg{cfg} {g.name:<20} m={g.m:<6} k={g.k:<5} n={g.n:<5} planned t{chosen[0]}/s{chosen[1]} "
                 f"{t_plan:7.1f} us  best t{best[0]}/s{best[1]} {times[best]:7.1f} us  "
                 f"norm {times[best] / t_plan:.3f}")
-    norm = np.array([r["t_best_us"] / r["t_planned_us"] for r in rows])
-    fixed = np.array([r["t_fixed_split1_us"] / r["t_planned_us"] for r in rows if r["t_fixed_split1_us"]])
-    summary = {
-        "cases": len(rows),
-        "top1_hit_rate": round(float(np.mean([r["planned"] == r["best"] for r in rows])), 3),
-        "avg_norm_perf": round(float(norm.mean()), 3),
-        "worst_norm_perf": round(float(norm.min()), 3),
-        "gain_over_fixed_split1": round(float(fixed.mean()), 3),
-    }
-    log(json.dumps(summary))
+    summary = sweep_summary([r for r in rows if r["pattern"] != "dense"])
+    dense_summary = sweep_summary([r for r in rows if r["pattern"] == "dense"])
+    log(json.dumps({"sparse": summary, "dense": dense_summary}))
     if out_path:
         with open(out_path, "w") as f:
-            json.dump({"summary": summary, "rows": rows}, f, indent=1)
+            json.dump({"summary": summary, "dense_summary": dense_summary, "rows": rows}, f, indent=1)
     return summary
 
 
@@ -771,16 +800,22 @@ def write_sweep_report(sweep_json, path):
     s = d["summary"]
     md = ["# Planner evaluation (Table-1 methodology) on MI355X", "",
           "Commands: `python3 bench.py --sweep 0,1,2,3,4 --sweep-out sweep.json` (GPU; every (tile, split_k) "
-          "candidate timed in two passes of 10 launches each, the faster pass kept, outputs rotated over buffers "
-          "larger than the 256 MB last-level cache), "
+          "candidate timed in two passes of 10 launches each (the second pass in reverse order, each behind a 1 ms "
+          "spin), the faster pass kept, outputs rotated over at least two "
+          "buffers and at least 512 MB in all, twice the last-level cache), "
           "then `python3 bench.py --sweep-report sweep.json --report <this file>`.", "",
           "Normalised performance = t(sweep optimum) / t(planner choice); tile indices are those of the "
           "library's tile table (`nm_tile_info`).", "",
-          f"Summary: {s['cases']} distinct (shape, N:M) cases; planner Top-1 hit rate {s['top1_hit_rate']}, "
-          f"average normalised performance {s['avg_norm_perf']}, worst {s['worst_norm_perf']}; gain over a fixed "
-          f"split_k = 1 with the same tile {s['gain_over_fixed_split1']}.", "",
-          "| workload | m | k | n | N:M | planner tile/split | us | best tile/split | us | norm |",
-          "|---|---:|---:|---:|---|---|---:|---|---:|---:|"]
+          f"Summary, sparse GEMMs: {s['cases']} distinct (shape, N:M) cases; planner Top-1 hit rate "
+          f"{s['top1_hit_rate']}, average normalised performance {s['avg_norm_perf']}, worst {s['worst_norm_perf']}; "
+          f"gain over a fixed split_k = 1 with the same tile {s['gain_over_fixed_split1']}.", ""]
+    ds = d.get("dense_summary")
+    if ds:
+        md += [f"Dense INT8 baseline (every sparse shape's dense counterpart and the dense layers of the chain): "
+               f"{ds['cases']} distinct shapes; planner Top-1 hit rate {ds['top1_hit_rate']}, average normalised "
+               f"performance {ds['avg_norm_perf']}, worst {ds['worst_norm_perf']}.", ""]
+    md += ["| workload | m | k | n | N:M | planner tile/split | us | best tile/split | us | norm |",
+           "|---|---:|---:|---:|---|---|---:|---|---:|---:|"]
     for r in d["rows"]:
         md.append(f"| cfg{r['cfg']} {r['gemm']} | {r['m']} | {r['k']} | {r['n']} | {r['pattern']} | "
                   f"{r['planned'][0]}/{r['planned'][1]} | {r['t_planned_us']:.1f} | {r['best'][0]}/{r['best'][1]} | "

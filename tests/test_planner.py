@@ -67,9 +67,17 @@ def test_large_shapes_use_large_tiles():
     d = nmspmm.compress_size(3072, 768, 2, 4)
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # DeiT-Base fc1 at batch 128
     assert nmspmm.plan_kernel_name(p) == "k_gemm<1, 2, 2, 4, 4, 2>"   # 128 x 128, 2-slot ring
-    d = nmspmm.compress_size(4096, 1024, 4, 8)
-    p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)    # ViT-L fc1, two-stream weight
+    d = nmspmm.compress_size(3072, 1024, 4, 8)
+    p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)    # ViT-L qkv, two-stream weight
     assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 2, 2, 4, 4, 2>"
+    # the widest outputs of the heavier operands: 256 x 256 on 8 waves (ViT-L fc1)
+    d = nmspmm.compress_size(4096, 1024, 4, 8)
+    p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)
+    assert (p.tile_n, p.tile_m) == (256, 256) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 2, 4, 8, 4, 3>"
+    p = nmspmm.dense_plan(18464, 4096, 1024, nmspmm.NM_OUT_I32)
+    assert (p.tile_n, p.tile_m) == (256, 256)
+    d = nmspmm.compress_size(4096, 1024, 2, 4)           # one-stream weight: 128 x 128
+    assert (nmspmm.spmm_plan(d, 18464, 1).tile_n, nmspmm.spmm_plan(d, 18464, 1).tile_m) == (128, 128)
     d = nmspmm.compress_size(768, 3072, 2, 4)
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # fc2 at batch 128
     assert (p.tile_n, p.tile_m) == (128, 128)
@@ -82,21 +90,29 @@ def test_large_shapes_use_large_tiles():
     d = nmspmm.compress_size(384, 384, 2, 4)
     assert (nmspmm.spmm_plan(d, 12608, 1).tile_n, nmspmm.spmm_plan(d, 12608, 1).tile_m) == (128, 64)
     # medium token counts: half-height tiles, narrower for two-stream weights
-    d = nmspmm.compress_size(1536, 2048, 2, 4)
+    # (Swin-B stage 3 qkv, k = 512)
+    d = nmspmm.compress_size(1536, 512, 2, 4)
     assert (nmspmm.spmm_plan(d, 6272, 1).tile_n, nmspmm.spmm_plan(d, 6272, 1).tile_m) == (128, 64)
-    d = nmspmm.compress_size(1536, 2048, 4, 8)
+    d = nmspmm.compress_size(1536, 512, 4, 8)
     assert (nmspmm.spmm_plan(d, 6272, 1).tile_n, nmspmm.spmm_plan(d, 6272, 1).tile_m) == (64, 128)
+    # ... but 128 x 128 for long reductions while every compute unit gets a
+    # tile (Swin-B stage 2 fc2, k = 1024: 392 tiles), not when fewer (stage 3
+    # fc2, k = 2048: 196 tiles)
+    d = nmspmm.compress_size(256, 1024, 2, 4)
+    assert (nmspmm.spmm_plan(d, 25088, 1).tile_n, nmspmm.spmm_plan(d, 25088, 1).tile_m) == (128, 128)
+    d = nmspmm.compress_size(512, 2048, 2, 4)
+    assert (nmspmm.spmm_plan(d, 6272, 1).tile_n, nmspmm.spmm_plan(d, 6272, 1).tile_m) == (128, 64)
     # ... or 64 x 64 when half-height tiles would leave compute units idle
     # (DeiT-Base fc2 at batch 8: 150 tiles of 128 x 64 on 256 compute units)
     d = nmspmm.compress_size(768, 3072, 2, 4)
     assert (nmspmm.spmm_plan(d, 1576, 1).tile_n, nmspmm.spmm_plan(d, 1576, 1).tile_m) == (64, 64)
     assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 1576, 1)) == "k_gemm<1, 2, 2, 2, 2, 2>"
-    # one or two k-steps: 64 x 64 tiles (Swin-B stage 1, k = 128), 128 x 64
-    # for wide one-stream outputs (Swin-B stage 2 qkv, k = 256)
+    # one or two k-steps: 64 x 64 tiles (Swin-B stage 1, k = 128; stage 2
+    # qkv, k = 256)
     d = nmspmm.compress_size(384, 128, 2, 4)
     assert (nmspmm.spmm_plan(d, 100352, 1).tile_n, nmspmm.spmm_plan(d, 100352, 1).tile_m) == (64, 64)
     d = nmspmm.compress_size(768, 256, 2, 4)
-    assert (nmspmm.spmm_plan(d, 25088, 1).tile_n, nmspmm.spmm_plan(d, 25088, 1).tile_m) == (128, 64)
+    assert (nmspmm.spmm_plan(d, 25088, 1).tile_n, nmspmm.spmm_plan(d, 25088, 1).tile_m) == (64, 64)
 
 
 def test_forced_plan_validation():
