@@ -161,6 +161,59 @@ def time_steps(preps, groups, steps, torch, sleep_cycles):
     return t
 
 
+def graph_steps(preps, groups, steps, torch, sleep_cycles):
+    """The step's launches captured once per side (sparse, dense) in a HIP
+    graph, in the same group order, and replayed `steps` times behind the same
+    device sleep; returns the mean sparse and dense milliseconds per step.
+    The outputs are rewritten by every replay, so the sampled-row parity check
+    that follows sees the graphs' results."""
+    side = torch.cuda.Stream()
+    h = ctypes.c_void_p(side.cuda_stream)
+
+    def on_side(args):  # the stream is argument 10 of both entry points
+        a = list(args)
+        a[10] = h
+        return tuple(a)
+    calls = {"sparse": [], "dense": []}
+    for (kind, _), idx in groups:
+        for i in idx:
+            p = preps[i]
+            calls[kind].append((p.sparse_fn, on_side(p.sparse_args)) if kind == "sparse"
+                               else (p.dense_fn, on_side(p.dense_args)))
+
+    def run(kind):
+        for fn, a in calls[kind]:
+            st = fn(*a)
+            if st:
+                raise nmspmm.NmError(st, f"graph step ({kind})")
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run("sparse")
+        run("dense")
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graphs = {}
+    for kind in ("sparse", "dense"):
+        graphs[kind] = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graphs[kind], stream=side):
+            run(kind)
+    torch.cuda.synchronize()
+    E = torch.cuda.Event
+    ev = [[E(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    for s in range(steps):
+        if sleep_cycles:
+            torch.cuda._sleep(sleep_cycles)
+        ev[s][0].record()
+        graphs["sparse"].replay()
+        ev[s][1].record()
+        graphs["dense"].replay()
+        ev[s][2].record()
+    torch.cuda.synchronize()
+    sp = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    dn = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    return sp, dn
+
+
 def time_each(preps, torch, reps=5):
     """Untimed detail pass: mean time of each GEMM, sparse and dense, each
     over `reps` back-to-back launches (for the per-GEMM table only)."""
@@ -998,6 +1051,8 @@ def main():
                     help="skip the DeiT-Base per-batch speedups reported beside the main line")
     ap.add_argument("--no-mfma-ceiling", action="store_true",
                     help="skip the measured matrix-instruction rate reported beside the main line")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the HIP-graph replay of the step reported beside the main line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after timing, run one plain device copy of MIB MiB (profiler counter calibration)")
     ap.add_argument("--sweep", type=str, default=None,
@@ -1092,6 +1147,8 @@ def main():
     wall = time.perf_counter() - w0
     ms_per_step = wall * 1e3 / args.steps
     tg = t.mean(axis=0)  # per group: mean over steps (the paper averages repeated runs, Sec. 5.1)
+    graph_sparse_ms, graph_dense_ms = (graph_steps(preps, groups, args.steps, torch, sleep_cycles)
+                                       if not args.no_graph else (None, None))
 
     ops = np.array([p.g.dense_eq_ops for p in preps], np.float64)
     sparse_ms = sum(tg[gi] for gi, ((side, _), _) in enumerate(groups) if side == "sparse")
@@ -1188,6 +1245,16 @@ def main():
         "dense_ms_per_step": round(float(dense_ms), 4),
         "roofline": roofline,
     }
+    if graph_sparse_ms is not None:
+        # the same step with its launches replayed from HIP graphs (no host
+        # launch path between kernels): context, not `value`
+        line["hip_graph"] = {
+            "sparse_ms_per_step": round(graph_sparse_ms, 4),
+            "dense_ms_per_step": round(graph_dense_ms, 4),
+            "tops": round(float(ops.sum() / (graph_sparse_ms * 1e-3) / 1e12), 2),
+            "speedup_vs_dense": round(graph_dense_ms / graph_sparse_ms, 3),
+        }
+        log(json.dumps({"hip_graph": line["hip_graph"]}))
     if not args.no_mfma_ceiling:
         line["mfma_measured"] = mfma_ceiling(torch)
         log(json.dumps(line["mfma_measured"]))
