@@ -234,6 +234,35 @@ def time_each(preps, torch, reps=5):
     return out
 
 
+def time_keyed_in_steps(preps, key, torch, reps):
+    """Untimed detail pass in the step's own cache state: `reps` whole steps in
+    which the GEMMs are ordered by `key(prep)` (sparse calls of each key, then
+    the dense calls of each key) with an event at every key boundary only, so
+    no event separates two GEMMs of one key; returns {key: (sparse ms, dense
+    ms)} per step.  Each step starts behind a device sleep long enough for the
+    host to queue it."""
+    E = torch.cuda.Event
+    keys = sorted({key(p) for p in preps})
+    members = {k: [p for p in preps if key(p) == k] for k in keys}
+    sleep_cycles = int(2.4e9 * 25e-6 * 2 * len(preps))
+    ev = [[E(enable_timing=True) for _ in range(2 * len(keys) + 1)] for _ in range(reps)]
+    for r in range(reps):
+        torch.cuda._sleep(sleep_cycles)
+        ev[r][0].record()
+        for side in (0, 1):
+            for j, k in enumerate(keys):
+                for p in members[k]:
+                    p.run_dense() if side else p.run_sparse()
+                ev[r][side * len(keys) + j + 1].record()
+    torch.cuda.synchronize()
+    out = {}
+    for j, k in enumerate(keys):
+        sp = np.mean([ev[r][j].elapsed_time(ev[r][j + 1]) for r in range(reps)])
+        dn = np.mean([ev[r][len(keys) + j].elapsed_time(ev[r][len(keys) + j + 1]) for r in range(reps)])
+        out[k] = (float(sp), float(dn))
+    return out
+
+
 def secondary_workload(cfg, steps, warmup, torch):
     """Speedup over the dense baseline per (token count, N:M) on another
     workload (same protocol as the main measurement, fewer steps); reported
@@ -246,15 +275,11 @@ def secondary_workload(cfg, steps, warmup, torch):
     sleep_cycles = int(2.4e9 * 25e-6 * len(preps) * 2)
     groups = launch_groups(preps)
     time_steps(preps, groups, max(1, warmup), torch, sleep_cycles)
-    each = np.zeros((len(preps), 2))
-    for _ in range(steps):
-        each += time_each(preps, torch, reps=3)
-    each /= steps
+    keyfn = lambda p: (p.g.m, pattern_name(p.g))
+    times = time_keyed_in_steps(preps, keyfn, torch, 3 * steps)
     out = {}
-    for key in sorted({(p.g.m, pattern_name(p.g)) for p in preps}):
-        sel = [i for i, p in enumerate(preps) if (p.g.m, pattern_name(p.g)) == key]
-        ops = sum(preps[i].g.dense_eq_ops for i in sel)
-        ts, td = each[sel, 0].sum(), each[sel, 1].sum()
+    for key, (ts, td) in times.items():
+        ops = sum(p.g.dense_eq_ops for p in preps if keyfn(p) == key)
         out[f"m={key[0]} {key[1]}"] = {"tops": round(ops / (ts * 1e-3) / 1e12, 1),
                                         "speedup_vs_dense": round(float(td / ts), 3)}
     del preps
@@ -1157,15 +1182,13 @@ def main():
     dense_tops = ops.sum() / (dense_ms * 1e-3) / 1e12
     speedup = dense_ms / sparse_ms
 
-    # per GEMM and per pattern (detail pass, outside the timed region)
-    each = time_each(preps, torch)
-    ts, td = each[:, 0], each[:, 1]
+    # per pattern (detail pass in whole steps ordered by pattern, outside the timed region)
     per_pattern = {}
-    for pat in sorted({pattern_name(p.g) for p in preps}):
+    for pat, (ts, td) in time_keyed_in_steps(preps, lambda p: pattern_name(p.g), torch, 5).items():
         sel = np.array([pattern_name(p.g) == pat for p in preps])
         per_pattern[pat] = {
-            "tops": round(float(ops[sel].sum() / (ts[sel].sum() * 1e-3) / 1e12), 1),
-            "speedup_vs_dense": round(float(td[sel].sum() / ts[sel].sum()), 3),
+            "tops": round(float(ops[sel].sum() / (ts * 1e-3) / 1e12), 1),
+            "speedup_vs_dense": round(float(td / ts), 3),
         }
 
     # dominant kernel: the sparse-side kernel instantiation with the most time per step
@@ -1202,6 +1225,10 @@ def main():
         "algorithmic_bytes_per_launch": int(dom["bytes"] / dom["launches"]),
     }
 
+    # per GEMM, inside whole steps with an event after every GEMM (stderr table only)
+    per_gemm = time_keyed_in_steps(preps, lambda p: preps.index(p), torch, 3)
+    ts = np.array([per_gemm[i][0] for i in range(len(preps))])
+    td = np.array([per_gemm[i][1] for i in range(len(preps))])
     log(f"\n{'gemm':<22}{'m':>7}{'k':>6}{'n':>6}  {'sparse kernel':<30}{'sparse us':>10}{'dense us':>10}"
         f"{'TOPS':>8}{'dTOPS':>8}{'spd':>7}{'GB/s':>8}")
     for i, p in enumerate(preps):
