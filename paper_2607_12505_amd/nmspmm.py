@@ -311,6 +311,50 @@ class DeviceWeight:
         return cls(v, m, p.desc)
 
 
+def _need(t, name, dtypes, shape=None, numel=None):
+    """Validates one tensor argument before its address reaches the library:
+    the C ABI takes bare pointers, so a tensor of the wrong size, type or
+    layout would otherwise be read or written out of bounds on the GPU."""
+    if t is None:
+        return
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected one of {[str(d) for d in dtypes]}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name}: {t.numel()} elements, at least {numel} needed")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+
+
+def _on_device(named, device=None):
+    """Every given tensor is a device tensor, all on one device."""
+    for name, t in named:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError(f"{name}: must be a device tensor")
+        if device is None:
+            device = t.device
+        elif t.device != device:
+            raise ValueError(f"{name}: on {t.device}, expected {device}")
+
+
+def _check_outputs(torch, m, n, Y, scale, Yh, Yq, qscale):
+    _need(Y, "Y", (torch.int32,), (m, n))
+    _need(Yh, "Yh", (torch.float16, torch.int16), (m, n))
+    _need(Yq, "Yq", (torch.int8,), (m, n))
+    _need(scale, "scale", (torch.float32,), (n,))
+    _need(qscale, "qscale", (torch.float32,), (n,))
+
+
+_WS_DTYPES = ("uint8", "int8", "int32", "int64", "float32")
+
+
+def _check_ws(torch, ws):
+    _need(ws, "ws", tuple(getattr(torch, d) for d in _WS_DTYPES))
+
+
 def _outputs(Y, scale, Yh, Yq, qscale) -> NmOutputs:
     return NmOutputs(_ptr(Y), _ptr(Yh), _ptr(scale), _ptr(Yq), _ptr(qscale))
 
@@ -326,7 +370,18 @@ def spmm(X, w: DeviceWeight, Y=None, scale=None, Yh=None, plan: Optional[NmPlan]
     view of binary16) and Yq (int8) are written in place; returns (Y, Yh), or
     (Y, Yh, Yq) when Yq is given.  Without Yq this calls nm_spmm_ex, with it
     nm_spmm_out."""
+    torch = _torch()
+    d = w.desc
+    if X.dim() != 2:
+        raise ValueError(f"X: {X.dim()}-D, expected [m x {d.k}]")
     m = X.shape[0]
+    _need(X, "X", (torch.int8,), (m, d.k))
+    _need(w.vals, "w.vals", (torch.int8,), numel=d.vals_bytes)
+    _need(w.meta, "w.meta", (torch.uint8,), numel=d.meta_bytes)
+    _check_outputs(torch, m, d.n, Y, scale, Yh, Yq, qscale)
+    _check_ws(torch, ws)
+    _on_device((("X", X), ("w.vals", w.vals), ("w.meta", w.meta), ("Y", Y), ("Yh", Yh), ("Yq", Yq),
+                ("scale", scale), ("qscale", qscale), ("ws", ws)))
     mode = _out_mode(Y, Yh, Yq)
     p = plan if plan is not None else spmm_plan(w.desc, m, mode or NM_OUT_I32)
     need = workspace_size(p, m, w.desc.n)
@@ -350,8 +405,17 @@ def spmm(X, w: DeviceWeight, Y=None, scale=None, Yh=None, plan: Optional[NmPlan]
 def gemm_i8_dense(X, W, Y=None, scale=None, Yh=None, plan: Optional[NmPlan] = None, ws=None, stream=None,
                   Yq=None, qscale=None):
     """Dense baseline GEMM (nm_gemm_i8_dense_ex, or nm_gemm_i8_dense_out when Yq is given)."""
+    torch = _torch()
+    if X.dim() != 2 or W.dim() != 2:
+        raise ValueError("X and W must be 2-D ([m x k] and [n x k])")
     m, k = X.shape
     n = W.shape[0]
+    _need(X, "X", (torch.int8,), (m, k))
+    _need(W, "W", (torch.int8,), (n, k))
+    _check_outputs(torch, m, n, Y, scale, Yh, Yq, qscale)
+    _check_ws(torch, ws)
+    _on_device((("X", X), ("W", W), ("Y", Y), ("Yh", Yh), ("Yq", Yq), ("scale", scale), ("qscale", qscale),
+                ("ws", ws)))
     mode = _out_mode(Y, Yh, Yq)
     p = plan if plan is not None else dense_plan(m, n, k, mode or NM_OUT_I32)
     need = workspace_size(p, m, n)
@@ -375,8 +439,11 @@ def gemm_i8_dense(X, W, Y=None, scale=None, Yh=None, plan: Optional[NmPlan] = No
 def quantize_f16(x, inv_scale: float, xq=None, stream=None):
     """nm_quantize_f16: int8 codes of a float16 (or int16-bits) device tensor."""
     torch = _torch()
+    _need(x, "x", (torch.float16, torch.int16))
     if xq is None:
         xq = torch.empty(x.shape, dtype=torch.int8, device=x.device)
+    _need(xq, "xq", (torch.int8,), tuple(x.shape))
+    _on_device((("x", x), ("xq", xq)))
     _check(lib().nm_quantize_f16(_ptr(x), x.numel(), float(inv_scale), _ptr(xq), _stream(stream)),
            "nm_quantize_f16")
     return xq
@@ -416,5 +483,7 @@ def probe_mfma_layout(kind: int, a, b, pos, d, stream=None):
 
 
 def workspace_init(ws, stream=None):
+    _check_ws(_torch(), ws)
+    _on_device((("ws", ws),))
     _check(lib().nm_workspace_init(_ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
            "nm_workspace_init")
