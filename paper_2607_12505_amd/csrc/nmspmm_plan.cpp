@@ -92,6 +92,7 @@ nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *p) {
 // Tile indices used by the rules below (see kTiles).
 constexpr int kT64x64 = 6, kT32x32ks = 10;
 constexpr int kT128x128r2 = 16, kT128x64r2 = 17, kT64x128r2 = 18, kT64x64r2 = 19, kT256x256w8 = 20;
+constexpr int kT128x32r2 = 22;
 
 static int64_t tiles_of(int t, int m, int n) {
     return ceil_div(n, kTiles[t].tile_n()) * ceil_div(m, kTiles[t].tile_m());
@@ -118,23 +119,27 @@ nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *
         tile = (k_steps >= 2 && tiles_of(kT32x32ks, mm, n) <= 2 * cus) ? kT32x32ks : kT64x64;
     } else if (k_steps <= 2) {
         // Very short reductions: the output stream dominates; small tiles
-        // give the most workgroups in flight.
-        tile = kT64x64r2;
-    } else if (k_steps == 3 && (heavy || n >= 768)) {
-        // Three k-steps: 64 x 64 tiles; for one-stream weights (with wide
-        // outputs) the 4-slot ring, which loads the whole reduction at once.
-        tile = heavy ? kT64x64r2 : kT64x64;
+        // give the most workgroups in flight.  With one k-step and one-stream
+        // weights, 128 channels x 32 tokens: the same number of workgroups
+        // as 64 x 64, with output rows twice as long.
+        tile = (!heavy && k_steps == 1 && n >= 384) ? kT128x32r2 : kT64x64r2;
+    } else if (k_steps == 3) {
+        // Three k-steps (DeiT-S, k = 384): 128 x 32 for one-stream weights,
+        // 64 x 64 for the heavier operands.
+        tile = heavy ? kT64x64r2 : kT128x32r2;
     } else if (tiles_of(kT128x128r2, mm, n) < 4 * cus) {
         // Medium: with long reductions (8 k-steps or more) the operand fill
         // per output decides, so 128 x 128 as long as every compute unit
         // still gets a tile; otherwise half-height tiles (narrower for the
-        // heavier operands), or 64 x 64 when those would leave compute units
-        // without a tile.
+        // heavier operands).
         if (k_steps >= 8 && tiles_of(kT128x128r2, mm, n) >= cus) {
             tile = kT128x128r2;
         } else {
             tile = heavy ? kT64x128r2 : kT128x64r2;
-            if (tiles_of(tile, mm, n) < cus) tile = kT64x64r2;
+            // 64 x 64 when those would leave compute units without a tile,
+            // and for one-stream weights when they already give 4 or more
+            // workgroups per compute unit
+            if (tiles_of(tile, mm, n) < cus || (!heavy && tiles_of(tile, mm, n) >= 4 * cus)) tile = kT64x64r2;
         }
     } else {
         // Large outputs: 128 x 128; for the heavier operands on the widest

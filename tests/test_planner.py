@@ -81,18 +81,24 @@ def test_large_shapes_use_large_tiles():
     d = nmspmm.compress_size(768, 3072, 2, 4)
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # fc2 at batch 128
     assert (p.tile_n, p.tile_m) == (128, 128)
-    # three k-steps (DeiT-Small, k = 384): 64 x 64, the whole reduction in a
-    # 4-slot ring for one-stream weights with wide outputs
+    # three k-steps (DeiT-Small, k = 384): 128 channels x 32 tokens for
+    # one-stream weights, 64 x 64 for two streams
     d = nmspmm.compress_size(1152, 384, 2, 4)
-    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 12608, 1)) == "k_gemm<1, 2, 2, 2, 2, 4>"
+    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 12608, 1)) == "k_gemm<1, 2, 2, 4, 1, 2>"
     d = nmspmm.compress_size(1152, 384, 4, 8)
     assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 12608, 1)) == "k_gemm<2, 2, 2, 2, 2, 2>"
     d = nmspmm.compress_size(384, 384, 2, 4)
-    assert (nmspmm.spmm_plan(d, 12608, 1).tile_n, nmspmm.spmm_plan(d, 12608, 1).tile_m) == (128, 64)
+    assert (nmspmm.spmm_plan(d, 12608, 1).tile_n, nmspmm.spmm_plan(d, 12608, 1).tile_m) == (128, 32)
     # medium token counts: half-height tiles, narrower for two-stream weights
-    # (Swin-B stage 3 qkv, k = 512)
+    # (DeiT-B qkv at batch 8, k = 768)
+    d = nmspmm.compress_size(2304, 768, 2, 4)
+    assert (nmspmm.spmm_plan(d, 1576, 1).tile_n, nmspmm.spmm_plan(d, 1576, 1).tile_m) == (128, 64)
+    d = nmspmm.compress_size(2304, 768, 4, 8)
+    assert (nmspmm.spmm_plan(d, 1576, 1).tile_n, nmspmm.spmm_plan(d, 1576, 1).tile_m) == (64, 128)
+    # ... but 64 x 64 for one-stream weights once half-height tiles give 4 or
+    # more workgroups per compute unit (Swin-B stage 3 qkv, k = 512: 1176)
     d = nmspmm.compress_size(1536, 512, 2, 4)
-    assert (nmspmm.spmm_plan(d, 6272, 1).tile_n, nmspmm.spmm_plan(d, 6272, 1).tile_m) == (128, 64)
+    assert (nmspmm.spmm_plan(d, 6272, 1).tile_n, nmspmm.spmm_plan(d, 6272, 1).tile_m) == (64, 64)
     d = nmspmm.compress_size(1536, 512, 4, 8)
     assert (nmspmm.spmm_plan(d, 6272, 1).tile_n, nmspmm.spmm_plan(d, 6272, 1).tile_m) == (64, 128)
     # ... but 128 x 128 for long reductions while every compute unit gets a
@@ -107,10 +113,14 @@ def test_large_shapes_use_large_tiles():
     d = nmspmm.compress_size(768, 3072, 2, 4)
     assert (nmspmm.spmm_plan(d, 1576, 1).tile_n, nmspmm.spmm_plan(d, 1576, 1).tile_m) == (64, 64)
     assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 1576, 1)) == "k_gemm<1, 2, 2, 2, 2, 2>"
-    # one or two k-steps: 64 x 64 tiles (Swin-B stage 1, k = 128; stage 2
-    # qkv, k = 256)
+    # one or two k-steps: 64 x 64 tiles (Swin-B stage 2 qkv, k = 256), and
+    # 128 x 32 for one k-step of one-stream weights at least 384 wide (Swin-B
+    # stage 1 qkv, k = 128; its proj, 128 wide, stays at 64 x 64)
     d = nmspmm.compress_size(384, 128, 2, 4)
+    assert (nmspmm.spmm_plan(d, 100352, 1).tile_n, nmspmm.spmm_plan(d, 100352, 1).tile_m) == (128, 32)
+    d = nmspmm.compress_size(128, 128, 2, 4)
     assert (nmspmm.spmm_plan(d, 100352, 1).tile_n, nmspmm.spmm_plan(d, 100352, 1).tile_m) == (64, 64)
+    assert nmspmm.dense_plan(100352, 384, 128, 1).tile_m == 64
     d = nmspmm.compress_size(768, 256, 2, 4)
     assert (nmspmm.spmm_plan(d, 25088, 1).tile_n, nmspmm.spmm_plan(d, 25088, 1).tile_m) == (64, 64)
 
