@@ -471,13 +471,15 @@ def predictor_experiment(torch, n_cal, n_test, report):
     names = {(8, 8): "dense"}
     pname = lambda p: names.get(p, f"{p[0]}:{p[1]}")
     family = {}
-    for shape, lin in zip(shapes[:4], ("qkv", "proj", "fc1", "fc2")):
-        m, k, n = shape
-        dense_us = table[(shape, (8, 8))]
-        family[lin] = {"m": m, "k": k, "n": n, "patterns": {
-            pname(p): {"us": round(table[(shape, p)], 2),
-                       "tops": round(2.0 * m * n * k / (table[(shape, p)] * 1e-6) / 1e12, 1),
-                       "speedup_vs_dense": round(dense_us / table[(shape, p)], 3)} for p in pats}}
+    for which, tab in (("hot", hot), ("cold", table)):
+        family[which] = {}
+        for shape, lin in zip(shapes[:4], ("qkv", "proj", "fc1", "fc2")):
+            m, k, n = shape
+            dense_us = tab[(shape, (8, 8))]
+            family[which][lin] = {"m": m, "k": k, "n": n, "patterns": {
+                pname(p): {"us": round(tab[(shape, p)], 2),
+                           "tops": round(2.0 * m * n * k / (tab[(shape, p)] * 1e-6) / 1e12, 1),
+                           "speedup_vs_dense": round(dense_us / tab[(shape, p)], 3)} for p in pats}}
     cal = lt.random_assignments(n_cal, L, lt.FAMILY_N8, seed=1)
     test = lt.random_assignments(n_test, L, lt.FAMILY_N8, seed=2)
     test += [[p] * L for p in lt.FAMILY_N8]            # the uniform configurations
@@ -590,14 +592,20 @@ def write_predictor_report(res, path):
            f"configurations): {c['lut']} LUT, gamma per {c['gamma']}; cross-validated mean error "
            f"{c['cv_mean_abs_pct']}%, on the test configurations {c['test']['mean_abs_pct']}% mean, "
            f"{c['test']['max_abs_pct']}% max, {c['test']['within_5pct']} within 5%.", "",
-           "N:8 family per linear from the cold LUT (mean us; dense-equivalent TOPS; speedup over the dense GEMM):",
-           "",
-           "| linear | m | k | n | " + " | ".join(next(iter(res["family"].values()))["patterns"]) + " |",
-           "|---|---:|---:|---:|" + "---:|" * len(next(iter(res["family"].values()))["patterns"])]
-    for lin, f in res["family"].items():
-        md.append(f"| {lin} | {f['m']} | {f['k']} | {f['n']} | " + " | ".join(
-            f"{v['us']} / {v['tops']} / {v['speedup_vs_dense']}x" for v in f["patterns"].values()) + " |")
-    md += ["", "Algorithm 1 on the calibrated predictor (30 generations, 8 offspring, overshoot 4, synthetic "
+           ]
+    for which, how in (("hot", "back-to-back repeats, as the linears of a chain run"),
+                       ("cold", "caches flushed before every run")):
+        fam = res["family"][which]
+        pnames = next(iter(fam.values()))["patterns"]
+        md += [f"N:8 family per linear from the {which} LUT ({how}; mean us; dense-equivalent TOPS; speedup over "
+               f"the dense GEMM):", "",
+               "| linear | m | k | n | " + " | ".join(pnames) + " |",
+               "|---|---:|---:|---:|" + "---:|" * len(pnames)]
+        for lin, f in fam.items():
+            md.append(f"| {lin} | {f['m']} | {f['k']} | {f['n']} | " + " | ".join(
+                f"{v['us']} / {v['tops']} / {v['speedup_vs_dense']}x" for v in f["patterns"].values()) + " |")
+        md.append("")
+    md += ["Algorithm 1 on the calibrated predictor (30 generations, 8 offspring, overshoot 4, synthetic "
            "accuracy stand-in), then the returned configuration measured:", "",
            "| target speedup | target us | predicted us | measured us | measured speedup | error % | layers per N (1..8) | search s |",
            "|---:|---:|---:|---:|---:|---:|---|---:|"]
