@@ -234,6 +234,39 @@ def time_each(preps, torch, reps=5):
     return out
 
 
+def store_only_time(preps, idx, torch, reps=10):
+    """Mean time per launch of the GEMMs `idx` with their reduction skipped
+    (nm_probe_store_only: the same plans, outputs and epilogue stores, no
+    loads or matrix work), timed like a launch group of the step; None if a
+    plan's layout has no such mode.  The real results are written back
+    afterwards."""
+    L = nmspmm.lib()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    calls = []
+    for i in idx:
+        p = preps[i]
+        o = nmspmm.NmOutputs(p.Y.data_ptr() if p.Y is not None else None,
+                             p.Yh.data_ptr() if p.Yh is not None else None,
+                             p.scale.data_ptr(), None, None)
+        calls.append((ctypes.byref(p.splan), p.g.m, p.g.n, o))
+    for plan, m, n, o in calls:
+        if L.nm_probe_store_only(plan, m, n, ctypes.byref(o), stream) != nmspmm.NM_OK:
+            return None
+    E = torch.cuda.Event
+    ev = [(E(enable_timing=True), E(enable_timing=True)) for _ in range(reps)]
+    for e0, e1 in ev:
+        torch.cuda._sleep(int(2.4e9 * 25e-6 * len(calls)))
+        e0.record()
+        for plan, m, n, o in calls:
+            L.nm_probe_store_only(plan, m, n, ctypes.byref(o), stream)
+        e1.record()
+    torch.cuda.synchronize()
+    for i in idx:  # the real results again, for the parity check that follows
+        preps[i].run_sparse()
+    torch.cuda.synchronize()
+    return float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev])) / len(calls)
+
+
 def time_keyed_in_steps(preps, key, torch, reps):
     """Untimed detail pass in the step's own cache state: `reps` whole steps in
     which the GEMMs are ordered by `key(prep)` (sparse calls of each key, then
@@ -1210,6 +1243,8 @@ def main():
     dom_name = max(gsum, key=lambda k: gsum[k]["time_ms"])
     dom = gsum[dom_name]
     avg_ms = dom["time_ms"] / dom["launches"]
+    dom_idx = next(idx for (side, name), idx in groups if side == "sparse" and name == dom_name)
+    store_ms = store_only_time(preps, dom_idx, torch)
     achieved = dom["bytes"] / dom["launches"] / (avg_ms * 1e-3) / 1e9
     traffic = None
     tpath = args.traffic or default_traffic_path(work.name)
@@ -1232,6 +1267,11 @@ def main():
         "avg_launch_us": round(avg_ms * 1e3, 2),
         "algorithmic_bytes_per_launch": int(dom["bytes"] / dom["launches"]),
     }
+    if store_ms is not None:
+        # the same launches with the reduction skipped: the ceiling this
+        # kernel's own output stream sets (context beside the HBM peak)
+        roofline["output_stream_only_us"] = round(store_ms * 1e3, 2)
+        roofline["frac_of_output_stream_only"] = round(store_ms / avg_ms, 3)
 
     # per GEMM, inside whole steps with an event after every GEMM (stderr table only)
     per_gemm = time_keyed_in_steps(preps, lambda p: preps.index(p), torch, 3)

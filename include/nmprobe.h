@@ -61,6 +61,22 @@ nm_status nm_wall_clock_khz(int32_t *khz);
 nm_status nm_probe_mfma_layout(int kind, const int32_t *a, const int32_t *b, const int32_t *pos, int32_t *d,
                                void *stream);
 
+/* The output stream of a GEMM plan alone: launches the plan's kernel for an
+ * [m x n] output with the reduction skipped (no operand loads, no matrix
+ * instructions), so every output element is written with the value of an
+ * empty sum (int32 0; fp16 and int8 of 0 times the scale, 0 for finite
+ * scales) through the same epilogue, store pattern and cache policy as
+ * nm_spmm_out.  Timing it beside the real call
+ * gives the ceiling the GEMM's own stores set.  plan: a plan of an
+ * output-split tile layout (the layouts nm_tile_info reports for k_gemm) with
+ * split_k == 1, for the plan's kind; out: as for nm_spmm_out (device buffers,
+ * caller owned; scales are read).  Asynchronous on `stream`.
+ * Errors: NM_ERR_ARG for a NULL plan/out, no output, a missing scale,
+ * misaligned pointers, another tile layout or split_k != 1; NM_ERR_SHAPE for
+ * m < 0, n < 4, n % 4 != 0 or m * n >= 2^29; NM_ERR_HIP if the launch fails.
+ * m == 0 writes nothing. */
+nm_status nm_probe_store_only(const nm_plan *plan, int m, int n, const nm_outputs *out, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

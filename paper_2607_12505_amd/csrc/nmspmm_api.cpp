@@ -204,6 +204,52 @@ extern "C" nm_status nm_gemm_i8_dense(const int8_t *X, int m, const int8_t *W, i
     return nm_gemm_i8_dense_ex(X, m, W, n, k, Y, scale, Yh, ws, ws_bytes, stream, nullptr);
 }
 
+extern "C" nm_status nm_probe_store_only(const nm_plan *plan, int m, int n, const nm_outputs *out, void *stream) {
+    if (!plan || !out) return NM_ERR_ARG;
+    if (m < 0 || n < 4 || n % 4 != 0) return NM_ERR_SHAPE;
+    if (m == 0) return NM_OK;
+    if ((int64_t)m * n >= ((int64_t)1 << 29)) return NM_ERR_SHAPE;
+    const nm_outputs o = *out;
+    if (!o.y && !o.yh && !o.yq) return NM_ERR_ARG;
+    if ((o.yh && !o.scale) || (o.yq && !o.qscale)) return NM_ERR_ARG;
+    if ((o.y && !aligned16(o.y)) || (o.yh && !aligned16(o.yh)) || (o.yh && !aligned16(o.scale)) ||
+        (o.yq && !aligned16(o.yq)) || (o.yq && !aligned16(o.qscale)))
+        return NM_ERR_ARG;
+    if (plan->tile < 0 || plan->tile >= kNumTiles || kTiles[plan->tile].layout != kOutSplit || plan->split_k != 1)
+        return NM_ERR_ARG;
+    if (plan->kind != NM_KIND_SP42 && plan->kind != NM_KIND_SP42X2 && plan->kind != NM_KIND_DENSE) return NM_ERR_ARG;
+    nm_plan p = *plan;
+    nm_status st = complete_plan(p.kind, m, n, 1, &p);
+    if (st != NM_OK) return st;
+    // Zero k-steps: the kernel issues no operand loads and no matrix
+    // instructions; the epilogue stores the zero accumulators.  The epilogue
+    // reads its multipliers unconditionally, from X when one is absent, so X
+    // must still be a readable device address of at least 16 aligned bytes:
+    // a scale vector (n >= 4 floats) or, when there is none, the int32 output
+    // (m * n >= 4 words).
+    const void *readable = o.scale ? (const void *)o.scale : o.qscale ? (const void *)o.qscale : (const void *)o.y;
+    GemmArgs a;
+    a.X = (const int8_t *)readable;
+    a.A = nullptr;
+    a.meta = nullptr;
+    a.Y = o.y;
+    a.Yh = o.yh;
+    a.scale = o.scale;
+    a.Yq = o.yq;
+    a.qscale = o.qscale;
+    a.counters = nullptr;
+    a.partials = nullptr;
+    a.m = m;
+    a.n = n;
+    a.k = 128;
+    a.k_steps = 0;
+    a.n_frags = (n + kFragRows - 1) / kFragRows;
+    a.tiles_n = (n + p.tile_n - 1) / p.tile_n;
+    a.tiles_m = (m + p.tile_m - 1) / p.tile_m;
+    a.split_k = 1;
+    return launch_gemm(p.kind, p.tile, a, p.grid, stream) == 0 ? NM_OK : NM_ERR_HIP;
+}
+
 extern "C" nm_status nm_quantize_f16(const uint16_t *x, int64_t count, float inv_scale, int8_t *xq, void *stream) {
     if (count < 0) return NM_ERR_SHAPE;
     if (count == 0) return NM_OK;

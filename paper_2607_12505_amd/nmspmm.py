@@ -30,7 +30,7 @@ EXPORTED = (
     "nm_status_string", "nm_compress_size", "nm_compress", "nm_decompress", "nm_num_tiles",
     "nm_tile_info", "nm_plan_kernel_name", "nm_spmm_plan", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
     "nm_spmm", "nm_spmm_ex", "nm_gemm_i8_dense", "nm_gemm_i8_dense_ex", "nm_spmm_out", "nm_gemm_i8_dense_out",
-    "nm_quantize_f16", "nm_probe_mfma_rate", "nm_probe_mfma_layout", "nm_wall_clock_khz",
+    "nm_quantize_f16", "nm_probe_mfma_rate", "nm_probe_mfma_layout", "nm_wall_clock_khz", "nm_probe_store_only",
 )
 NM_PROBE_WORDS = 4096
 
@@ -100,6 +100,7 @@ def lib() -> ctypes.CDLL:
             "nm_probe_mfma_rate": ([i32, vp, i32, i32, vp, vp, vp], i32),
             "nm_wall_clock_khz": ([ctypes.POINTER(ctypes.c_int32)], i32),
             "nm_probe_mfma_layout": ([i32, vp, vp, vp, vp, vp], i32),
+            "nm_probe_store_only": ([pp, i32, i32, ctypes.POINTER(NmOutputs), vp], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -480,6 +481,17 @@ def probe_mfma_layout(kind: int, a, b, pos, d, stream=None):
         raise ValueError("operand buffers smaller than the instruction needs")
     _check(lib().nm_probe_mfma_layout(int(kind), _ptr(a), _ptr(b), _ptr(pos), _ptr(d), _stream(stream)),
            "nm_probe_mfma_layout")
+
+
+def probe_store_only(plan: NmPlan, m: int, n: int, Y=None, scale=None, Yh=None, Yq=None, qscale=None, stream=None):
+    """nm_probe_store_only: the plan's kernel with the reduction skipped, so
+    only its epilogue stores run (nmprobe.h); the outputs receive zeros."""
+    torch = _torch()
+    _check_outputs(torch, m, n, Y, scale, Yh, Yq, qscale)
+    _on_device((("Y", Y), ("Yh", Yh), ("Yq", Yq), ("scale", scale), ("qscale", qscale)))
+    o = _outputs(Y, scale, Yh, Yq, qscale)
+    _check(lib().nm_probe_store_only(ctypes.byref(plan), int(m), int(n), ctypes.byref(o), _stream(stream)),
+           "nm_probe_store_only")
 
 
 def workspace_init(ws, stream=None):

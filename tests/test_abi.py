@@ -76,6 +76,21 @@ def test_host_side_argument_checks_need_no_gpu():
     assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, nul, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
     assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, fake, fake, nul, fake, nul) == nmspmm.NM_ERR_ARG
     assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42X2, fake, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
+    ok_plan = nmspmm.make_plan(nmspmm.NM_KIND_SP42, 16, 1)
+    y_only = nmspmm.NmOutputs(fake.value, None, None, None, None)
+    assert L.nm_probe_store_only(None, 64, 64, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_probe_store_only(ctypes.byref(ok_plan), 64, 66, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_SHAPE
+    assert L.nm_probe_store_only(ctypes.byref(ok_plan), -1, 64, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_SHAPE
+    assert L.nm_probe_store_only(ctypes.byref(ok_plan), 0, 64, ctypes.byref(y_only), nul) == nmspmm.NM_OK
+    no_out = nmspmm.NmOutputs(None, None, None, None, None)
+    assert L.nm_probe_store_only(ctypes.byref(ok_plan), 64, 64, ctypes.byref(no_out), nul) == nmspmm.NM_ERR_ARG
+    fp16_no_scale = nmspmm.NmOutputs(None, fake.value, None, None, None)
+    assert L.nm_probe_store_only(ctypes.byref(ok_plan), 64, 64, ctypes.byref(fp16_no_scale), nul) == nmspmm.NM_ERR_ARG
+    for bad in (nmspmm.make_plan(nmspmm.NM_KIND_SP42, 10, 1),      # k-sliced layout
+                nmspmm.make_plan(nmspmm.NM_KIND_SP42, 11, 1),      # row-stationary layout
+                nmspmm.make_plan(nmspmm.NM_KIND_SP42, 16, 2),      # split_k != 1
+                nmspmm.make_plan(7, 16, 1)):                        # unknown kind
+        assert L.nm_probe_store_only(ctypes.byref(bad), 64, 64, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_ARG
 
 
 def _gpu_visible():
@@ -105,3 +120,6 @@ def test_launch_failures_report_nm_err_hip():
     khz = ctypes.c_int32(0)
     assert L.nm_wall_clock_khz(ctypes.byref(khz)) == nmspmm.NM_ERR_HIP
     assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_DENSE, fake, fake, nul, fake, nul) == nmspmm.NM_ERR_HIP
+    y_only = nmspmm.NmOutputs(fake.value, None, None, None, None)
+    assert L.nm_probe_store_only(ctypes.byref(nmspmm.make_plan(nmspmm.NM_KIND_SP42, 16, 1)), 64, 64,
+                                 ctypes.byref(y_only), nul) == nmspmm.NM_ERR_HIP

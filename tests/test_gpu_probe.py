@@ -51,3 +51,29 @@ def test_bench_reports_positive_rates():
     for key in ("smfmac_i32_16x16x128_i8_random", "mfma_i32_16x16x64_i8_random",
                 "smfmac_i32_16x16x128_i8_zero", "mfma_i32_16x16x64_i8_zero"):
         assert res[key + "_pops"] > 0 and res[key + "_clock_mhz"] > 0
+
+
+@pytest.mark.parametrize("m,n", [(1000, 260), (12608, 1152), (33, 4)])
+def test_store_only_probe_writes_zeros_exactly_in_the_outputs(m, n):
+    # every output-split tile of all three kinds, on ragged shapes: the probe
+    # writes the empty-sum values into [m x n] and nothing past it
+    import torch
+    bigY = torch.full((m * n + 4096,), 7, dtype=torch.int32, device="cuda")
+    bigH = torch.full((m * n + 4096,), 7, dtype=torch.int16, device="cuda")
+    bigQ = torch.full((m * n + 4096,), 7, dtype=torch.int8, device="cuda")
+    scale = torch.full((n,), 0.5, dtype=torch.float32, device="cuda")
+    Y, Yh, Yq = bigY[:m * n].view(m, n), bigH[:m * n].view(m, n), bigQ[:m * n].view(m, n)
+    for kind in (nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_SP42X2, nmspmm.NM_KIND_DENSE):
+        for tile in range(nmspmm.num_tiles()):
+            plan = nmspmm.make_plan(kind, tile, 1)
+            try:
+                nmspmm.probe_store_only(plan, m, n, Y=Y, scale=scale, Yh=Yh, Yq=Yq, qscale=scale)
+            except nmspmm.NmError as e:
+                assert e.status == nmspmm.NM_ERR_ARG     # not an output-split layout
+                continue
+            torch.cuda.synchronize()
+            assert not Y.any() and not Yh.any() and not Yq.any(), (kind, tile)
+            assert (bigY[m * n:] == 7).all() and (bigH[m * n:] == 7).all() and (bigQ[m * n:] == 7).all()
+            Y.fill_(7)
+            Yh.fill_(7)
+            Yq.fill_(7)
