@@ -1117,6 +1117,9 @@ def main():
                     help="skip the DeiT-Base per-batch speedups reported beside the main line")
     ap.add_argument("--no-mfma-ceiling", action="store_true",
                     help="skip the measured matrix-instruction rate reported beside the main line")
+    ap.add_argument("--no-store-only", action="store_true",
+                    help="skip the output-stream-only launches of the dominant kernel (keeps profiler traces to the "
+                         "real launches)")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the HIP-graph replay of the step reported beside the main line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -1244,7 +1247,7 @@ def main():
     dom = gsum[dom_name]
     avg_ms = dom["time_ms"] / dom["launches"]
     dom_idx = next(idx for (side, name), idx in groups if side == "sparse" and name == dom_name)
-    store_ms = store_only_time(preps, dom_idx, torch)
+    store_ms = None if args.no_store_only else store_only_time(preps, dom_idx, torch)
     achieved = dom["bytes"] / dom["launches"] / (avg_ms * 1e-3) / 1e9
     traffic = None
     tpath = args.traffic or default_traffic_path(work.name)
