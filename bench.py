@@ -370,13 +370,29 @@ def sweep_summary(rows):
         return None
     norm = np.array([r["t_best_us"] / r["t_planned_us"] for r in rows])
     fixed = np.array([r["t_fixed_split1_us"] / r["t_planned_us"] for r in rows if r["t_fixed_split1_us"]])
+    fixed_tile = np.array([r["times"]["16/1"] / r["t_planned_us"] for r in rows if r["times"].get("16/1")])
     return {
         "cases": len(rows),
         "top1_hit_rate": round(float(np.mean([r["planned"] == r["best"] for r in rows])), 3),
         "avg_norm_perf": round(float(norm.mean()), 3),
         "worst_norm_perf": round(float(norm.min()), 3),
         "gain_over_fixed_split1": round(float(fixed.mean()), 3) if len(fixed) else None,
+        # against one fixed plan for every shape (128 x 128, no split)
+        "gain_over_fixed_128x128": round(float(fixed_tile.mean()), 3) if len(fixed_tile) else None,
     }
+
+
+GRID_PATTERNS = (((2, 4), 50), ((4, 8), 50), ((1, 4), 75), ((2, 8), 75), ((1, 8), 87.5))
+
+
+def paper_grid_workload():
+    """The paper's kernel benchmark grid (Sec. 6.1) as a sweep workload: m in
+    {64, 128, 256, 512}, n and k in {128, 256, 512, 1024}, the five patterns of
+    50 / 75 / 87.5 % sparsity, int32 output."""
+    sizes = (128, 256, 512, 1024)
+    gemms = tuple(wl.Gemm(f"m{m} n{n} k{k} {N}:{M}", m, k, n, N, M)
+                  for m in (64, 128, 256, 512) for n in sizes for k in sizes for (N, M), _ in GRID_PATTERNS)
+    return wl.Workload(-1, "paper_kernel_grid", gemms)
 
 
 def sweep(configs, torch, reps, out_path):
@@ -389,7 +405,7 @@ def sweep(configs, torch, reps, out_path):
     rows = []
     seen = set()
     for cfg in configs:
-        work = wl.workload(cfg)
+        work = paper_grid_workload() if cfg == "grid" else wl.workload(cfg)
         out = (nmspmm.NM_OUT_I32 if work.out_int32 else 0) | (nmspmm.NM_OUT_F16 if work.out_f16 else 0)
         cases = []
         for g in work.gemms:
@@ -404,7 +420,12 @@ def sweep(configs, torch, reps, out_path):
             if key in seen:
                 continue
             seen.add(key)
-            X, W, scale = wl.inputs_for(cfg, g)
+            if cfg == "grid":
+                rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([6, g.m, g.n, g.k, g.N, g.M])))
+                X = wl.gen_x(g.m, g.k, rng)
+                W, scale = wl.gen_w(g.n, g.k, g.N, g.M, rng)
+            else:
+                X, W, scale = wl.inputs_for(cfg, g)
             Xd = torch.from_numpy(X).cuda()
             sd = torch.from_numpy(scale).cuda()
             sparse = g.N < g.M
@@ -472,12 +493,20 @@ def sweep(configs, torch, reps, out_path):
             log(f"cfg{cfg} {g.name:<20} m={g.m:<6} k={g.k:<5} n={g.n:<5} planned t{chosen[0]}/s{chosen[1]} "
                 f"{t_plan:7.1f} us  best t{best[0]}/s{best[1]} {times[best]:7.1f} us  "
                 f"norm {times[best] / t_plan:.3f}")
-    summary = sweep_summary([r for r in rows if r["pattern"] != "dense"])
-    dense_summary = sweep_summary([r for r in rows if r["pattern"] == "dense"])
-    log(json.dumps({"sparse": summary, "dense": dense_summary}))
+    summary = sweep_summary([r for r in rows if r["pattern"] != "dense" and r["cfg"] != "grid"])
+    dense_summary = sweep_summary([r for r in rows if r["pattern"] == "dense" and r["cfg"] != "grid"])
+    # the paper's Table 1 rows: the kernel grid per sparsity (and its dense baseline)
+    spars = {f"{N}:{M}": sp for (N, M), sp in GRID_PATTERNS}
+    grid_summary = None
+    if "grid" in configs:
+        grid_summary = {str(sp): sweep_summary([r for r in rows if r["cfg"] == "grid" and
+                                                spars.get(r["pattern"]) == sp]) for sp in (50, 75, 87.5)}
+        grid_summary["dense"] = sweep_summary([r for r in rows if r["cfg"] == "grid" and r["pattern"] == "dense"])
+    log(json.dumps({"sparse": summary, "dense": dense_summary, "grid": grid_summary}))
     if out_path:
         with open(out_path, "w") as f:
-            json.dump({"summary": summary, "dense_summary": dense_summary, "rows": rows}, f, indent=1)
+            json.dump({"summary": summary, "dense_summary": dense_summary, "grid_summary": grid_summary,
+                       "rows": rows}, f, indent=1)
     return summary
 
 
@@ -928,6 +957,18 @@ def write_sweep_report(sweep_json, path):
           f"Summary, sparse GEMMs: {s['cases']} distinct (shape, N:M) cases; planner Top-1 hit rate "
           f"{s['top1_hit_rate']}, average normalised performance {s['avg_norm_perf']}, worst {s['worst_norm_perf']}; "
           f"gain over a fixed split_k = 1 with the same tile {s['gain_over_fixed_split1']}.", ""]
+    gs = d.get("grid_summary")
+    if gs:
+        md += ["The paper's kernel grid (Sec. 6.1: m in {64, 128, 256, 512}, n and k in {128, 256, 512, 1024}; int32 "
+               "output), per sparsity as in Table 1:", "",
+               "| sparsity | cases | Top-1 hit rate | average normalised | worst normalised | gain over a fixed "
+               "128x128 plan |", "|---|---:|---:|---:|---:|---:|"]
+        for key, v in gs.items():
+            if v:
+                label = "dense baseline" if key == "dense" else f"{key} %"
+                md.append(f"| {label} | {v['cases']} | {v['top1_hit_rate']} | {v['avg_norm_perf']} | "
+                          f"{v['worst_norm_perf']} | {v.get('gain_over_fixed_128x128')} |")
+        md.append("")
     ds = d.get("dense_summary")
     if ds:
         md += [f"Dense INT8 baseline (every sparse shape's dense counterpart and the dense layers of the chain): "
@@ -1125,7 +1166,8 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after timing, run one plain device copy of MIB MiB (profiler counter calibration)")
     ap.add_argument("--sweep", type=str, default=None,
-                    help="planner evaluation over the given comma-separated configs (e.g. 0,1,2,3,4)")
+                    help="planner evaluation over the given comma-separated configs (e.g. 0,1,2,3,4); 'grid' adds "
+                         "the paper's kernel grid")
     ap.add_argument("--sweep-out", type=str, default=None, help="JSON file for the sweep results")
     ap.add_argument("--sweep-report", type=str, default=None, metavar="SWEEP_JSON",
                     help="markdown report (--report) of a sweep JSON (no GPU needed)")
@@ -1175,7 +1217,7 @@ def main():
     nmspmm.lib()
     torch.cuda.set_device(0)
     if args.sweep:
-        summary = sweep([int(c) for c in args.sweep.split(",")], torch, 10, args.sweep_out)
+        summary = sweep([c if c == "grid" else int(c) for c in args.sweep.split(",")], torch, 10, args.sweep_out)
         print(json.dumps({"planner_evaluation": summary}), flush=True)
         return
     if args.chaining:

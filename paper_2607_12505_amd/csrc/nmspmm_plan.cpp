@@ -90,7 +90,7 @@ nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *p) {
 }
 
 // Tile indices used by the rules below (see kTiles).
-constexpr int kT64x64 = 6, kT32x32ks = 10;
+constexpr int kT32x64ks = 8, kT64x32ks = 9, kT32x32ks = 10;
 constexpr int kT128x128r2 = 16, kT128x64r2 = 17, kT64x128r2 = 18, kT64x64r2 = 19, kT256x256w8 = 20;
 constexpr int kT128x32r2 = 22;
 
@@ -113,10 +113,21 @@ nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *
     int tile;
     if (mm <= 512) {
         // Few tokens: too few output tiles to occupy the GPU.  Split the
-        // reduction over the waves of each workgroup (k-sliced tile, merged in
-        // LDS) when k has at least two k-steps and the 32 x 32 tiles do not
-        // oversubscribe.
-        tile = (k_steps >= 2 && tiles_of(kT32x32ks, mm, n) <= 2 * cus) ? kT32x32ks : kT64x64;
+        // reduction over the waves of each workgroup (k-sliced 32 x 32 tile,
+        // merged in LDS) while those tiles give at most 2 workgroups per CU.
+        // For the heavier operands past one workgroup per CU, twice the tokens
+        // per tile halve the weight fill (64 tokens, unless that pads m by more
+        // than 15 %: then 64 channels); with a single k-step, 64 x 64.
+        // Otherwise 64 x 64 with a 2-slot ring.
+        const int64_t t32 = tiles_of(kT32x32ks, mm, n);
+        if (t32 > 2 * cus)
+            tile = kT64x64r2;
+        else if (!heavy || t32 <= cus)
+            tile = kT32x32ks;
+        else if (k_steps == 1)
+            tile = kT64x64r2;
+        else
+            tile = ceil_div(mm, 64) * 64 * 100 <= (int64_t)mm * 115 ? kT32x64ks : kT64x32ks;
     } else if (k_steps <= 2) {
         // Very short reductions: the output stream dominates; small tiles
         // give the most workgroups in flight.  With one k-step and one-stream

@@ -60,7 +60,19 @@ def test_small_token_counts_split_the_reduction_inside_workgroups():
     # but not when 32 x 32 tiles would oversubscribe (DeiT-Base fc1 at batch 1)
     d = nmspmm.compress_size(3072, 768, 2, 4)
     p = nmspmm.spmm_plan(d, 197, nmspmm.NM_OUT_I32)
-    assert (p.tile_n, p.tile_m) == (64, 64)
+    assert (p.tile_n, p.tile_m) == (64, 64) and nmspmm.plan_kernel_name(p) == "k_gemm<1, 2, 2, 2, 2, 2>"
+    # a single k-step splits too (the paper's grid at k = 128)
+    d = nmspmm.compress_size(1024, 128, 2, 4)
+    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 256, 1)) == "k_gemm_ks<1, 2, 2, 3>"
+    # heavier operands past one 32 x 32 tile per CU: 64 tokens per tile ...
+    p = nmspmm.dense_plan(512, 1024, 512, nmspmm.NM_OUT_I32)
+    assert (p.tile_n, p.tile_m) == (32, 64) and "k_gemm_ks" in nmspmm.plan_kernel_name(p)
+    # ... or 64 channels when 64-token tiles would pad m by more than 15 % (197 -> 256)
+    p = nmspmm.dense_plan(197, 2304, 768, nmspmm.NM_OUT_I32)
+    assert (p.tile_n, p.tile_m) == (64, 32) and "k_gemm_ks" in nmspmm.plan_kernel_name(p)
+    # ... and 64 x 64 with a single k-step
+    p = nmspmm.dense_plan(512, 1024, 128, nmspmm.NM_OUT_I32)
+    assert (p.tile_n, p.tile_m) == (64, 64) and "k_gemm<" in nmspmm.plan_kernel_name(p)
 
 
 def test_large_shapes_use_large_tiles():
