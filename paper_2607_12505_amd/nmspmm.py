@@ -75,6 +75,14 @@ def lib() -> ctypes.CDLL:
             return _lib
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_12505_amd/build.py")
+        # PyTorch ships its own HIP runtime under the same soname as the
+        # system one the library links.  Loaded first, it is the one the
+        # library binds to, so a process has a single HIP runtime; loaded
+        # after the library, a second runtime would start and find no device.
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = ctypes.CDLL(LIB_PATH)
         vp, i32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
         pd, pp = ctypes.POINTER(NmDesc), ctypes.POINTER(NmPlan)

@@ -25,9 +25,18 @@ def test_header_declares_the_binding_names():
 
 
 def test_library_exports_every_declared_symbol():
-    lib = ctypes.CDLL(nmspmm.LIB_PATH)
+    lib = nmspmm.lib()
     for name in declared_functions():
         assert hasattr(lib, name), name
+
+
+def test_one_hip_runtime_per_process():
+    # the binding loads PyTorch's HIP runtime first, so the library binds to
+    # it instead of starting a second one (which would find no device)
+    nmspmm.lib()
+    maps = open("/proc/self/maps").read().splitlines()
+    runtimes = {line.split()[-1] for line in maps if "libamdhip64" in line}
+    assert len(runtimes) == 1, runtimes
 
 
 def test_status_strings():

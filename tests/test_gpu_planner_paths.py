@@ -1,0 +1,62 @@
+"""GPU parity along every branch of the adaptive-parallelism planner (Sec.
+4.3): one seeded shape per rule, for one-stream (2:4), two-stream (4:8) and
+dense weights, compared element by element with the oracle in the launch
+configuration the planner picks (int32 and fp16 outputs, guard bands after
+both).  The expected tile of each case documents the rule it exercises."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_12505_amd import nmspmm
+import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+KS = "k_gemm_ks"
+# (m, n, k, kind, expected (tile_n, tile_m), k-sliced?)
+CASES = [
+    (100, 256, 256, "sp", (32, 32), True),      # few tokens: k-sliced 32 x 32
+    (100, 256, 128, "sp", (32, 32), True),      # ... also with a single k-step
+    (512, 1024, 256, "dn", (32, 64), True),     # heavier operands past one tile per CU: 64 tokens
+    (512, 1024, 256, "x2", (32, 64), True),
+    (197, 2304, 256, "dn", (64, 32), True),     # ... or 64 channels when 64 tokens pad m too much
+    (512, 1024, 128, "dn", (64, 64), False),    # ... and 64 x 64 with a single k-step
+    (400, 4096, 128, "sp", (64, 64), False),    # more than 2 k-sliced tiles per CU: 64 x 64
+    (3000, 512, 128, "sp", (128, 32), False),   # one k-step, one stream, >= 384 wide: 128 x 32
+    (3000, 256, 128, "sp", (64, 64), False),    # ... narrower: 64 x 64
+    (3000, 512, 256, "sp", (64, 64), False),    # two k-steps: 64 x 64
+    (2000, 768, 384, "sp", (128, 32), False),   # three k-steps, one stream: 128 x 32
+    (2000, 768, 384, "x2", (64, 64), False),    # ... heavier operands: 64 x 64
+    (4000, 1024, 1024, "sp", (128, 128), False),  # medium, long reduction: 128 x 128
+    (1600, 2304, 768, "sp", (128, 64), False),  # medium: half-height tiles
+    (1600, 2304, 768, "dn", (64, 128), False),  # ... narrower for the heavier operands
+    (6272, 1536, 512, "sp", (64, 64), False),   # ... 64 x 64 past 4 half-height tiles per CU
+    (8192, 2048, 512, "sp", (128, 128), False),  # large: 128 x 128
+    (4096, 4096, 512, "x2", (256, 256), False),  # large, heavier operands, 4096 wide: 256 x 256 on 8 waves
+]
+
+
+@pytest.mark.parametrize("m,n,k,kind,tile,ks", CASES)
+def test_planner_branch_matches_oracle(m, n, k, kind, tile, ks):
+    print(f"planner branch m={m} n={n} k={k} {kind}", flush=True)
+    rng = np.random.default_rng(m * 31 + n * 7 + k)
+    X = rng.integers(-128, 128, (m, k)).astype(np.int8)
+    scale = rng.uniform(1e-6, 1e-3, n).astype(np.float32)
+    if kind == "dn":
+        W = rng.integers(-128, 128, (n, k)).astype(np.int8)
+        plan = nmspmm.dense_plan(m, n, k, nmspmm.NM_OUT_I32 | nmspmm.NM_OUT_F16)
+    else:
+        from paper_2607_12505_amd import workloads as wl
+        N, M = (2, 4) if kind == "sp" else (4, 8)
+        W = wl.random_nm(n, k, N, M, rng, full=True)
+        packed = nmspmm.compress(W, N, M)
+        plan = nmspmm.spmm_plan(packed.desc, m, nmspmm.NM_OUT_I32 | nmspmm.NM_OUT_F16)
+    name = nmspmm.plan_kernel_name(plan)
+    assert (plan.tile_n, plan.tile_m) == tile and (KS in name) == ks, name
+    if kind == "dn":
+        Y, Yh = gu.run_dense(X, W, scale, want_i32=True, want_f16=True)
+    else:
+        Y, Yh = gu.run_sparse(X, packed, scale, want_i32=True, want_f16=True)
+    ref = oracle.matmul_i8(X, W)
+    assert np.array_equal(Y, ref), name
+    gu.assert_f16_close(Yh, oracle.dequant_f16(ref, scale))
