@@ -64,6 +64,7 @@ constexpr TileCfg kTiles[] = {
     {2, 4, 8, 4, 3, kOutSplit},  // 20: 256 ch x 256 tok, 8 waves (2 x 4), 3-slot ring
     {2, 4, 8, 2, 2, kOutSplit},  // 21: 256 ch x 128 tok, 8 waves, 2-slot ring
     {2, 2, 4, 1, 2, kOutSplit},  // 22: 128 ch x  32 tok, 2-slot ring
+    {4, 2, 2, 4, 2, kOutSplit},  // 23: 128 ch x 128 tok, 8 waves (4 x 2), 2-slot ring
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 

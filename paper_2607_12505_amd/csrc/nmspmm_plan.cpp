@@ -92,7 +92,7 @@ nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *p) {
 // Tile indices used by the rules below (see kTiles).
 constexpr int kT32x64ks = 8, kT64x32ks = 9, kT32x32ks = 10;
 constexpr int kT128x128r2 = 16, kT128x64r2 = 17, kT64x128r2 = 18, kT64x64r2 = 19, kT256x256w8 = 20;
-constexpr int kT128x32r2 = 22;
+constexpr int kT128x32r2 = 22, kT128x128w8 = 23;
 
 static int64_t tiles_of(int t, int m, int n) {
     return ceil_div(n, kTiles[t].tile_n()) * ceil_div(m, kTiles[t].tile_m());
@@ -152,11 +152,17 @@ nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *
             // workgroups per compute unit
             if (tiles_of(tile, mm, n) < cus || (!heavy && tiles_of(tile, mm, n) >= 4 * cus)) tile = kT64x64r2;
         }
+    } else if (heavy) {
+        // Large outputs, heavier operands: 128 x 128 on 8 waves (4 along the
+        // channels x 2 along the tokens, twice the waves to overlap the
+        // operand reads with the stores), or on the widest outputs the
+        // 256 x 256 tile on 8 waves, which halves the operand fill per output.
+        tile = n >= 4096 ? kT256x256w8 : kT128x128w8;
     } else {
-        // Large outputs: 128 x 128; for the heavier operands on the widest
-        // outputs the 256 x 256 tile on 8 waves, which halves the operand
-        // fill per output.
-        tile = (heavy && n >= 4096) ? kT256x256w8 : kT128x128r2;
+        // Large outputs, one-stream weights: 128 x 128 on 8 waves, except for
+        // long reductions (24 k-steps or more) and the widest outputs, where
+        // the 4-wave 128 x 128 tile's larger per-wave fragment grid wins.
+        tile = (k_steps >= 24 || n >= 4096) ? kT128x128r2 : kT128x128w8;
     }
     plan->kind = kind;
     plan->tile = tile;

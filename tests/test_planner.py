@@ -78,10 +78,18 @@ def test_small_token_counts_split_the_reduction_inside_workgroups():
 def test_large_shapes_use_large_tiles():
     d = nmspmm.compress_size(3072, 768, 2, 4)
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # DeiT-Base fc1 at batch 128
-    assert nmspmm.plan_kernel_name(p) == "k_gemm<1, 2, 2, 4, 4, 2>"   # 128 x 128, 2-slot ring
+    assert nmspmm.plan_kernel_name(p) == "k_gemm<1, 4, 2, 2, 4, 2>"   # 128 x 128 on 8 waves, 2-slot ring
     d = nmspmm.compress_size(3072, 1024, 4, 8)
     p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)    # ViT-L qkv, two-stream weight
-    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 2, 2, 4, 4, 2>"
+    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 4, 2, 2, 4, 2>"
+    # one-stream weights on the widest outputs or with long reductions: the
+    # 4-wave 128 x 128 tile (ViT-L fc1, DeiT-B fc2 at batch 128)
+    d = nmspmm.compress_size(4096, 1024, 2, 4)
+    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 18464, 1)) == "k_gemm<1, 2, 2, 4, 4, 2>"
+    d = nmspmm.compress_size(768, 3072, 2, 4)
+    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 25216, 1)) == "k_gemm<1, 2, 2, 4, 4, 2>"
+    # the dense baseline of DeiT-B fc2 at batch 128: 8 waves
+    assert nmspmm.plan_kernel_name(nmspmm.dense_plan(25216, 768, 3072, 1)) == "k_gemm<3, 4, 2, 2, 4, 2>"
     # the widest outputs of the heavier operands: 256 x 256 on 8 waves (ViT-L fc1)
     d = nmspmm.compress_size(4096, 1024, 4, 8)
     p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)
