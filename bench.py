@@ -267,6 +267,25 @@ def store_only_time(preps, idx, torch, reps=10):
     return float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev])) / len(calls)
 
 
+def chain_times(preps, torch, reps, sleep_cycles):
+    """A chain workload in network order: one event pair around all its
+    launches, back to back on one stream (the sparse chain, then the all-dense
+    chain), behind the step's device sleep; mean milliseconds per chain."""
+    E = torch.cuda.Event
+    ev = [[E(enable_timing=True) for _ in range(4)] for _ in range(reps)]
+    for r in range(reps):
+        for side in (0, 1):
+            torch.cuda._sleep(sleep_cycles)
+            ev[r][2 * side].record()
+            for p in preps:
+                p.run_dense() if side else p.run_sparse()
+            ev[r][2 * side + 1].record()
+    torch.cuda.synchronize()
+    sp = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    dn = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
+    return sp, dn
+
+
 def time_keyed_in_steps(preps, key, torch, reps):
     """Untimed detail pass in the step's own cache state: `reps` whole steps in
     which the GEMMs are ordered by `key(prep)` (sparse calls of each key, then
@@ -550,6 +569,9 @@ def predictor_experiment(torch, n_cal, n_test, report):
     T_cal = np.array([cb.measure(a) for a in cal])
     T_test = np.array([cb.measure(a) for a in test])
     log(f"{len(cal) + len(test)} chains measured in {time.perf_counter() - t0:.1f} s")
+    # the chain workload's own layer-wise draw (the last test configuration)
+    draw = {"measured_us": round(float(T_test[-1]), 1),                # the all-dense chain is T_test[-2]
+            "speedup_vs_dense": round(float(T_test[-2] / T_test[-1]), 3)}
     luts = {"cold": table, "hot": hot}
     R_cal = {k: np.array([cb.layer_times(t, a) for a in cal]) for k, t in luts.items()}
     R_test = {k: np.array([cb.layer_times(t, a) for a in test]) for k, t in luts.items()}
@@ -632,7 +654,7 @@ def predictor_experiment(torch, n_cal, n_test, report):
     res = {"workload": "vit_large_384_b32 linears (96 GEMMs, int32 outputs)", "lut_entries": len(table),
            "lut_build_s": round(lut_s, 2), "calibration_configs": len(cal), "test_configs": len(test),
            "chain_dense_us": round(float(T_test[len(test) - 2]), 1), "fits": fits, "predictor": chosen,
-           "family": family, "search": searches}
+           "family": family, "search": searches, "workload_draw": draw}
     if report:
         write_predictor_report(res, report)
     return res
@@ -645,7 +667,9 @@ def write_predictor_report(res, path):
           f"{res['lut_build_s']} s (each run starts with flushed caches; the hot LUT of back-to-back repeats is "
           f"shown for comparison).  Calibration on {res['calibration_configs']} random layer-wise N:8 "
           f"configurations, prediction error on {res['test_configs']} others (random, the eight uniform ones and "
-          f"the seeded layer-wise draw of the chain workload).  All-dense chain: {res['chain_dense_us']} us.", "",
+          f"the seeded layer-wise draw of the chain workload).  All-dense chain: {res['chain_dense_us']} us; the "
+          f"chain workload's seeded layer-wise draw: {res['workload_draw']['measured_us']} us "
+          f"({res['workload_draw']['speedup_vs_dense']}x).", "",
           "| fit | mean abs error % | max abs error % | share within 5% |", "|---|---:|---:|---:|"]
     for k, v in res["fits"].items():
         md.append(f"| {k} | {v['mean_abs_pct']} | {v['max_abs_pct']} | {v['within_5pct']} |")
@@ -1260,6 +1284,7 @@ def main():
     tg = t.mean(axis=0)  # per group: mean over steps (the paper averages repeated runs, Sec. 5.1)
     graph_sparse_ms, graph_dense_ms = (graph_steps(preps, groups, args.steps, torch, sleep_cycles)
                                        if not args.no_graph else (None, None))
+    chain = chain_times(preps, torch, max(3, min(args.steps, 10)), sleep_cycles) if work.chain else None
 
     ops = np.array([p.g.dense_eq_ops for p in preps], np.float64)
     sparse_ms = sum(tg[gi] for gi, ((side, _), _) in enumerate(groups) if side == "sparse")
@@ -1291,6 +1316,11 @@ def main():
     dom_idx = next(idx for (side, name), idx in groups if side == "sparse" and name == dom_name)
     store_ms = None if args.no_store_only else store_only_time(preps, dom_idx, torch)
     achieved = dom["bytes"] / dom["launches"] / (avg_ms * 1e-3) / 1e9
+    # which roofline binds this kernel: its algorithmic bytes at the HBM peak
+    # against its dense-equivalent ops at the matrix-core peak of its kind
+    dom_ops = sum(preps[i].g.dense_eq_ops for i in dom_idx)
+    peak_ops = PEAK_SPARSE_TOPS if preps[dom_idx[0]].splan.kind == nmspmm.NM_KIND_SP42 else PEAK_INT8_TOPS
+    mfma_bound = dom_ops / (peak_ops * 1e12) > dom["bytes"] / (PEAK_HBM_GBS * 1e9)
     traffic = None
     tpath = args.traffic or default_traffic_path(work.name)
     if os.path.exists(tpath):
@@ -1300,18 +1330,22 @@ def main():
         if (tr.get("kernel") == dom_name and tr.get("workload") == work.name
                 and tr.get("kernel_source_sha256") == kernel_source_sha256()):
             traffic = tr.get("bytes_per_launch")
-    roofline = {
-        "bound": "hbm",
-        "achieved": round(achieved, 1),
-        "peak": PEAK_HBM_GBS,
-        "unit": "GB/s",
-        "frac": round(achieved / PEAK_HBM_GBS, 4),
+    if mfma_bound:
+        achieved_ops = dom_ops / dom["launches"] / (avg_ms * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "achieved": round(achieved_ops, 1), "peak": peak_ops, "unit": "TOPS",
+                    "frac": round(achieved_ops / peak_ops, 4)}
+    else:
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roofline.update({
         "traffic": traffic,
         "kernel": dom_name,
         "launches_per_step": dom["launches"],
         "avg_launch_us": round(avg_ms * 1e3, 2),
         "algorithmic_bytes_per_launch": int(dom["bytes"] / dom["launches"]),
-    }
+        "algorithmic_ops_per_launch": int(dom_ops / dom["launches"]),
+        "hbm_gbs": round(achieved, 1),
+    })
     if store_ms is not None:
         # the same launches with the reduction skipped: the ceiling this
         # kernel's own output stream sets (context beside the HBM peak)
@@ -1365,6 +1399,12 @@ def main():
         "dense_ms_per_step": round(float(dense_ms), 4),
         "roofline": roofline,
     }
+    if chain is not None:
+        # the layers in network order, one event pair around the whole chain
+        line["chain"] = {"sparse_ms": round(chain[0], 4), "dense_ms": round(chain[1], 4),
+                         "speedup_vs_dense": round(chain[1] / chain[0], 3),
+                         "tops": round(float(ops.sum() / (chain[0] * 1e-3) / 1e12), 2)}
+        log(json.dumps({"chain": line["chain"]}))
     if graph_sparse_ms is not None:
         # the same step with its launches replayed from HIP graphs (no host
         # launch path between kernels): context, not `value`

@@ -2,6 +2,7 @@
 in this process): the JSON line carries the contract's fields with sane
 values, and the roofline object names the dominant kernel."""
 import json
+import re
 import sys
 
 import pytest
@@ -25,7 +26,15 @@ def test_bench_config_line(cfg, capsys, monkeypatch):
     assert line["value"] > 0 and line["ms_per_step"] > 0 and line["speedup_vs_dense"] > 0
     assert line["dtype"] == "int8" and line["vs_baseline"] is None and line["cpu_baseline"] is None
     r = line["roofline"]
-    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    # the binding roofline: HBM bytes or matrix-core ops, whichever takes longer at its peak
+    t_hbm = r["algorithmic_bytes_per_launch"] / 8000e9
+    if r["bound"] == "hbm":
+        assert r["unit"] == "GB/s" and r["peak"] == 8000.0
+        one_stream = re.match(r"k_gemm(_ks|_rs|_ps)?<1,", r["kernel"]) is not None
+        assert r["algorithmic_ops_per_launch"] / (10066e12 if one_stream else 5033e12) <= t_hbm
+    else:
+        assert r["bound"] == "mfma" and r["unit"] == "TOPS" and r["peak"] in (10066.0, 5033.0)
+        assert r["algorithmic_ops_per_launch"] / (r["peak"] * 1e12) > t_hbm
     assert 0 < r["frac"] <= 1 and r["kernel"].startswith("k_gemm")
     assert abs(r["achieved"] / r["peak"] - r["frac"]) < 1e-3
     assert line["config"]["workload"]
