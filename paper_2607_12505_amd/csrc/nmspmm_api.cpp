@@ -26,6 +26,26 @@ nm_outputs outputs_of(int32_t *Y, const float *scale, uint16_t *Yh) {
     return o;
 }
 
+// Tile order of the launch.  Row by row, the tiles in flight on one XCD sweep
+// the whole weight operand once per row of tiles; once the weight as stored
+// (packed values and positions, or dense W) no longer fits in most of the
+// XCD's 4 MB L2, every row reads it again from the last-level cache or HBM.
+// Walking groups of 8 tile rows column by column reads it once per group
+// instead.  Measured over m 4096-25216, n 1024-8192, k 768-4096, for dense,
+// one- and two-stream weights, with operands resident in or evicted from the
+// last-level cache: up to 23 % faster on large weights and at most 5 % slower
+// on any shape this rule groups.  Smaller weights, and launches with fewer
+// than 64 rows of tiles, keep the row order: grouping them cost up to 20 %.
+constexpr int64_t kGroupWeightBytes = (int64_t)7 << 19;  // 3.5 MiB
+constexpr int kGroupRows = 8;
+
+int group_rows_for(int kind, int n, int k, int n_frags, int k_steps, int tiles_m) {
+    const int streams = kind == NM_KIND_SP42X2 ? 2 : 1;
+    const int64_t stored =
+        kind == NM_KIND_DENSE ? (int64_t)n * k : (int64_t)n_frags * k_steps * streams * (kVBlock + kMBlock);
+    return stored >= kGroupWeightBytes && tiles_m >= 8 * kGroupRows ? kGroupRows : 0;
+}
+
 nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint8_t *meta, int n, int k,
                    int k_steps, int n_frags, const nm_outputs *out, void *ws, size_t ws_bytes, void *stream,
                    const nm_plan *forced) {
@@ -77,6 +97,7 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
     a.tiles_n = (n + plan.tile_n - 1) / plan.tile_n;
     a.tiles_m = (m + plan.tile_m - 1) / plan.tile_m;
     a.split_k = plan.split_k;
+    a.group_rows = group_rows_for(kind, n, k, n_frags, k_steps, a.tiles_m);
     int err = launch_gemm(kind, plan.tile, a, plan.grid, stream);
     return err == 0 ? NM_OK : NM_ERR_HIP;
 }
@@ -247,6 +268,7 @@ extern "C" nm_status nm_probe_store_only(const nm_plan *plan, int m, int n, cons
     a.tiles_n = (n + p.tile_n - 1) / p.tile_n;
     a.tiles_m = (m + p.tile_m - 1) / p.tile_m;
     a.split_k = 1;
+    a.group_rows = 0;
     return launch_gemm(p.kind, p.tile, a, p.grid, stream) == 0 ? NM_OK : NM_ERR_HIP;
 }
 

@@ -116,6 +116,7 @@ struct GemmArgs {
     int m, n, k;
     int k_steps, n_frags;
     int tiles_n, tiles_m, split_k;
+    int group_rows;         // tile order: 0 row by row, else groups of this many tile rows
 };
 
 // Workspace of a split-K plan: a fixed block of per-tile arrival counters,

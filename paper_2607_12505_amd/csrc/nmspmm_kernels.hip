@@ -55,6 +55,25 @@ __device__ inline int map_block(int bid, int nwg) {
     return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
+// Logical tile -> (column tile tn, row index `rest`) over `rows` rows of
+// tiles_n tiles.  group_rows == 0: row by row (consecutive tiles share rows of
+// X and sweep all of W).  Otherwise groups of group_rows rows, each walked
+// column by column, so the tiles in flight on one XCD touch a group's rows of
+// X and only part of W.  Either way a bijection onto [0, rows * tiles_n).
+__device__ inline void tile_order(int lid, int tiles_n, int rows, int group_rows, int *tn, int *rest) {
+    if (group_rows <= 0) {
+        *tn = lid % tiles_n;
+        *rest = lid / tiles_n;
+        return;
+    }
+    const int span = group_rows * tiles_n;
+    const int g = lid / span, r = lid - g * span;
+    const int left = rows - g * group_rows;
+    const int h = left < group_rows ? left : group_rows;
+    *rest = g * group_rows + r % h;
+    *tn = r / h;
+}
+
 // Buffer-resource word 3 for raw 32-bit accesses, and the cache-policy bit
 // that makes a buffer access coherent at agent scope (sc1).
 constexpr int kBufferFlags = 0x00020000;
@@ -492,8 +511,8 @@ __global__ __launch_bounds__(64 * WN * WM) void k_gemm(GemmArgs a) {
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
 
     const int lid = map_block(blockIdx.x, gridDim.x);
-    const int tn = lid % a.tiles_n;
-    const int rest = lid / a.tiles_n;
+    int tn, rest;
+    tile_order(lid, a.tiles_n, a.tiles_m * a.split_k, a.group_rows, &tn, &rest);
     const int split = rest % a.split_k;
     const int tm = rest / a.split_k;
     const int tid = threadIdx.x, lane = tid & 63;

@@ -2,7 +2,8 @@
 4.3): one seeded shape per rule, for one-stream (2:4), two-stream (4:8) and
 dense weights, compared element by element with the oracle in the launch
 configuration the planner picks (int32 and fp16 outputs, guard bands after
-both).  The expected tile of each case documents the rule it exercises."""
+both).  The expected tile of each case documents the rule it exercises; the
+last cases launch with the grouped tile order that large weights take."""
 import numpy as np
 import pytest
 
@@ -33,6 +34,10 @@ CASES = [
     (6272, 1536, 512, "sp", (64, 64), False),   # ... 64 x 64 past 4 half-height tiles per CU
     (8192, 2048, 512, "sp", (128, 128), False),  # large: 128 x 128
     (4096, 4096, 512, "x2", (256, 256), False),  # large, heavier operands, 4096 wide: 256 x 256 on 8 waves
+    # weights of 3.5 MiB or more over at least 64 rows of tiles: tiles walked in groups of 8 rows
+    (8300, 3072, 2048, "sp", (128, 128), False),  # 65 tile rows: the last group has one row
+    (8192, 3072, 1024, "x2", (128, 128), False),
+    (8192, 2048, 2048, "dn", (128, 128), False),
 ]
 
 
