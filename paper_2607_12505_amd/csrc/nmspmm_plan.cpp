@@ -155,9 +155,13 @@ nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *
     } else if (heavy) {
         // Large outputs, heavier operands: 128 x 128 on 8 waves (4 along the
         // channels x 2 along the tokens, twice the waves to overlap the
-        // operand reads with the stores), or on the widest outputs the
-        // 256 x 256 tile on 8 waves, which halves the operand fill per output.
-        tile = n >= 4096 ? kT256x256w8 : kT128x128w8;
+        // operand reads with the stores), or, on the widest outputs with long
+        // reductions (24 k-steps or more), the 256 x 256 tile on 8 waves,
+        // which halves the operand fill per output.  With the grouped tile
+        // order that large weights take, 128 x 128 is 7-14 % faster than
+        // 256 x 256 at k = 1024 and 256 x 256 6-13 % faster at k = 4096
+        // (n 4096 and 8192, m 8192-25216, dense and 4:8).
+        tile = (n >= 4096 && k_steps >= 24) ? kT256x256w8 : kT128x128w8;
     } else {
         // Large outputs, one-stream weights: 128 x 128 on 8 waves, except for
         // long reductions (24 k-steps or more) and the widest outputs, where

@@ -33,7 +33,8 @@ CASES = [
     (1600, 2304, 768, "dn", (64, 128), False),  # ... narrower for the heavier operands
     (6272, 1536, 512, "sp", (64, 64), False),   # ... 64 x 64 past 4 half-height tiles per CU
     (8192, 2048, 512, "sp", (128, 128), False),  # large: 128 x 128
-    (4096, 4096, 512, "x2", (256, 256), False),  # large, heavier operands, 4096 wide: 256 x 256 on 8 waves
+    (4096, 4096, 3072, "x2", (256, 256), False),  # large, heavier operands, 4096 wide, long reduction: 256 x 256
+    (4096, 4096, 512, "x2", (128, 128), False),   # ... shorter reduction: 128 x 128 on 8 waves
     # weights of 3.5 MiB or more over at least 64 rows of tiles: tiles walked in groups of 8 rows
     (8300, 3072, 2048, "sp", (128, 128), False),  # 65 tile rows: the last group has one row
     (8192, 3072, 1024, "x2", (128, 128), False),

@@ -90,12 +90,18 @@ def test_large_shapes_use_large_tiles():
     assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 25216, 1)) == "k_gemm<1, 2, 2, 4, 4, 2>"
     # the dense baseline of DeiT-B fc2 at batch 128: 8 waves
     assert nmspmm.plan_kernel_name(nmspmm.dense_plan(25216, 768, 3072, 1)) == "k_gemm<3, 4, 2, 2, 4, 2>"
-    # the widest outputs of the heavier operands: 256 x 256 on 8 waves (ViT-L fc1)
-    d = nmspmm.compress_size(4096, 1024, 4, 8)
+    # the widest outputs of the heavier operands with long reductions: 256 x 256 on 8 waves
+    d = nmspmm.compress_size(4096, 4096, 4, 8)
     p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)
     assert (p.tile_n, p.tile_m) == (256, 256) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 2, 4, 8, 4, 3>"
-    p = nmspmm.dense_plan(18464, 4096, 1024, nmspmm.NM_OUT_I32)
+    p = nmspmm.dense_plan(18464, 8192, 3072, nmspmm.NM_OUT_I32)
     assert (p.tile_n, p.tile_m) == (256, 256)
+    # ... and 128 x 128 on 8 waves for shorter ones (ViT-L fc1, 4:8 and its dense baseline)
+    d = nmspmm.compress_size(4096, 1024, 4, 8)
+    p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)
+    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 4, 2, 2, 4, 2>"
+    p = nmspmm.dense_plan(18464, 4096, 1024, nmspmm.NM_OUT_I32)
+    assert nmspmm.plan_kernel_name(p) == "k_gemm<3, 4, 2, 2, 4, 2>"
     d = nmspmm.compress_size(4096, 1024, 2, 4)           # one-stream weight: 128 x 128
     assert (nmspmm.spmm_plan(d, 18464, 1).tile_n, nmspmm.spmm_plan(d, 18464, 1).tile_m) == (128, 128)
     d = nmspmm.compress_size(768, 3072, 2, 4)
