@@ -30,7 +30,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from paper_2607_12505_amd import nmspmm  # noqa: E402
+from paper_2607_12505_amd import nmprobe, nmspmm  # noqa: E402
 from paper_2607_12505_amd import workloads as wl  # noqa: E402
 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
@@ -240,7 +240,7 @@ def store_only_time(preps, idx, torch, reps=10):
     loads or matrix work), timed like a launch group of the step; None if a
     plan's layout has no such mode.  The real results are written back
     afterwards."""
-    L = nmspmm.lib()
+    L = nmprobe.lib()
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     calls = []
     for i in idx:
@@ -1138,23 +1138,23 @@ def mfma_ceiling(torch, iters: int = 4000, reps: int = 3) -> dict:
     the chip lower its clock)."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     g = torch.Generator().manual_seed(2607)
-    rnd = torch.randint(-2 ** 31, 2 ** 31, (nmspmm.NM_PROBE_WORDS,), generator=g, dtype=torch.int64)
+    rnd = torch.randint(-2 ** 31, 2 ** 31, (nmprobe.NM_PROBE_WORDS,), generator=g, dtype=torch.int64)
     rnd = rnd.to(torch.int32).cuda()
     zero = torch.zeros_like(rnd)
     wgs = 4 * cus
     out = torch.empty(wgs * 256, dtype=torch.int32, device="cuda")
     ticks = torch.zeros(2 * wgs, dtype=torch.int64, device="cuda")
-    wall_hz = nmspmm.wall_clock_khz() * 1e3
+    wall_hz = nmprobe.wall_clock_khz() * 1e3
     res = {}
     for kind, name, macs in ((nmspmm.NM_KIND_SP42, "smfmac_i32_16x16x128_i8", 16 * 16 * 128),
                              (nmspmm.NM_KIND_DENSE, "mfma_i32_16x16x64_i8", 16 * 16 * 64)):
         for tname, tab in (("random", rnd), ("zero", zero)):
-            nmspmm.probe_mfma_rate(kind, tab, 16, out)
+            nmprobe.probe_mfma_rate(kind, tab, 16, out)
             best, mhz = float("inf"), 0.0
             for _ in range(reps):
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 e0.record()
-                nmspmm.probe_mfma_rate(kind, tab, iters, out, ticks)
+                nmprobe.probe_mfma_rate(kind, tab, iters, out, ticks)
                 e1.record()
                 torch.cuda.synchronize()
                 ms = e0.elapsed_time(e1)

@@ -46,9 +46,13 @@ int group_rows_for(int kind, int n, int k, int n_frags, int k_steps, int tiles_m
     return stored >= kGroupWeightBytes && tiles_m >= 8 * kGroupRows ? kGroupRows : 0;
 }
 
+}  // namespace
+
+namespace nmspmm {
+
 nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint8_t *meta, int n, int k,
                    int k_steps, int n_frags, const nm_outputs *out, void *ws, size_t ws_bytes, void *stream,
-                   const nm_plan *forced) {
+                   const nm_plan *forced, WorkspaceFn ws_fn) {
     if (m < 0) return NM_ERR_SHAPE;
     if (m == 0) return NM_OK;  // nothing to compute; empty tensors may carry null pointers
     if (!out) return NM_ERR_ARG;
@@ -76,6 +80,10 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
     }
     const int tiles = plan.grid / plan.split_k;
     const size_t need = workspace_bytes(plan.split_k, tiles, m, n);
+    if (need > 0 && ws_fn) {
+        nm_status st = ws_fn(need, stream, &ws, &ws_bytes);
+        if (st != NM_OK) return st;
+    }
     if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return NM_ERR_WORKSPACE;
 
     GemmArgs a;
@@ -112,7 +120,7 @@ nm_status check_desc(const nm_desc *d) {
 
 int kind_of(const nm_desc *d) { return d->streams == 1 ? NM_KIND_SP42 : NM_KIND_SP42X2; }
 
-}  // namespace
+}  // namespace nmspmm
 
 extern "C" const char *nm_status_string(nm_status s) {
     switch (s) {
@@ -143,11 +151,6 @@ extern "C" nm_status nm_plan_kernel_name(const nm_plan *plan, char *buf, int len
     int w;
     if (t.layout == kKSliced)
         w = std::snprintf(buf, (size_t)len, "k_gemm_ks<%d, %d, %d, %d>", plan->kind, t.fn, t.fm, t.nst);
-    else if (t.layout == kRowStat)
-        w = std::snprintf(buf, (size_t)len, "k_gemm_rs<%d, %d, %d, %d>", plan->kind, t.fn, t.fm, t.nst);
-    else if (t.layout == kPersist)
-        w = std::snprintf(buf, (size_t)len, "k_gemm_ps<%d, %d, %d, %d, %d, %d>", plan->kind, t.wn, t.wm, t.fn, t.fm,
-                          t.nst);
     else
         w = std::snprintf(buf, (size_t)len, "k_gemm<%d, %d, %d, %d, %d, %d>", plan->kind, t.wn, t.wm, t.fn, t.fm, t.nst);
     return (w > 0 && w < len) ? NM_OK : NM_ERR_ARG;
@@ -186,7 +189,7 @@ extern "C" nm_status nm_spmm_out(const int8_t *X, int m, const int8_t *vals, con
     nm_status st = check_desc(desc);
     if (st != NM_OK) return st;
     return run_gemm(kind_of(desc), X, m, vals, meta, desc->n, desc->k, desc->k_steps, desc->n_frags, out, ws,
-                    ws_bytes, stream, plan);
+                    ws_bytes, stream, plan, nullptr);
 }
 
 extern "C" nm_status nm_spmm_ex(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
@@ -209,7 +212,7 @@ extern "C" nm_status nm_gemm_i8_dense_out(const int8_t *X, int m, const int8_t *
     if (k % 16 != 0 || n % 4 != 0) return NM_ERR_SHAPE;
     const int k_steps = (k + kKStep - 1) / kKStep;
     return run_gemm(NM_KIND_DENSE, X, m, W, nullptr, n, k, k_steps, (n + kFragRows - 1) / kFragRows, out, ws,
-                    ws_bytes, stream, plan);
+                    ws_bytes, stream, plan, nullptr);
 }
 
 extern "C" nm_status nm_gemm_i8_dense_ex(const int8_t *X, int m, const int8_t *W, int n, int k,
@@ -223,53 +226,6 @@ extern "C" nm_status nm_gemm_i8_dense(const int8_t *X, int m, const int8_t *W, i
                                       int32_t *Y, const float *scale, uint16_t *Yh,
                                       void *ws, size_t ws_bytes, void *stream) {
     return nm_gemm_i8_dense_ex(X, m, W, n, k, Y, scale, Yh, ws, ws_bytes, stream, nullptr);
-}
-
-extern "C" nm_status nm_probe_store_only(const nm_plan *plan, int m, int n, const nm_outputs *out, void *stream) {
-    if (!plan || !out) return NM_ERR_ARG;
-    if (m < 0 || n < 4 || n % 4 != 0) return NM_ERR_SHAPE;
-    if (m == 0) return NM_OK;
-    if ((int64_t)m * n >= ((int64_t)1 << 29)) return NM_ERR_SHAPE;
-    const nm_outputs o = *out;
-    if (!o.y && !o.yh && !o.yq) return NM_ERR_ARG;
-    if ((o.yh && !o.scale) || (o.yq && !o.qscale)) return NM_ERR_ARG;
-    if ((o.y && !aligned16(o.y)) || (o.yh && !aligned16(o.yh)) || (o.yh && !aligned16(o.scale)) ||
-        (o.yq && !aligned16(o.yq)) || (o.yq && !aligned16(o.qscale)))
-        return NM_ERR_ARG;
-    if (plan->tile < 0 || plan->tile >= kNumTiles || kTiles[plan->tile].layout != kOutSplit || plan->split_k != 1)
-        return NM_ERR_ARG;
-    if (plan->kind != NM_KIND_SP42 && plan->kind != NM_KIND_SP42X2 && plan->kind != NM_KIND_DENSE) return NM_ERR_ARG;
-    nm_plan p = *plan;
-    nm_status st = complete_plan(p.kind, m, n, 1, &p);
-    if (st != NM_OK) return st;
-    // Zero k-steps: the kernel issues no operand loads and no matrix
-    // instructions; the epilogue stores the zero accumulators.  The epilogue
-    // reads its multipliers unconditionally, from X when one is absent, so X
-    // must still be a readable device address of at least 16 aligned bytes:
-    // a scale vector (n >= 4 floats) or, when there is none, the int32 output
-    // (m * n >= 4 words).
-    const void *readable = o.scale ? (const void *)o.scale : o.qscale ? (const void *)o.qscale : (const void *)o.y;
-    GemmArgs a;
-    a.X = (const int8_t *)readable;
-    a.A = nullptr;
-    a.meta = nullptr;
-    a.Y = o.y;
-    a.Yh = o.yh;
-    a.scale = o.scale;
-    a.Yq = o.yq;
-    a.qscale = o.qscale;
-    a.counters = nullptr;
-    a.partials = nullptr;
-    a.m = m;
-    a.n = n;
-    a.k = 128;
-    a.k_steps = 0;
-    a.n_frags = (n + kFragRows - 1) / kFragRows;
-    a.tiles_n = (n + p.tile_n - 1) / p.tile_n;
-    a.tiles_m = (m + p.tile_m - 1) / p.tile_m;
-    a.split_k = 1;
-    a.group_rows = 0;
-    return launch_gemm(p.kind, p.tile, a, p.grid, stream) == 0 ? NM_OK : NM_ERR_HIP;
 }
 
 extern "C" nm_status nm_quantize_f16(const uint16_t *x, int64_t count, float inv_scale, int8_t *xq, void *stream) {

@@ -23,15 +23,8 @@ constexpr int kThreads = 256;    // threads of a k-sliced workgroup (4 waves of 
 //               FM * 16 tokens); one output tile per workgroup.
 //   kKSliced:   every wave computes the whole FN x FM-fragment tile over a
 //               quarter of the k-steps (wn = wm = 1); one tile per workgroup.
-//   kRowStat:   2 x 2 consumer waves as kOutSplit plus one producer wave; the
-//               workgroup keeps a token block of X in LDS and walks a range of
-//               output tiles (row-stationary), so the grid is a fixed number
-//               of workgroups.
-//   kPersist:   kOutSplit tiles walked by a fixed grid of workgroups, the
-//               (tile, k-step) slices streaming through one ring so the next
-//               tile loads while the current one is stored; split_k = 1.
 // nst = depth of the ring of k-step slots staged in LDS.
-enum Layout { kOutSplit = 0, kKSliced = 1, kRowStat = 2, kPersist = 3 };
+enum Layout { kOutSplit = 0, kKSliced = 1 };
 
 struct TileCfg {
     int wn, wm, fn, fm, nst, layout;
@@ -39,67 +32,23 @@ struct TileCfg {
     constexpr int tile_m() const { return wm * fm * 16; }
 };
 
-// Tiles the kernels are instantiated for, from the largest to the smallest.
+// Tiles the kernels are instantiated for: the candidates of the planner
+// (each is its choice for some class of shapes).
 constexpr TileCfg kTiles[] = {
-    {2, 2, 8, 8, 2, kOutSplit},  // 0: 256 ch x 256 tok
-    {2, 2, 8, 4, 3, kOutSplit},  // 1: 256 ch x 128 tok
-    {2, 2, 4, 4, 3, kOutSplit},  // 2: 128 ch x 128 tok
-    {4, 1, 4, 4, 3, kOutSplit},  // 3: 256 ch x  64 tok
-    {2, 2, 4, 2, 4, kOutSplit},  // 4: 128 ch x  64 tok
-    {2, 2, 2, 4, 4, kOutSplit},  // 5:  64 ch x 128 tok
-    {2, 2, 2, 2, 4, kOutSplit},  // 6:  64 ch x  64 tok
+    {2, 2, 4, 4, 2, kOutSplit},  // 0: 128 ch x 128 tok, 2-slot ring (3 workgroups per CU)
+    {2, 2, 4, 2, 2, kOutSplit},  // 1: 128 ch x  64 tok, 2-slot ring
+    {2, 2, 2, 4, 2, kOutSplit},  // 2:  64 ch x 128 tok, 2-slot ring
+    {2, 2, 2, 2, 2, kOutSplit},  // 3:  64 ch x  64 tok, 2-slot ring
+    {2, 4, 8, 4, 3, kOutSplit},  // 4: 256 ch x 256 tok, 8 waves (2 x 4), 3-slot ring
+    {2, 2, 4, 1, 2, kOutSplit},  // 5: 128 ch x  32 tok, 2-slot ring
+    {4, 2, 2, 4, 2, kOutSplit},  // 6: 128 ch x 128 tok, 8 waves (4 x 2), 2-slot ring
     {1, 1, 4, 4, 3, kKSliced},   // 7:  64 ch x  64 tok, k-sliced over the waves
     {1, 1, 2, 4, 3, kKSliced},   // 8:  32 ch x  64 tok, k-sliced
     {1, 1, 4, 2, 3, kKSliced},   // 9:  64 ch x  32 tok, k-sliced
     {1, 1, 2, 2, 3, kKSliced},   // 10: 32 ch x  32 tok, k-sliced
-    {2, 2, 4, 4, 3, kRowStat},   // 11: 128 ch x 128 tok, row-stationary
-    {2, 2, 4, 2, 3, kRowStat},   // 12: 128 ch x  64 tok, row-stationary
-    {2, 2, 8, 2, 3, kRowStat},   // 13: 256 ch x  64 tok, row-stationary
-    {2, 2, 4, 4, 3, kPersist},   // 14: 128 ch x 128 tok, persistent
-    {2, 2, 4, 2, 4, kPersist},   // 15: 128 ch x  64 tok, persistent
-    {2, 2, 4, 4, 2, kOutSplit},  // 16: 128 ch x 128 tok, 2-slot ring (3 workgroups per CU)
-    {2, 2, 4, 2, 2, kOutSplit},  // 17: 128 ch x  64 tok, 2-slot ring
-    {2, 2, 2, 4, 2, kOutSplit},  // 18:  64 ch x 128 tok, 2-slot ring
-    {2, 2, 2, 2, 2, kOutSplit},  // 19:  64 ch x  64 tok, 2-slot ring
-    {2, 4, 8, 4, 3, kOutSplit},  // 20: 256 ch x 256 tok, 8 waves (2 x 4), 3-slot ring
-    {2, 4, 8, 2, 2, kOutSplit},  // 21: 256 ch x 128 tok, 8 waves, 2-slot ring
-    {2, 2, 4, 1, 2, kOutSplit},  // 22: 128 ch x  32 tok, 2-slot ring
-    {4, 2, 2, 4, 2, kOutSplit},  // 23: 128 ch x 128 tok, 8 waves (4 x 2), 2-slot ring
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
-
-// LDS of a row-stationary workgroup: the resident X block (every k-step of
-// tile_m tokens), the weight ring, and per-wave epilogue staging.
-struct RowStatLds {
-    size_t xblock, wslot, ring, staging, total;
-};
-inline RowStatLds rowstat_lds(int kind, const TileCfg &t, int k_steps) {
-    const bool sparse = kind != NM_KIND_DENSE;
-    const int S = kind == NM_KIND_SP42X2 ? 2 : 1;
-    const int BN = t.tile_n(), BM = t.tile_m();
-    RowStatLds L;
-    L.xblock = (size_t)k_steps * BM * 128;
-    L.wslot = sparse ? (size_t)(BN / 16) * S * (kVBlock + kMBlock) : (size_t)BN * 128;
-    L.ring = (size_t)t.nst * L.wslot;
-    L.staging = (size_t)4 * 16 * (t.fn * 64 + 16);
-    L.total = L.xblock + L.ring + L.staging;
-    return L;
-}
 constexpr size_t kLdsPerCu = 160 * 1024;
-
-// LDS of an output-split workgroup (kOutSplit, kPersist): the ring of k-step
-// slots (X slice and weight slice), as deep as asked or as 160 KB allows, or
-// the epilogue staging if larger.
-inline size_t outsplit_lds(int kind, const TileCfg &t) {
-    const bool sparse = kind != NM_KIND_DENSE;
-    const int S = kind == NM_KIND_SP42X2 ? 2 : 1;
-    const size_t BN = t.tile_n(), BM = t.tile_m();
-    const size_t slot = BM * 128 + (sparse ? (BN / 16) * S * (kVBlock + kMBlock) : BN * 128);
-    const size_t cap = kLdsPerCu - 1024;
-    const size_t ring = (size_t)t.nst * slot <= cap ? (size_t)t.nst : cap / slot;
-    const size_t epi = (size_t)t.wn * t.wm * 16 * (t.fn * 64 + 16);
-    return ring * slot > epi ? ring * slot : epi;
-}
 
 // Everything a GEMM kernel needs; passed by value as the kernel argument.
 struct GemmArgs {
@@ -133,6 +82,16 @@ int device_cu_count();     // cached per device; 256 when no device is visible
 int launch_gemm(int kind, int tile, const GemmArgs &args, int grid, void *stream);
 int launch_zero(void *ptr, size_t bytes, void *stream);
 int launch_quantize_f16(const uint16_t *x, int64_t count, float inv_scale, int8_t *xq, void *stream);
+
+// Argument checks, planning and launch of one GEMM (nmspmm_api.cpp).  When
+// the plan needs a workspace and ws_fn is given, ws_fn supplies it instead of
+// ws / ws_bytes.
+typedef nm_status (*WorkspaceFn)(size_t need, void *stream, void **ws, size_t *ws_bytes);
+nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint8_t *meta, int n, int k,
+                   int k_steps, int n_frags, const nm_outputs *out, void *ws, size_t ws_bytes, void *stream,
+                   const nm_plan *forced, WorkspaceFn ws_fn);
+nm_status check_desc(const nm_desc *d);
+int kind_of(const nm_desc *d);
 
 // Planner shared by both GEMM families.
 nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *plan);

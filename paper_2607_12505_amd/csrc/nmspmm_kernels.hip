@@ -209,12 +209,17 @@ __device__ inline void emit_out(const GemmArgs &a, int tok, int ch, const v4i &v
     }
 }
 
+// Multipliers read in place of an absent multiplier array (the value is never
+// used: the output it scales is absent too).  A valid address owned by the
+// library, so no caller pointer is read for a missing array.
+__device__ const float kNoScale[4] = {1.0f, 1.0f, 1.0f, 1.0f};
+
 // The multipliers of 4 consecutive channels.  The loads are issued whatever
-// outputs are present (from a valid dummy address when a multiplier array is
-// absent, or from channel 0 past n) so that no branch guards them: the
-// compiler then waits for them once, at their first use, instead of emitting
-// a full vector-memory wait before every later use, which would also wait
-// for every store issued in between.
+// outputs are present (from kNoScale when a multiplier array is absent, or
+// from channel 0 past n) so that no branch guards them: the compiler then
+// waits for them once, at their first use, instead of emitting a full
+// vector-memory wait before every later use, which would also wait for every
+// store issued in between.
 //
 // The loads are also awaited right away (all vector-memory operations of the
 // wave): the compiler's own wait tracking cannot see through the output
@@ -223,11 +228,11 @@ __device__ inline void emit_out(const GemmArgs &a, int tok, int ch, const v4i &v
 // that they could keep waiting for.
 __device__ inline EpiScale load_scale(const GemmArgs &a, int ch) {
     const int c = ch < a.n ? ch : 0;
-    const float *sc = a.scale ? a.scale : (const float *)a.X;    // X holds at least 16 aligned bytes
-    const float *qs = a.qscale ? a.qscale : (const float *)a.X;
+    const float *sc = a.scale ? a.scale + c : kNoScale;
+    const float *qs = a.qscale ? a.qscale + c : kNoScale;
     EpiScale es;
-    es.sc = *(const v4f *)(sc + (a.scale ? c : 0));
-    es.qs = *(const v4f *)(qs + (a.qscale ? c : 0));
+    es.sc = *(const v4f *)sc;
+    es.qs = *(const v4f *)qs;
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0); expcnt and lgkmcnt not waited for
     return es;
 }
@@ -252,15 +257,20 @@ __device__ inline v4i merge_partials(const GemmArgs &a, __amdgpu_buffer_rsrc_t r
     return sum;
 }
 
-// After every thread published its part of this split's partial tile: wait
-// for the stores to complete, count the arrival, and tell whether this
-// workgroup is the last split of the tile (then it merges).  The counter is
-// left at zero for the next call.
+// After every thread published its part of this split's partial tile: count
+// the arrival and tell whether this workgroup is the last split of the tile
+// (then it merges).  Ordering: the barrier makes every wave's partial stores
+// happen before thread 0's arrival, which is a release at agent scope, so a
+// split that arrives later and reads the count with acquire ordering sees
+// them; the last arriver's acquire is passed to its other threads by the
+// second barrier.  (The wait for this wave's stores before the barrier is
+// not needed by that argument; it keeps the stores complete before the
+// counter moves.)  The counter is left at zero for the next call.
 __device__ inline bool arrive_last(const GemmArgs &a, int tile, int *s_flag) {
-    __builtin_amdgcn_s_waitcnt(0);  // every store of this wave has completed
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x == 0) {
-        const int old = __hip_atomic_fetch_add(&a.counters[tile], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int old = __hip_atomic_fetch_add(&a.counters[tile], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
         const int last = old == a.split_k - 1;
         if (last) __hip_atomic_store(&a.counters[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         *s_flag = last;
@@ -297,8 +307,7 @@ struct Geometry {
 };
 
 // The stages of an output-split tile (WN x WM waves, each FN x FM
-// accumulators), shared by the one-tile-per-workgroup kernel and the
-// persistent one.
+// accumulators).
 template <class G>
 struct OutSplit {
     static constexpr int BN = G::BN, BM = G::BM, S = G::S, FN = G::FN, FM = G::FM, NW = G::NW;
@@ -398,13 +407,6 @@ struct OutSplit {
                 }
             }
         }
-    }
-
-    // The same for a tile given by its origin (the persistent kernel, whose
-    // slices belong to changing tiles).
-    static __device__ __forceinline__ void issue(const GemmArgs &a, int8_t *lds, uint32_t lds0, int wave, int lane,
-                                                 int tok0, int ch0, int s, int st) {
-        issue(a, cursor(a, wave, lane, tok0, ch0), lds, lds0, wave, lane, s, st);
     }
 
     // One k-step of the wave's FN x FM accumulators from ring slot st.
@@ -563,74 +565,6 @@ __global__ __launch_bounds__(64 * WN * WM) void k_gemm(GemmArgs a) {
             const int tok = tok0 + (wm * FM + j) * 16 + r0 + er;
             if (tok < a.m && ch_ok) emit_out(a, tok, ch, merge_partials(a, prsrc, tok, ch), sc);
         }
-}
-
-// ---------------------------------------------------------------------------
-// Persistent output-split variant for shapes with many output tiles: a fixed
-// grid of workgroups walks the tiles (workgroup w takes tiles w, w + grid, ...)
-// and streams the (tile, k-step) slices through one continuous ring, so the
-// first k-steps of the next tile are loading while the current tile's
-// epilogue runs.  The epilogue stages through the ring slot computed last:
-// nothing is loaded into it before the next iteration's barrier, which every
-// wave reaches only after its staging reads.  split_k must be 1.
-//
-// Store completions also count in the vector-memory counter.  The waits count
-// only loads issued after the awaited one; since loads complete in order,
-// extra stores in flight can only make a wait longer, never let it pass
-// early.
-template <int KIND, int WN, int WM, int FN, int FM, int NST>
-__global__ __launch_bounds__(64 * WN * WM) void k_gemm_ps(GemmArgs a) {
-    using G = Geometry<KIND, WN, WM, FN, FM, NST>;
-    using O = OutSplit<G>;
-    constexpr int BN = G::BN, BM = G::BM;
-    constexpr int R = G::RING;
-    static_assert(G::EPI <= G::SLOT && R >= 2, "the epilogue stages inside one ring slot");
-
-    __shared__ __attribute__((aligned(1024))) int8_t lds[G::LDSB];
-    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
-
-    const int lid = map_block(blockIdx.x, gridDim.x);
-    const int T = a.tiles_m * a.tiles_n;
-    const int G_ = (int)gridDim.x;
-    const int ntiles = lid < T ? (T - 1 - lid) / G_ + 1 : 0;
-    const int nq = ntiles * a.k_steps;  // (tile, k-step) pairs of this workgroup, in order
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wn = wave % WN, wm = wave / WN;
-
-    auto issue_pair = [&](int q) {
-        const int t = lid + (q / a.k_steps) * G_;
-        O::issue(a, lds, lds0, wave, lane, (t / a.tiles_n) * BM, (t % a.tiles_n) * BN, q % a.k_steps, q % R);
-    };
-
-    v4i acc[FN][FM];
-#pragma unroll
-    for (int i = 0; i < FN; ++i)
-#pragma unroll
-        for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
-
-#pragma unroll
-    for (int i = 0; i < R - 1; ++i)
-        if (i < nq) issue_pair(i);
-    for (int q = 0; q < nq; ++q) {
-        // pair q has landed; the slot computed in the previous iteration (or
-        // used there for staging) is free for pair q + R - 1
-        const int later = nq - 1 - q < R - 2 ? nq - 1 - q : R - 2;
-        wait_later_then_barrier<R - 2, G::DMA>(later);
-        if (q + R - 1 < nq) issue_pair(q + R - 1);
-        O::compute(lds, wn, wm, lane, q % R, acc);
-        if (q % a.k_steps == a.k_steps - 1) {
-            // every wave has read its operands from slot q % R: stage there
-            wait_then_barrier<63>();
-            const int t = lid + (q / a.k_steps) * G_;
-            O::store(a, lds + (q % R) * G::SLOT + wave * 16 * G::ROWB, lane, wn, wm, (t / a.tiles_n) * BM,
-                     (t % a.tiles_n) * BN, 0, acc);
-#pragma unroll
-            for (int i = 0; i < FN; ++i)
-#pragma unroll
-                for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
-        }
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -829,204 +763,6 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
     }
 }
 
-// ---------------------------------------------------------------------------
-// Row-stationary variant for shapes whose time goes into writing the output
-// (large token counts, short k).  The grid is a fixed number of workgroups;
-// each walks an equal, contiguous share of the output tiles in token-block
-// order.  While the token block stays the same, its X slice (all k-steps)
-// stays resident in LDS, so X is read once per workgroup instead of once per
-// output tile, and only the weight streams through a ring of k-step slots.
-// A fifth, producer wave issues every load and waits on their completion;
-// the four consumer waves only read LDS, run the matrix instructions and
-// store the outputs.  Because the consumers never wait on the vector-memory
-// counter, their output stores drain to HBM while the next tile computes.
-
-template <int KIND, int FN, int FM, int NST>
-__global__ __launch_bounds__(320) void k_gemm_rs(GemmArgs a) {
-    constexpr int BN = 2 * FN * 16;
-    constexpr int BM = 2 * FM * 16;
-    constexpr bool kSparse = KIND != NM_KIND_DENSE;
-    constexpr int S = KIND == NM_KIND_SP42X2 ? 2 : 1;
-    constexpr int WVB = kSparse ? (BN / 16) * S * kVBlock : BN * 128;
-    constexpr int WMB = kSparse ? (BN / 16) * S * kMBlock : 0;
-    constexpr int WSLOT = WVB + WMB;
-    constexpr int WI = kSparse ? (BN / 16) * S * 2 : BN / 8;  // producer loads per weight slot
-    constexpr int CPR = FN * 4;
-    constexpr int RPI = 64 / CPR;
-    constexpr int ROWB = FN * 64 + 16;
-    constexpr int R = NST;
-    static_assert(64 % CPR == 0 && R >= 2, "tile shape");
-
-    extern __shared__ __attribute__((aligned(1024))) int8_t lds[];
-    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
-    const int XBB = a.k_steps * BM * 128;            // resident X block
-    int8_t *ringp = lds + XBB;
-    const uint32_t ring = lds0 + XBB;
-    int8_t *stage_base = ringp + R * WSLOT;
-
-    const int T = a.tiles_m * a.tiles_n;
-    const int t_begin = (int)((int64_t)blockIdx.x * T / gridDim.x);
-    const int t_end = (int)((int64_t)(blockIdx.x + 1) * T / gridDim.x);
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const bool producer = wave == 4;
-    const int wn = wave & 1, wm = (wave >> 1) & 1;
-    const int lg = lane >> 4;
-
-    // weight slice of (tile tn, k-step s) into ring slot st (producer)
-    auto issue_w = [&](int tn, int s, int st) {
-        const uint32_t slot = ring + st * WSLOT;
-        if constexpr (kSparse) {
-#pragma unroll
-            for (int bl = 0; bl < (BN / 16) * S; ++bl) {
-                int f = tn * (BN / 16) + bl / S;
-                f = f < a.n_frags ? f : a.n_frags - 1;
-                const size_t b = ((size_t)f * a.k_steps + s) * S + bl % S;
-                dma16(a.A + b * kVBlock + lane * 16, slot + bl * kVBlock);
-                dma4(a.meta + b * kMBlock + lane * 4, slot + WVB + bl * kMBlock);
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < BN / 8; ++j) {
-                const int r = 8 * j + (lane >> 3);
-                const int c = (lane & 7) ^ (r & 7);
-                const int row = tn * BN + r < a.n ? tn * BN + r : a.n - 1;
-                const int kk = s * 128 + c * 16;
-                if (s * 128 + 128 <= a.k) {
-                    dma16(a.A + (size_t)row * a.k + kk, slot + j * 1024);
-                } else {  // tail k-step of a dense weight: zeros past k
-                    v4i v = v4i{0, 0, 0, 0};
-                    if (kk < a.k) v = *(const v4i *)(a.A + (size_t)row * a.k + kk);
-                    *(v4i *)(ringp + st * WSLOT + j * 1024 + lane * 16) = v;
-                }
-            }
-        }
-    };
-
-    v4i acc[FN][FM];
-    auto zero_acc = [&]() {
-#pragma unroll
-        for (int i = 0; i < FN; ++i)
-#pragma unroll
-            for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
-    };
-    auto compute = [&](int st, int s) {
-        const int8_t *xs = lds + s * BM * 128;
-        const int8_t *ws = ringp + st * WSLOT;
-        if constexpr (kSparse) {
-            v4i av[FN][S];
-            int ai[FN][S];
-#pragma unroll
-            for (int i = 0; i < FN; ++i)
-#pragma unroll
-                for (int q = 0; q < S; ++q) {
-                    const int bl = (wn * FN + i) * S + q;
-                    av[i][q] = *(const v4i *)(ws + bl * kVBlock + lane * 16);
-                    ai[i][q] = *(const int *)(ws + WVB + bl * kMBlock + lane * 4);
-                }
-#pragma unroll
-            for (int j = 0; j < FM; ++j) {
-                const int r = (wm * FM + j) * 16 + (lane & 15);
-                const int8_t *rowp = xs + r * 128;
-                const v4i blo = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
-                const v4i bhi = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
-                const v8i b = {blo[0], blo[1], blo[2], blo[3], bhi[0], bhi[1], bhi[2], bhi[3]};
-#pragma unroll
-                for (int i = 0; i < FN; ++i)
-#pragma unroll
-                    for (int q = 0; q < S; ++q)
-                        acc[i][j] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(av[i][q], b, acc[i][j], ai[i][q], 0, 0);
-            }
-        } else {
-            v4i alo[FN], ahi[FN];
-#pragma unroll
-            for (int i = 0; i < FN; ++i) {
-                const int r = (wn * FN + i) * 16 + (lane & 15);
-                const int8_t *rowp = ws + r * 128;
-                alo[i] = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
-                ahi[i] = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
-            }
-#pragma unroll
-            for (int j = 0; j < FM; ++j) {
-                const int r = (wm * FM + j) * 16 + (lane & 15);
-                const int8_t *rowp = xs + r * 128;
-                const v4i blo = *(const v4i *)(rowp + ((lg ^ (r & 7)) << 4));
-                const v4i bhi = *(const v4i *)(rowp + (((lg + 4) ^ (r & 7)) << 4));
-#pragma unroll
-                for (int i = 0; i < FN; ++i) {
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(alo[i], blo, acc[i][j], 0, 0, 0);
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ahi[i], bhi, acc[i][j], 0, 0, 0);
-                }
-            }
-        }
-    };
-    // consumer epilogue of one tile: stage 16 tokens at a time, store rows
-    int8_t *stg = stage_base + (wave & 3) * 16 * ROWB;
-    const int ec = lane % CPR, er = lane / CPR;
-    auto epilogue = [&](int tm, int tn) {
-        const int ch = tn * BN + wn * FN * 16 + ec * 4;
-        const bool ch_ok = ch < a.n;
-        const EpiScale sc = load_scale(a, ch);
-#pragma unroll
-        for (int j = 0; j < FM; ++j) {
-#pragma unroll
-            for (int i = 0; i < FN; ++i)
-                *(v4i *)(stg + (lane & 15) * ROWB + (i * 16 + 4 * lg) * 4) = acc[i][j];
-#pragma unroll
-            for (int r0 = 0; r0 < 16; r0 += RPI) {
-                const int t = r0 + er;
-                const v4i v = *(const v4i *)(stg + t * ROWB + ec * 16);
-                const int tok = tm * BM + (wm * FM + j) * 16 + t;
-                if (tok < a.m && ch_ok) emit_out(a, tok, ch, v, sc);
-            }
-        }
-    };
-
-    for (int ta = t_begin; ta < t_end;) {
-        // one phase: the tiles of one token block
-        const int tm = ta / a.tiles_n;
-        const int tb = (tm + 1) * a.tiles_n < t_end ? (tm + 1) * a.tiles_n : t_end;
-        const int nq = (tb - ta) * a.k_steps;  // (tile, k-step) pairs of the phase
-        if (producer) {
-            const uint32_t xb = lds0;
-            for (int s = 0; s < a.k_steps; ++s)
-#pragma unroll
-                for (int j = 0; j < BM / 8; ++j) {
-                    const int r = 8 * j + (lane >> 3);
-                    const int c = (lane & 7) ^ (r & 7);
-                    const int tok = tm * BM + r < a.m ? tm * BM + r : a.m - 1;
-                    const int kk = s * 128 + c * 16 < a.k ? s * 128 + c * 16 : a.k - 16;
-                    dma16(a.X + (size_t)tok * a.k + kk, xb + s * BM * 128 + j * 1024);
-                }
-#pragma unroll
-            for (int i = 0; i < R - 1; ++i)
-                if (i < nq) issue_w((ta + i / a.k_steps) % a.tiles_n, i % a.k_steps, i);
-            for (int q = 0; q < nq; ++q) {
-                // slot q (and, before it, the X block) has landed; the
-                // consumers are done with slot q-1, which is refilled next
-                const int later = nq - 1 - q < R - 2 ? nq - 1 - q : R - 2;
-                wait_later_then_barrier<R - 2, WI>(later);
-                const int qn = q + R - 1;
-                if (qn < nq) issue_w((ta + qn / a.k_steps) % a.tiles_n, qn % a.k_steps, qn % R);
-            }
-            wait_then_barrier<63>();  // end of phase: X block and ring are free again
-        } else {
-            zero_acc();
-            for (int q = 0; q < nq; ++q) {
-                wait_then_barrier<63>();  // own LDS reads done; slot q published
-                const int s = q % a.k_steps;
-                compute(q % R, s);
-                if (s == a.k_steps - 1) {
-                    epilogue(tm, (ta + q / a.k_steps) % a.tiles_n);
-                    zero_acc();
-                }
-            }
-            wait_then_barrier<63>();
-        }
-        ta = tb;
-    }
-}
-
 __global__ void k_zero(int *p, size_t n4, unsigned char *tail, int tail_bytes) {
     const size_t stride = (size_t)gridDim.x * blockDim.x;
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) p[i] = 0;
@@ -1036,22 +772,8 @@ __global__ void k_zero(int *p, size_t n4, unsigned char *tail, int tail_bytes) {
 template <int KIND, int T>
 int launch_one(const GemmArgs &args, int grid, void *stream) {
     constexpr TileCfg t = kTiles[T];
-    if constexpr (t.layout == kRowStat) {
-        const size_t bytes = rowstat_lds(KIND, t, args.k_steps).total;
-        static bool attr_set = false;  // the attribute is per kernel; setting it twice is harmless
-        if (!attr_set) {
-            hipError_t e = hipFuncSetAttribute((const void *)k_gemm_rs<KIND, t.fn, t.fm, t.nst>,
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsPerCu);
-            if (e != hipSuccess) return (int)e;
-            attr_set = true;
-        }
-        hipLaunchKernelGGL((k_gemm_rs<KIND, t.fn, t.fm, t.nst>), dim3(grid), dim3(320), bytes, (hipStream_t)stream,
-                           args);
-    } else if constexpr (t.layout == kKSliced)
+    if constexpr (t.layout == kKSliced)
         hipLaunchKernelGGL((k_gemm_ks<KIND, t.fn, t.fm, t.nst>), dim3(grid), dim3(kThreads), 0,
-                           (hipStream_t)stream, args);
-    else if constexpr (t.layout == kPersist)
-        hipLaunchKernelGGL((k_gemm_ps<KIND, t.wn, t.wm, t.fn, t.fm, t.nst>), dim3(grid), dim3(64 * t.wn * t.wm), 0,
                            (hipStream_t)stream, args);
     else
         hipLaunchKernelGGL((k_gemm<KIND, t.wn, t.wm, t.fn, t.fm, t.nst>), dim3(grid), dim3(64 * t.wn * t.wm), 0,

@@ -62,24 +62,6 @@ nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *p) {
     p->tile_n = t.tile_n();
     p->tile_m = t.tile_m();
     const int64_t tiles = ceil_div(n, p->tile_n) * ceil_div(m > 0 ? m : 1, p->tile_m);
-    if (t.layout == kRowStat) {
-        // a fixed grid of workgroups, each walking an equal share of the tiles
-        if (p->split_k != 1) return NM_ERR_ARG;
-        const RowStatLds L = rowstat_lds(kind, t, k_steps);
-        if (L.total > kLdsPerCu) return NM_ERR_SHAPE;
-        const int64_t per_cu = (int64_t)(kLdsPerCu / L.total);
-        const int64_t slots = (int64_t)device_cu_count() * per_cu;
-        p->grid = (int)(tiles < slots ? tiles : slots);
-        return NM_OK;
-    }
-    if (t.layout == kPersist) {
-        // a fixed grid: as many workgroups as fit on the chip at once
-        if (p->split_k != 1) return NM_ERR_ARG;
-        const int64_t per_cu = (int64_t)(kLdsPerCu / outsplit_lds(kind, t));
-        const int64_t slots = (int64_t)device_cu_count() * (per_cu > 0 ? per_cu : 1);
-        p->grid = (int)(tiles < slots ? tiles : slots);
-        return NM_OK;
-    }
     const int64_t grid = tiles * p->split_k;
     if (grid > 0x7fffffff) return NM_ERR_SHAPE;
     if (p->split_k > 1 && tiles > kMaxSplitTiles) return NM_ERR_ARG;
@@ -90,9 +72,9 @@ nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *p) {
 }
 
 // Tile indices used by the rules below (see kTiles).
+constexpr int kT128x128r2 = 0, kT128x64r2 = 1, kT64x128r2 = 2, kT64x64r2 = 3, kT256x256w8 = 4;
+constexpr int kT128x32r2 = 5, kT128x128w8 = 6;
 constexpr int kT32x64ks = 8, kT64x32ks = 9, kT32x32ks = 10;
-constexpr int kT128x128r2 = 16, kT128x64r2 = 17, kT64x128r2 = 18, kT64x64r2 = 19, kT256x256w8 = 20;
-constexpr int kT128x32r2 = 22, kT128x128w8 = 23;
 
 static int64_t tiles_of(int t, int m, int n) {
     return ceil_div(n, kTiles[t].tile_n()) * ceil_div(m, kTiles[t].tile_m());

@@ -1,8 +1,13 @@
-// Matrix-instruction rate loop and single-instruction layout probe (measurement
-// and test aids, declared in nmprobe.h).
+// Measurement and test aids declared in nmprobe.h: the matrix-instruction
+// rate loop, the single-instruction layout probe and the store-only run of a
+// GEMM plan.  Built as libnmprobe.so, apart from the method's library, which
+// it links for the GEMM kernels that the store-only probe launches.
 #include <hip/hip_runtime.h>
 
-#include "../../include/nmprobe.h"
+#include <cstdint>
+
+#include "../nmspmm_internal.h"
+#include "../../../include/nmprobe.h"
 
 namespace {
 
@@ -109,4 +114,53 @@ extern "C" nm_status nm_probe_mfma_rate(int kind, const int32_t *operands, int i
     else
         return NM_ERR_ARG;
     return hipGetLastError() == hipSuccess ? NM_OK : NM_ERR_HIP;
+}
+
+using namespace nmspmm;
+
+namespace {
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+}  // namespace
+
+extern "C" nm_status nm_probe_store_only(const nm_plan *plan, int m, int n, const nm_outputs *out, void *stream) {
+    if (!plan || !out) return NM_ERR_ARG;
+    if (m < 0 || n < 4 || n % 4 != 0) return NM_ERR_SHAPE;
+    if (m == 0) return NM_OK;
+    if ((int64_t)m * n >= ((int64_t)1 << 29)) return NM_ERR_SHAPE;
+    const nm_outputs o = *out;
+    if (!o.y && !o.yh && !o.yq) return NM_ERR_ARG;
+    if ((o.yh && !o.scale) || (o.yq && !o.qscale)) return NM_ERR_ARG;
+    if ((o.y && !aligned16(o.y)) || (o.yh && !aligned16(o.yh)) || (o.yh && !aligned16(o.scale)) ||
+        (o.yq && !aligned16(o.yq)) || (o.yq && !aligned16(o.qscale)))
+        return NM_ERR_ARG;
+    if (plan->tile < 0 || plan->tile >= kNumTiles || kTiles[plan->tile].layout != kOutSplit || plan->split_k != 1)
+        return NM_ERR_ARG;
+    if (plan->kind != NM_KIND_SP42 && plan->kind != NM_KIND_SP42X2 && plan->kind != NM_KIND_DENSE) return NM_ERR_ARG;
+    nm_plan p = *plan;
+    nm_status st = complete_plan(p.kind, m, n, 1, &p);
+    if (st != NM_OK) return st;
+    // Zero k-steps: the kernel issues no operand loads and no matrix
+    // instructions; the epilogue stores the zero accumulators.  No operand
+    // pointer is read.
+    GemmArgs a;
+    a.X = nullptr;
+    a.A = nullptr;
+    a.meta = nullptr;
+    a.Y = o.y;
+    a.Yh = o.yh;
+    a.scale = o.scale;
+    a.Yq = o.yq;
+    a.qscale = o.qscale;
+    a.counters = nullptr;
+    a.partials = nullptr;
+    a.m = m;
+    a.n = n;
+    a.k = 128;
+    a.k_steps = 0;
+    a.n_frags = (n + kFragRows - 1) / kFragRows;
+    a.tiles_n = (n + p.tile_n - 1) / p.tile_n;
+    a.tiles_m = (m + p.tile_m - 1) / p.tile_m;
+    a.split_k = 1;
+    a.group_rows = 0;
+    return launch_gemm(p.kind, p.tile, a, p.grid, stream) == 0 ? NM_OK : NM_ERR_HIP;
 }

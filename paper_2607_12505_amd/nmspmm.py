@@ -30,9 +30,8 @@ EXPORTED = (
     "nm_status_string", "nm_compress_size", "nm_compress", "nm_decompress", "nm_num_tiles",
     "nm_tile_info", "nm_plan_kernel_name", "nm_spmm_plan", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
     "nm_spmm", "nm_spmm_ex", "nm_gemm_i8_dense", "nm_gemm_i8_dense_ex", "nm_spmm_out", "nm_gemm_i8_dense_out",
-    "nm_quantize_f16", "nm_probe_mfma_rate", "nm_probe_mfma_layout", "nm_wall_clock_khz", "nm_probe_store_only",
+    "nm_quantize_f16",
 )
-NM_PROBE_WORDS = 4096
 
 
 class NmDesc(ctypes.Structure):
@@ -105,10 +104,6 @@ def lib() -> ctypes.CDLL:
             "nm_spmm_out": ([vp, i32, vp, vp, pd, ctypes.POINTER(NmOutputs), vp, sz, vp, pp], i32),
             "nm_gemm_i8_dense_out": ([vp, i32, vp, i32, i32, ctypes.POINTER(NmOutputs), vp, sz, vp, pp], i32),
             "nm_quantize_f16": ([vp, ctypes.c_int64, ctypes.c_float, vp, vp], i32),
-            "nm_probe_mfma_rate": ([i32, vp, i32, i32, vp, vp, vp], i32),
-            "nm_wall_clock_khz": ([ctypes.POINTER(ctypes.c_int32)], i32),
-            "nm_probe_mfma_layout": ([i32, vp, vp, vp, vp, vp], i32),
-            "nm_probe_store_only": ([pp, i32, i32, ctypes.POINTER(NmOutputs), vp], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -456,50 +451,6 @@ def quantize_f16(x, inv_scale: float, xq=None, stream=None):
     _check(lib().nm_quantize_f16(_ptr(x), x.numel(), float(inv_scale), _ptr(xq), _stream(stream)),
            "nm_quantize_f16")
     return xq
-
-
-def probe_mfma_rate(kind: int, operands, iters: int, out, ticks=None, stream=None):
-    """nm_probe_mfma_rate: launches the matrix-instruction rate loop (nmprobe.h).
-
-    operands: int32 device tensor of NM_PROBE_WORDS words; out: int32 device
-    tensor whose size (a multiple of 256) sets the number of workgroups;
-    ticks: optional int64 device tensor of 2 words per workgroup."""
-    wgs = out.numel() // 256
-    if operands.numel() < NM_PROBE_WORDS or out.numel() % 256 or (ticks is not None and ticks.numel() < 2 * wgs):
-        raise ValueError("operands needs NM_PROBE_WORDS words, out a multiple of 256, ticks 2 per workgroup")
-    _check(lib().nm_probe_mfma_rate(int(kind), _ptr(operands), int(iters), wgs, _ptr(out), _ptr(ticks),
-                                    _stream(stream)), "nm_probe_mfma_rate")
-
-
-def wall_clock_khz() -> int:
-    """nm_wall_clock_khz: rate of the device's real-time counter."""
-    khz = ctypes.c_int32(0)
-    _check(lib().nm_wall_clock_khz(ctypes.byref(khz)), "nm_wall_clock_khz")
-    return int(khz.value)
-
-
-def probe_mfma_layout(kind: int, a, b, pos, d, stream=None):
-    """nm_probe_mfma_layout: one matrix instruction on one wave (nmprobe.h).
-
-    a, d: int32 device tensors of 256 words; b: 512 words (NM_KIND_SP42) or
-    256 (NM_KIND_DENSE); pos: 64 words (NM_KIND_SP42) or None."""
-    nb = 512 if kind == NM_KIND_SP42 else 256
-    if a.numel() < 256 or d.numel() < 256 or b.numel() < nb or (kind == NM_KIND_SP42 and
-                                                                 (pos is None or pos.numel() < 64)):
-        raise ValueError("operand buffers smaller than the instruction needs")
-    _check(lib().nm_probe_mfma_layout(int(kind), _ptr(a), _ptr(b), _ptr(pos), _ptr(d), _stream(stream)),
-           "nm_probe_mfma_layout")
-
-
-def probe_store_only(plan: NmPlan, m: int, n: int, Y=None, scale=None, Yh=None, Yq=None, qscale=None, stream=None):
-    """nm_probe_store_only: the plan's kernel with the reduction skipped, so
-    only its epilogue stores run (nmprobe.h); the outputs receive zeros."""
-    torch = _torch()
-    _check_outputs(torch, m, n, Y, scale, Yh, Yq, qscale)
-    _on_device((("Y", Y), ("Yh", Yh), ("Yq", Yq), ("scale", scale), ("qscale", qscale)))
-    o = _outputs(Y, scale, Yh, Yq, qscale)
-    _check(lib().nm_probe_store_only(ctypes.byref(plan), int(m), int(n), ctypes.byref(o), _stream(stream)),
-           "nm_probe_store_only")
 
 
 def workspace_init(ws, stream=None):

@@ -5,7 +5,7 @@ import glob
 import os
 import re
 
-from paper_2607_12505_amd import nmsearch, nmspmm
+from paper_2607_12505_amd import nmprobe, nmsearch, nmspmm
 
 HEADERS = sorted(glob.glob(os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
                                         "*.h")))
@@ -19,15 +19,32 @@ def declared_functions():
     return sorted(names)
 
 
+def declared_in(header):
+    src = re.sub(r"/\*.*?\*/", "", open(os.path.join(os.path.dirname(HEADERS[0]), header)).read(), flags=re.S)
+    return set(re.findall(r"\b(nm_[a-z0-9_]+)\s*\(", src))
+
+
 def test_header_declares_the_binding_names():
     assert len(HEADERS) == 3
-    assert declared_functions() == sorted(nmspmm.EXPORTED + nmsearch.EXPORTED)
+    assert declared_functions() == sorted(nmspmm.EXPORTED + nmsearch.EXPORTED + nmprobe.EXPORTED)
+    assert declared_in("nmprobe.h") == set(nmprobe.EXPORTED)
 
 
 def test_library_exports_every_declared_symbol():
     lib = nmspmm.lib()
-    for name in declared_functions():
+    for name in nmspmm.EXPORTED + nmsearch.EXPORTED:
         assert hasattr(lib, name), name
+    probe = nmprobe.lib()
+    for name in nmprobe.EXPORTED:
+        assert hasattr(probe, name), name
+
+
+def test_method_library_carries_no_probe():
+    # the measurement aids live in libnmprobe.so only
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", nmspmm.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    assert "nm_probe" not in out and "nm_wall_clock_khz" not in out
 
 
 def test_one_hip_runtime_per_process():
@@ -77,29 +94,29 @@ def test_host_side_argument_checks_need_no_gpu():
         nmspmm.NM_ERR_ARG
     assert L.nm_quantize_f16(fake, -1, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_SHAPE
     assert L.nm_quantize_f16(misaligned, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, nul, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42X2, fake, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 0, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 1, 0, fake, nul, nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_wall_clock_khz(None) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, nul, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, fake, fake, nul, fake, nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42X2, fake, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
-    ok_plan = nmspmm.make_plan(nmspmm.NM_KIND_SP42, 16, 1)
+    P = nmprobe.lib()
+    assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, nul, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
+    assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42X2, fake, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
+    assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 0, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
+    assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 1, 0, fake, nul, nul) == nmspmm.NM_ERR_ARG
+    assert P.nm_wall_clock_khz(None) == nmspmm.NM_ERR_ARG
+    assert P.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, nul, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
+    assert P.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, fake, fake, nul, fake, nul) == nmspmm.NM_ERR_ARG
+    assert P.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42X2, fake, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
+    ok_plan = nmspmm.make_plan(nmspmm.NM_KIND_SP42, 0, 1)
     y_only = nmspmm.NmOutputs(fake.value, None, None, None, None)
-    assert L.nm_probe_store_only(None, 64, 64, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_ARG
-    assert L.nm_probe_store_only(ctypes.byref(ok_plan), 64, 66, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_SHAPE
-    assert L.nm_probe_store_only(ctypes.byref(ok_plan), -1, 64, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_SHAPE
-    assert L.nm_probe_store_only(ctypes.byref(ok_plan), 0, 64, ctypes.byref(y_only), nul) == nmspmm.NM_OK
+    assert P.nm_probe_store_only(None, 64, 64, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_ARG
+    assert P.nm_probe_store_only(ctypes.byref(ok_plan), 64, 66, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_SHAPE
+    assert P.nm_probe_store_only(ctypes.byref(ok_plan), -1, 64, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_SHAPE
+    assert P.nm_probe_store_only(ctypes.byref(ok_plan), 0, 64, ctypes.byref(y_only), nul) == nmspmm.NM_OK
     no_out = nmspmm.NmOutputs(None, None, None, None, None)
-    assert L.nm_probe_store_only(ctypes.byref(ok_plan), 64, 64, ctypes.byref(no_out), nul) == nmspmm.NM_ERR_ARG
+    assert P.nm_probe_store_only(ctypes.byref(ok_plan), 64, 64, ctypes.byref(no_out), nul) == nmspmm.NM_ERR_ARG
     fp16_no_scale = nmspmm.NmOutputs(None, fake.value, None, None, None)
-    assert L.nm_probe_store_only(ctypes.byref(ok_plan), 64, 64, ctypes.byref(fp16_no_scale), nul) == nmspmm.NM_ERR_ARG
+    assert P.nm_probe_store_only(ctypes.byref(ok_plan), 64, 64, ctypes.byref(fp16_no_scale), nul) == nmspmm.NM_ERR_ARG
     for bad in (nmspmm.make_plan(nmspmm.NM_KIND_SP42, 10, 1),      # k-sliced layout
-                nmspmm.make_plan(nmspmm.NM_KIND_SP42, 11, 1),      # row-stationary layout
-                nmspmm.make_plan(nmspmm.NM_KIND_SP42, 16, 2),      # split_k != 1
-                nmspmm.make_plan(7, 16, 1)):                        # unknown kind
-        assert L.nm_probe_store_only(ctypes.byref(bad), 64, 64, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_ARG
+                nmspmm.make_plan(nmspmm.NM_KIND_SP42, 0, 2),       # split_k != 1
+                nmspmm.make_plan(7, 0, 1)):                         # unknown kind
+        assert P.nm_probe_store_only(ctypes.byref(bad), 64, 64, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_ARG
 
 
 def _gpu_visible():
@@ -125,10 +142,11 @@ def test_launch_failures_report_nm_err_hip():
     assert L.nm_gemm_i8_dense_ex(fake, 64, fake, 64, 128, fake, nul, nul, nul, 0, nul, None) == nmspmm.NM_ERR_HIP
     assert L.nm_quantize_f16(fake, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_HIP
     assert L.nm_workspace_init(fake, 64, nul) == nmspmm.NM_ERR_HIP
-    assert L.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, fake, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_HIP
+    P = nmprobe.lib()
+    assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, fake, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_HIP
     khz = ctypes.c_int32(0)
-    assert L.nm_wall_clock_khz(ctypes.byref(khz)) == nmspmm.NM_ERR_HIP
-    assert L.nm_probe_mfma_layout(nmspmm.NM_KIND_DENSE, fake, fake, nul, fake, nul) == nmspmm.NM_ERR_HIP
+    assert P.nm_wall_clock_khz(ctypes.byref(khz)) == nmspmm.NM_ERR_HIP
+    assert P.nm_probe_mfma_layout(nmspmm.NM_KIND_DENSE, fake, fake, nul, fake, nul) == nmspmm.NM_ERR_HIP
     y_only = nmspmm.NmOutputs(fake.value, None, None, None, None)
-    assert L.nm_probe_store_only(ctypes.byref(nmspmm.make_plan(nmspmm.NM_KIND_SP42, 16, 1)), 64, 64,
+    assert P.nm_probe_store_only(ctypes.byref(nmspmm.make_plan(nmspmm.NM_KIND_SP42, 0, 1)), 64, 64,
                                  ctypes.byref(y_only), nul) == nmspmm.NM_ERR_HIP

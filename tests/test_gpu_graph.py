@@ -45,7 +45,7 @@ def test_captured_layer_replays_bit_exactly():
     Ws = wl.random_nm(n, k, 2, 4, rng, full=True)
     Xsd = torch.from_numpy(Xs).cuda()
     dws = nmspmm.DeviceWeight.from_packed(nmspmm.compress(Ws, 2, 4))
-    plan = nmspmm.make_plan(nmspmm.NM_KIND_SP42, 6, 4)
+    plan = nmspmm.make_plan(nmspmm.NM_KIND_SP42, 3, 4)
     ws = torch.empty(nmspmm.workspace_size(plan, m, n), dtype=torch.uint8, device="cuda")
     Ys = torch.empty((m, n), dtype=torch.int32, device="cuda")
 

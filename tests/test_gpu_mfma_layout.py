@@ -18,7 +18,7 @@ import itertools
 import numpy as np
 import pytest
 
-from paper_2607_12505_amd import nmspmm
+from paper_2607_12505_amd import nmprobe, nmspmm
 
 pytestmark = pytest.mark.gpu
 
@@ -34,7 +34,7 @@ def run(kind, a_bytes, b_bytes, pos_words=None):
     a, b = dev(words(a_bytes)), dev(words(b_bytes))
     pos = dev(pos_words.astype(np.int32)) if pos_words is not None else None
     d = torch.empty(256, dtype=torch.int32, device="cuda")
-    nmspmm.probe_mfma_layout(kind, a, b, pos, d)
+    nmprobe.probe_mfma_layout(kind, a, b, pos, d)
     torch.cuda.synchronize()
     return d.cpu().numpy().reshape(64, 4)
 

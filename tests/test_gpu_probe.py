@@ -3,7 +3,7 @@ the C ABI for both instruction kinds, is deterministic, and bench.py turns its
 timing into a positive rate."""
 import pytest
 
-from paper_2607_12505_amd import nmspmm
+from paper_2607_12505_amd import nmprobe, nmspmm
 
 pytestmark = pytest.mark.gpu
 
@@ -11,32 +11,32 @@ pytestmark = pytest.mark.gpu
 def test_rate_loop_runs_and_is_deterministic():
     import torch
     g = torch.Generator().manual_seed(5)
-    tab = torch.randint(-2 ** 31, 2 ** 31, (nmspmm.NM_PROBE_WORDS,), generator=g, dtype=torch.int64)
+    tab = torch.randint(-2 ** 31, 2 ** 31, (nmprobe.NM_PROBE_WORDS,), generator=g, dtype=torch.int64)
     tab = tab.to(torch.int32).cuda()
     for kind in (nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_DENSE):
         out1 = torch.empty(8 * 256, dtype=torch.int32, device="cuda")
         out2 = torch.empty_like(out1)
-        nmspmm.probe_mfma_rate(kind, tab, 3, out1)
-        nmspmm.probe_mfma_rate(kind, tab, 3, out2)
+        nmprobe.probe_mfma_rate(kind, tab, 3, out1)
+        nmprobe.probe_mfma_rate(kind, tab, 3, out2)
         torch.cuda.synchronize()
         assert torch.equal(out1, out2)
         # every workgroup runs the same loop on the same table
         assert torch.equal(out1[:256], out1[256:512])
     zero = torch.zeros_like(tab)
     out = torch.empty(256, dtype=torch.int32, device="cuda")
-    nmspmm.probe_mfma_rate(nmspmm.NM_KIND_SP42, zero, 2, out)
+    nmprobe.probe_mfma_rate(nmspmm.NM_KIND_SP42, zero, 2, out)
     torch.cuda.synchronize()
     assert int(out.abs().sum()) == 0
 
 
 def test_loop_ticks_give_a_plausible_clock():
     import torch
-    khz = nmspmm.wall_clock_khz()
+    khz = nmprobe.wall_clock_khz()
     assert khz > 0
-    tab = torch.zeros(nmspmm.NM_PROBE_WORDS, dtype=torch.int32, device="cuda")
+    tab = torch.zeros(nmprobe.NM_PROBE_WORDS, dtype=torch.int32, device="cuda")
     out = torch.empty(4 * 256, dtype=torch.int32, device="cuda")
     ticks = torch.zeros(8, dtype=torch.int64, device="cuda")
-    nmspmm.probe_mfma_rate(nmspmm.NM_KIND_DENSE, tab, 2000, out, ticks)
+    nmprobe.probe_mfma_rate(nmspmm.NM_KIND_DENSE, tab, 2000, out, ticks)
     torch.cuda.synchronize()
     t = ticks.cpu().numpy().reshape(-1, 2)
     assert (t > 0).all()
@@ -55,8 +55,9 @@ def test_bench_reports_positive_rates():
 
 @pytest.mark.parametrize("m,n", [(1000, 260), (12608, 1152), (33, 4)])
 def test_store_only_probe_writes_zeros_exactly_in_the_outputs(m, n):
-    # every output-split tile of all three kinds, on ragged shapes: the probe
-    # writes the empty-sum values into [m x n] and nothing past it
+    # every output-split tile of all three kinds, on ragged shapes, with and
+    # without the multiplier arrays: the probe writes the empty-sum values into
+    # [m x n] and nothing past it
     import torch
     bigY = torch.full((m * n + 4096,), 7, dtype=torch.int32, device="cuda")
     bigH = torch.full((m * n + 4096,), 7, dtype=torch.int16, device="cuda")
@@ -65,15 +66,19 @@ def test_store_only_probe_writes_zeros_exactly_in_the_outputs(m, n):
     Y, Yh, Yq = bigY[:m * n].view(m, n), bigH[:m * n].view(m, n), bigQ[:m * n].view(m, n)
     for kind in (nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_SP42X2, nmspmm.NM_KIND_DENSE):
         for tile in range(nmspmm.num_tiles()):
-            plan = nmspmm.make_plan(kind, tile, 1)
-            try:
-                nmspmm.probe_store_only(plan, m, n, Y=Y, scale=scale, Yh=Yh, Yq=Yq, qscale=scale)
-            except nmspmm.NmError as e:
-                assert e.status == nmspmm.NM_ERR_ARG     # not an output-split layout
-                continue
-            torch.cuda.synchronize()
-            assert not Y.any() and not Yh.any() and not Yq.any(), (kind, tile)
-            assert (bigY[m * n:] == 7).all() and (bigH[m * n:] == 7).all() and (bigQ[m * n:] == 7).all()
-            Y.fill_(7)
-            Yh.fill_(7)
-            Yq.fill_(7)
+            for with_scales in (True, False):
+                plan = nmspmm.make_plan(kind, tile, 1)
+                outs = dict(Y=Y, scale=scale, Yh=Yh, Yq=Yq, qscale=scale) if with_scales else dict(Y=Y)
+                try:
+                    nmprobe.probe_store_only(plan, m, n, **outs)
+                except nmspmm.NmError as e:
+                    assert e.status == nmspmm.NM_ERR_ARG     # not an output-split layout
+                    break
+                torch.cuda.synchronize()
+                assert not Y.any(), (kind, tile)
+                if with_scales:
+                    assert not Yh.any() and not Yq.any(), (kind, tile)
+                assert (bigY[m * n:] == 7).all() and (bigH[m * n:] == 7).all() and (bigQ[m * n:] == 7).all()
+                Y.fill_(7)
+                Yh.fill_(7)
+                Yq.fill_(7)

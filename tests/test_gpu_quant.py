@@ -87,7 +87,7 @@ def qscales(ref, rng):
     return q
 
 
-PLANS = [None, (2, 1), (7, 1), (11, 1), (6, 2), (10, 2)]
+PLANS = [None, (0, 1), (7, 1), (6, 1), (4, 1), (3, 2), (10, 2)]
 
 
 @pytest.mark.parametrize("kind", ["2:4", "4:8", "dense"])
