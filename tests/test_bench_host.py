@@ -1,6 +1,7 @@
-"""Host-side arithmetic of bench.py (no GPU): the algorithmic byte counts the
-roofline uses, the profiler-summary scaling of FETCH_SIZE / WRITE_SIZE by the
-calibration copy, and the planner-evaluation report."""
+"""Host-side arithmetic of bench.py and bench_experiments.py (no GPU): the
+algorithmic byte counts the roofline uses, the ABBA ratio statistics, the
+profiler-summary scaling of FETCH_SIZE / WRITE_SIZE by the calibration copy,
+and the planner-evaluation report."""
 import csv
 import json
 import os
@@ -12,6 +13,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 import bench  # noqa: E402
+import bench_experiments  # noqa: E402
 from paper_2607_12505_amd import workloads as wl  # noqa: E402
 
 
@@ -25,6 +27,16 @@ def test_algorithmic_bytes_by_hand():
     g = wl.Gemm("x", 100, 256, 64, 1, 8)
     assert bench.algorithmic_bytes(g, True, False) == 100 * 256 + 64 * 256 // 8 + 64 * 32 * 3 // 8 + 4 * 100 * 64
     assert bench.algorithmic_bytes(g, True, False, sparse=False) == 100 * 256 + 64 * 256 + 4 * 100 * 64
+
+
+def test_ratio_stats_by_hand():
+    import numpy as np
+    # two ABBA rounds: A legs (1, 1) and (2, 2), B legs (2, 2) and (2, 2)
+    ta = np.array([1.0, 1.0, 2.0, 2.0])
+    tb = np.array([2.0, 2.0, 2.0, 2.0])
+    r = bench.ratio_stats(ta, tb)
+    assert r["ratio"] == round(8.0 / 6.0, 4) and r["rounds"] == 2
+    assert r["round_min"] == 1.0 and r["round_max"] == 2.0
 
 
 def _write_csv(path, header, rows):
@@ -59,7 +71,7 @@ def test_rocprof_summary_scales_counters_by_the_calibration_copy(tmp_path):
     md = tmp_path / "summary.md"
     traffic = os.path.join(ROOT, "profiles", "traffic_unit.json")
     try:
-        bench.rocprof_summary(str(trace), str(fetch), str(write), str(bj), mib, ["cmd"], str(md), str(sq))
+        bench_experiments.rocprof_summary(str(trace), str(fetch), str(write), str(bj), mib, ["cmd"], str(md), str(sq))
         rec = json.load(open(traffic))
     finally:
         if os.path.exists(traffic):
@@ -79,7 +91,7 @@ def test_sweep_report(tmp_path):
                    "best": [17, 1], "t_planned_us": 19.5, "t_best_us": 19.5}]}
     src, out = tmp_path / "s.json", tmp_path / "s.md"
     src.write_text(json.dumps(d))
-    subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--sweep-report", str(src), "--report", str(out)],
+    subprocess.run([sys.executable, os.path.join(ROOT, "bench_experiments.py"), "--sweep-report", str(src), "--report", str(out)],
                    check=True)
     assert "| cfg1 qkv | 12608 | 384 | 1152 | 2:4 | 17/1 | 19.5 | 17/1 | 19.5 | 1.000 |" in out.read_text()
 
