@@ -16,7 +16,9 @@
  *
  * Conventions for every entry point:
  *   - Every buffer is owned by the caller.  The library never allocates device
- *     memory and never frees anything it is given.
+ *     memory and never frees anything it is given.  (The one device array the
+ *     library owns is the fixed scratch of nm_spmm_noalloc, part of its code
+ *     object's static data.)
  *   - "host" pointers are ordinary CPU memory; "device" pointers are GPU
  *     memory of the current HIP device (hipMalloc or a PyTorch CUDA tensor).
  *   - Device pointers must be 16-byte aligned.
@@ -27,7 +29,8 @@
  *   - On any error status nothing has been written to any caller buffer
  *     (except the diagnostic fields of an nm_desc).
  *   - The library has no global mutable state besides a thread-safe cache of
- *     per-device properties.
+ *     per-device properties and, per device, the scratch array of
+ *     nm_spmm_noalloc with its looked-up address.
  */
 #ifndef NMSPMM_H
 #define NMSPMM_H
@@ -252,6 +255,23 @@ typedef struct nm_outputs {
 nm_status nm_spmm_out(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
                       const nm_desc *desc, const nm_outputs *out,
                       void *ws, size_t ws_bytes, void *stream, const nm_plan *plan);
+
+/* nm_spmm_out without a caller workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  A plan that needs a workspace (split_k > 1) uses a
+ * scratch array that the library holds in device memory instead: the 16384-byte
+ * counter block plus 32 MiB (33570816 bytes in all), one copy per device, kept
+ * until the process ends.  The call itself allocates nothing.  The first call
+ * on a device looks the array up and clears its counters with a kernel on
+ * `stream`; every call leaves them at zero again.  All calls on one device
+ * share that array, so calls that may overlap on one device (other streams,
+ * other host threads without ordering) race on it and must not be issued.
+ * Arguments as nm_spmm_out without ws / ws_bytes; plan may be NULL (the
+ * planner's).  Errors as nm_spmm_out; NM_ERR_WORKSPACE when the plan needs
+ * more than the array holds (nm_workspace_size() > 33570816), NM_ERR_HIP when
+ * the array cannot be looked up. */
+nm_status nm_spmm_noalloc(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
+                          const nm_desc *desc, const nm_outputs *out, void *stream, const nm_plan *plan);
 
 /* nm_gemm_i8_dense_ex with the outputs given by `out`. */
 nm_status nm_gemm_i8_dense_out(const int8_t *X, int m, const int8_t *W, int n, int k,

@@ -74,6 +74,9 @@ struct GemmArgs {
 // still zero for the next call with another plan.
 constexpr size_t kCounterBytes = 16384;
 constexpr int kMaxSplitTiles = (int)(kCounterBytes / 4);
+// Static scratch of nm_spmm_noalloc: the counter block plus 32 MiB of partial
+// tiles, held by every device the library runs on until the process ends.
+constexpr size_t kNoAllocScratchBytes = kCounterBytes + ((size_t)32 << 20);
 size_t workspace_bytes(int split_k, int tiles, int m, int n);
 
 int device_cu_count();     // cached per device; 256 when no device is visible

@@ -30,8 +30,9 @@ EXPORTED = (
     "nm_status_string", "nm_compress_size", "nm_compress", "nm_decompress", "nm_num_tiles",
     "nm_tile_info", "nm_plan_kernel_name", "nm_spmm_plan", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
     "nm_spmm", "nm_spmm_ex", "nm_gemm_i8_dense", "nm_gemm_i8_dense_ex", "nm_spmm_out", "nm_gemm_i8_dense_out",
-    "nm_quantize_f16",
+    "nm_quantize_f16", "nm_spmm_noalloc",
 )
+NM_NOALLOC_SCRATCH_BYTES = 16384 + (32 << 20)
 
 
 class NmDesc(ctypes.Structure):
@@ -104,6 +105,7 @@ def lib() -> ctypes.CDLL:
             "nm_spmm_out": ([vp, i32, vp, vp, pd, ctypes.POINTER(NmOutputs), vp, sz, vp, pp], i32),
             "nm_gemm_i8_dense_out": ([vp, i32, vp, i32, i32, ctypes.POINTER(NmOutputs), vp, sz, vp, pp], i32),
             "nm_quantize_f16": ([vp, ctypes.c_int64, ctypes.c_float, vp, vp], i32),
+            "nm_spmm_noalloc": ([vp, i32, vp, vp, pd, ctypes.POINTER(NmOutputs), vp, pp], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -403,6 +405,28 @@ def spmm(X, w: DeviceWeight, Y=None, scale=None, Yh=None, plan: Optional[NmPlan]
     st = lib().nm_spmm_out(_ptr(X), m, _ptr(w.vals), _ptr(w.meta), ctypes.byref(w.desc), ctypes.byref(o), _ptr(ws),
                            ws_bytes, _stream(stream), pl)
     _check(st, "nm_spmm_out")
+    return Y, Yh, Yq
+
+
+def spmm_noalloc(X, w: DeviceWeight, Y=None, scale=None, Yh=None, Yq=None, qscale=None,
+                 plan: Optional[NmPlan] = None, stream=None):
+    """nm_spmm_noalloc: nm_spmm_out with the library's static scratch in place
+    of a workspace (nothing is allocated by the call).  Returns (Y, Yh, Yq)."""
+    torch = _torch()
+    d = w.desc
+    if X.dim() != 2:
+        raise ValueError(f"X: {X.dim()}-D, expected [m x {d.k}]")
+    m = X.shape[0]
+    _need(X, "X", (torch.int8,), (m, d.k))
+    _need(w.vals, "w.vals", (torch.int8,), numel=d.vals_bytes)
+    _need(w.meta, "w.meta", (torch.uint8,), numel=d.meta_bytes)
+    _check_outputs(torch, m, d.n, Y, scale, Yh, Yq, qscale)
+    _on_device((("X", X), ("w.vals", w.vals), ("w.meta", w.meta), ("Y", Y), ("Yh", Yh), ("Yq", Yq),
+                ("scale", scale), ("qscale", qscale)))
+    o = _outputs(Y, scale, Yh, Yq, qscale)
+    pl = ctypes.byref(plan) if plan is not None else None
+    _check(lib().nm_spmm_noalloc(_ptr(X), m, _ptr(w.vals), _ptr(w.meta), ctypes.byref(d), ctypes.byref(o),
+                                 _stream(stream), pl), "nm_spmm_noalloc")
     return Y, Yh, Yq
 
 
