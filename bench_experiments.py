@@ -24,8 +24,8 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from bench import (PEAK_HBM_GBS, PEAK_INT8_TOPS, PEAK_SPARSE_TOPS, Prepared, algorithmic_bytes,  # noqa: E402
-                   default_traffic_path, kernel_source_sha256, log, mfma_ceiling, pattern_name)
+from bench import (PEAK_HBM_GBS, PEAK_INT8_TOPS, PEAK_SPARSE_TOPS, SP42_KINDS, Prepared,  # noqa: E402
+                   algorithmic_bytes, default_traffic_path, kernel_source_sha256, log, mfma_ceiling, pattern_name)
 from paper_2607_12505_amd import nmspmm  # noqa: E402
 from paper_2607_12505_amd import workloads as wl  # noqa: E402
 
@@ -531,9 +531,8 @@ def shape_report(torch, report, cfgs=(0, 1, 2, 3, 4)):
         for p, (ts, td), tv in zip(preps, each, vendor):
             g, kind = p.g, p.splan.kind
             ops = g.dense_eq_ops
-            peak = PEAK_SPARSE_TOPS if kind == nmspmm.NM_KIND_SP42 else PEAK_INT8_TOPS
-            rate = sp_rate if kind == nmspmm.NM_KIND_SP42 else sp_rate / 2 if kind == nmspmm.NM_KIND_SP42X2 \
-                else dn_rate
+            peak = PEAK_SPARSE_TOPS if kind in SP42_KINDS else PEAK_INT8_TOPS
+            rate = sp_rate if kind in SP42_KINDS else dn_rate
             b = algorithmic_bytes(g, work.out_int32, work.out_f16, sparse=p.sparse_kernel)
             bd = algorithmic_bytes(g, work.out_int32, work.out_f16, sparse=False)
             t_mfma, t_hbm = ops / (peak * 1e9), b / (PEAK_HBM_GBS * 1e6)      # ms
@@ -554,9 +553,10 @@ def shape_report(torch, report, cfgs=(0, 1, 2, 3, 4)):
               "Command: `python3 bench_experiments.py --shape-report --report profiles/per_shape_roofline.md` (repository root).  "
               "Every distinct (shape, N:M) of the five workloads; mean of 5 back-to-back launches with inputs resident "
               "(HIP events).  Peaks: HBM 8 TB/s; matrix cores 10.07 dense-equivalent POPS for one 4:2 stream "
-              "(smfmac), 5.03 POPS for two streams and dense.  \"MFMA frac (meas.)\" divides by the rate measured "
+              "(smfmac, for 2:4 and the 1:4, 1:8 and 2:8 weights expanded to it), 5.03 POPS for dense and for the mask "
+              "layouts expanded to dense tiles.  \"MFMA frac (meas.)\" divides by the rate measured "
               f"in the same run on random int8 operands: smfmac {ceil['smfmac_i32_16x16x128_i8_random_pops']} "
-              f"dense-equivalent POPS (two streams: half), dense {ceil['mfma_i32_16x16x64_i8_random_pops']} POPS "
+              f"dense-equivalent POPS, dense {ceil['mfma_i32_16x16x64_i8_random_pops']} POPS "
               f"(on zeros: {ceil['smfmac_i32_16x16x128_i8_zero_pops']} and {ceil['mfma_i32_16x16x64_i8_zero_pops']}).  "
               "Roofline fraction = max(compute time at peak, algorithmic bytes at 8 TB/s) / measured time; "
               "algorithmic bytes count the compact packed weight (N/M of the values plus ceil(log2 M) bits per value).  "

@@ -57,46 +57,74 @@ typedef enum nm_status {
 #define NM_OUT_F16 2
 #define NM_OUT_I8 4
 
-/* Physical layout of the packed weight produced by nm_compress. */
-#define NM_LAYOUT_SP42 1
+/* Physical layouts of the packed weight produced by nm_compress, and the
+ * kernel families they feed (nm_desc.layout, nm_desc.kind, nm_plan.kind; a
+ * layout and its kernel family share a number). */
+#define NM_LAYOUT_SP42 1   /* 2:4: the 4:2 operand of the structured-sparse MFMA as stored */
+#define NM_LAYOUT_C14 2    /* 1:4: one value and a 2-bit position per 4-group */
+#define NM_LAYOUT_DENSE 3  /* W itself, row-major (3:4, 4:4, 6:8, 7:8, 8:8) */
+#define NM_LAYOUT_C18 4    /* 1:8: one value and a 3-bit position per 8-window */
+#define NM_LAYOUT_C28 5    /* 2:8: two values and two 3-bit positions per 8-window */
+#define NM_LAYOUT_MK3 6    /* 3:8: three values and an 8-bit occupancy mask per 8-window */
+#define NM_LAYOUT_MK4 7    /* 4:8: four values and an 8-bit occupancy mask per 8-window */
+#define NM_LAYOUT_MK5 8    /* 5:8: five values and an 8-bit occupancy mask per 8-window */
 
 /*
  * Descriptor of a packed weight.  Filled by nm_compress / nm_compress_size and
  * treated as read-only afterwards.
  *
- * Layout NM_LAYOUT_SP42 ("4:2 streams"):  the paper's packed form B_pack keeps
- * each window's nonzero values together with their positions inside the
- * window (Sec. 4.2).  Here every window is cut into aligned 4-wide groups and
- * each group is stored as `streams` pairs of (value, 2-bit position): the form
- * the gfx950 structured-sparse matrix instruction consumes directly, so the
- * kernels need no decode step.  Patterns with at most 2 nonzeros in any
- * 4-group (1:4, 2:4, 1:8, 2:8) use one stream; the others (3:4, 4:4, 3:8 ..
- * 8:8) use two.  Inside a group the slots hold the group's nonzeros by
- * ascending position, then zero-valued padding at the smallest unused
- * positions; the slot positions are distinct and ascending.
+ * The paper's packed form B_pack keeps each window's nonzero values together
+ * with their positions inside the window (Sec. 4.2).  In memory it is compact:
+ * N/M of the values plus a few position bits per window; the GEMM kernels
+ * expand it on the fly -- into the 4:2 operand of the gfx950 structured-sparse
+ * matrix instruction (two (value, 2-bit position) slots per aligned 4-group of
+ * k) for the patterns with at most 2 nonzeros in every 4-group, or into a dense
+ * tile for the dense matrix instruction for 3:8, 4:8 and 5:8.  Patterns whose
+ * compact form would save too little (3:4, 4:4, 6:8, 7:8, 8:8) keep W as it is.
  *
- * With F = ceil(n / 16) row fragments and S = ceil(k / 128) k-steps, the packed
- * weight is a sequence of F * S * streams blocks, block b = (f * S + s) *
- * streams + q.  Block b holds
- *     vals[b * 1024 + 16 * L + 2 * g + t]   (int8)
- *     meta[b * 256 + 4 * L .. + 3]          (uint32, little endian)
- * for lane L in 0..63, group g in 0..7 and slot t in 0..1 of stream q:
- *     row     = 16 * f + (L % 16)
- *     group   = the 4 entries of W[row] starting at k0 = 128 * s + 32 * (L / 16) + 4 * g
- *     vals[...] = value of slot (2 * q + t) of that group
- *     bits [4 * g + 2 * t + 1 : 4 * g + 2 * t] of the meta word = its position (0..3)
- * Rows >= n and columns >= k are zero padding.
- *   vals_bytes = F * S * streams * 1024,  meta_bytes = F * S * streams * 256.
+ * Canonical slots (SP42, C14, C18, C28): a window (or 4-group) of M weights
+ * with S slots holds its nonzeros by ascending position, then zero-valued
+ * padding at the smallest unused positions; the S positions are sorted
+ * ascending.  Mask layouts (MKn) hold a window's nonzeros by ascending
+ * position, then zeros, and bit p of the window's mask is set iff position p
+ * is nonzero.
+ *
+ * Every layout except DENSE is a sequence of blocks, one per (16-row fragment
+ * f, 128-wide k-step s), block b = f * S + s with F = ceil(n / 16) fragments
+ * and S = ceil(k / 128) k-steps.  Lane L (0..63) of block b covers row
+ * r = 16 f + L % 16 and the 32 columns starting at c0 = 128 s + 32 (L / 16);
+ * "group g" is W[r][c0 + 4g .. +4) (g = 0..7) and "window w" is
+ * W[r][c0 + 8w .. +8) (w = 0..3).  With VB value bytes and MB position bytes
+ * per lane, lane L's bytes are vals[(64 b + L) * VB ..] and
+ * meta[(64 b + L) * MB ..] (little endian):
+ *
+ *   SP42 (VB 16, MB 4):  vals[.. + 2g + t] = slot t of group g (2 slots);
+ *                        meta bits [4g + 2t + 1 : 4g + 2t] = its position 0..3
+ *   C14  (VB 8, MB 2):   vals[.. + g] = slot of group g (1 slot);
+ *                        meta bits [2g + 1 : 2g] = its position 0..3
+ *   C18  (VB 4, MB 2):   vals[.. + w] = slot of window w (1 slot);
+ *                        meta bits [3w + 2 : 3w] = its position 0..7, bits 12..15 zero
+ *   C28  (VB 8, MB 4):   vals[.. + 2w + t] = slot t of window w (2 slots);
+ *                        meta bits [6w + 3t + 2 : 6w + 3t] = its position 0..7, bits 24..31 zero
+ *   MKn  (VB 4n, MB 4):  vals[.. + n w + j] = the j-th nonzero of window w (0 past the last);
+ *                        meta byte w = the occupancy mask of window w
+ *
+ * Rows >= n and columns >= k are zero.  vals_bytes = 64 F S VB and
+ * meta_bytes = 64 F S MB: per weight, N/M value bytes and (SP42, C14) exactly
+ * the position bits, (C18, C28) the position bits padded to 16 or 32 bits per
+ * lane (0.5 and 1 bit per weight against 0.375 and 0.75), (MKn) one mask bit,
+ * all rounded up to whole fragments and k-steps.  DENSE: vals = W [n x k]
+ * row-major (vals_bytes = n k), meta_bytes = 0 (meta may be NULL).
  */
 typedef struct nm_desc {
     int32_t n, k;          /* logical W shape [n x k] */
     int32_t nm_n, nm_m;    /* pattern: at most nm_n nonzeros per aligned window of nm_m */
-    int32_t streams;       /* 4:2 streams per 4-group: 1 or 2 */
-    int32_t layout;        /* NM_LAYOUT_SP42 */
+    int32_t kind;          /* NM_KIND_* of the kernels that consume this layout */
+    int32_t layout;        /* NM_LAYOUT_* */
     int32_t n_frags;       /* ceil(n / 16) */
     int32_t k_steps;       /* ceil(k / 128) */
     int64_t vals_bytes;    /* bytes of the packed values */
-    int64_t meta_bytes;    /* bytes of the packed positions */
+    int64_t meta_bytes;    /* bytes of the packed positions or masks */
     int32_t bad_row;       /* first offending row when NM_ERR_PATTERN, else -1 */
     int32_t bad_group;     /* its window index (k / nm_m units), else -1 */
 } nm_desc;
@@ -104,22 +132,36 @@ typedef struct nm_desc {
 /*
  * Launch plan of a GEMM (paper Sec. 4.3, adaptive parallelism): a workgroup
  * tile of tile_n output channels x tile_m tokens, and split_k partitions of
- * the reduction axis whose partial sums are merged at the end.  Plans come
- * from the planners below; callers may also build one from nm_tile_info to
- * force a schedule.  Every valid plan gives bit-identical results.
+ * the reduction axis whose partial sums are merged at the end.  For a compact
+ * weight (the C14, C18, C28 and MKn layouts) the plan also says where the
+ * weight is expanded: inside every workgroup, one k-step at a time, ahead of
+ * its use (expand = 0), or once per call by a separate kernel into the
+ * workspace, which the 4:2-operand (C14, C18, C28) or dense (MKn) GEMM kernel
+ * then reads (expand = 1): the first costs the expansion once per row of
+ * output tiles, the second once per call plus a launch.  Plans come from the
+ * planners below; callers may also build one from nm_tile_info to force a
+ * schedule.  Every valid plan gives bit-identical results.
  */
 typedef struct nm_plan {
-    int32_t kind;      /* NM_KIND_* */
-    int32_t tile;      /* index into the tile table, 0 .. nm_num_tiles()-1 */
-    int32_t tile_n;    /* output channels per workgroup (filled by the library) */
-    int32_t tile_m;    /* tokens per workgroup (filled by the library) */
-    int32_t split_k;   /* 1, 2, 4 or 8 */
-    int32_t grid;      /* workgroups launched (filled by the library) */
+    int32_t kind;          /* NM_KIND_* (the weight's kind) */
+    int32_t tile;          /* index into the tile table, 0 .. nm_num_tiles()-1 */
+    int32_t tile_n;        /* output channels per workgroup (filled by the library) */
+    int32_t tile_m;        /* tokens per workgroup (filled by the library) */
+    int32_t split_k;       /* 1, 2, 4 or 8 */
+    int32_t grid;          /* workgroups of the GEMM kernel (filled by the library) */
+    int32_t expand;        /* 0 or 1 (see above); must be 0 for NM_KIND_SP42 and NM_KIND_DENSE */
+    int32_t reserved;      /* 0 */
+    int64_t expand_bytes;  /* workspace bytes of the expanded weight (filled by the library) */
 } nm_plan;
 
-#define NM_KIND_SP42 1     /* structured-sparse MFMA, one 4:2 stream */
-#define NM_KIND_SP42X2 2   /* structured-sparse MFMA, two 4:2 streams */
+#define NM_KIND_SP42 1     /* structured-sparse MFMA on the stored 4:2 operand (2:4) */
+#define NM_KIND_C14 2      /* structured-sparse MFMA, 1:4 expanded in the kernel */
 #define NM_KIND_DENSE 3    /* dense MFMA on a plain row-major W */
+#define NM_KIND_C18 4      /* structured-sparse MFMA, 1:8 expanded in the kernel */
+#define NM_KIND_C28 5      /* structured-sparse MFMA, 2:8 expanded in the kernel */
+#define NM_KIND_MK3 6      /* dense MFMA, 3:8 expanded to a dense tile in the kernel */
+#define NM_KIND_MK4 7      /* dense MFMA, 4:8 expanded to a dense tile in the kernel */
+#define NM_KIND_MK5 8      /* dense MFMA, 5:8 expanded to a dense tile in the kernel */
 
 /* Human-readable name of a status code (static string, never NULL). */
 const char *nm_status_string(nm_status s);
@@ -128,7 +170,7 @@ const char *nm_status_string(nm_status s);
  * Offline packing of W into B_pack (Sec. 4.1-4.2; done once before
  * deployment, Sec. 6.1).  Host memory only, synchronous, thread-safe. */
 
-/* Fills desc (shape, streams, sizes) for W [n x k] with pattern nm_n:nm_m
+/* Fills desc (shape, layout, sizes) for W [n x k] with pattern nm_n:nm_m
  * without reading any weight.  Errors: NM_ERR_ARG (desc NULL, n or k < 1),
  * NM_ERR_UNSUPPORTED, NM_ERR_SHAPE. */
 nm_status nm_compress_size(int n, int k, int nm_n, int nm_m, nm_desc *desc);
@@ -160,19 +202,34 @@ nm_status nm_tile_info(int tile, int *tile_n, int *tile_m);
  * it assumes 256 compute units.  out_mode is a mask of NM_OUT_* bits. */
 nm_status nm_spmm_plan(const nm_desc *desc, int m, int out_mode, nm_plan *plan);
 
-/* Same for the dense baseline GEMM of shape (m, n, k). */
+/* Completes a plan built by the caller (kind, tile, split_k, expand set) for
+ * nm_spmm on this weight and token count: checks it and fills tile_n,
+ * tile_m, grid and expand_bytes, so that nm_workspace_size sizes its
+ * workspace.  Needs no GPU.  Errors: NM_ERR_ARG (bad descriptor or plan: a
+ * kind other than the descriptor's, an unknown tile, split_k outside
+ * {1, 2, 4, 8} or above the k-steps, expand = 1 for a kind that is not
+ * compact), NM_ERR_SHAPE. */
+nm_status nm_spmm_plan_complete(const nm_desc *desc, int m, nm_plan *plan);
+
+/* Same as nm_spmm_plan for the dense baseline GEMM of shape (m, n, k). */
 nm_status nm_gemm_i8_dense_plan(int m, int n, int k, int out_mode, nm_plan *plan);
 
-/* Writes into buf (NUL-terminated, at most len bytes) the name of the kernel
- * template instance a plan launches, e.g. "k_gemm<1, 2, 2, 4, 4, 3>", as it
- * appears in profiler traces.  For profiling tools; needs no GPU.
+/* Writes into buf (NUL-terminated, at most len bytes) the name of the GEMM
+ * kernel template instance a plan launches, e.g. "k_gemm<1, 2, 2, 4, 4, 3>",
+ * as it appears in profiler traces (with expand = 1: the 4:2-operand or dense
+ * kernel that follows the expansion kernel "k_expand<kind>").  For profiling
+ * tools; needs no GPU.
  * Errors: NM_ERR_ARG (bad plan, NULL buf, len too small). */
 nm_status nm_plan_kernel_name(const nm_plan *plan, char *buf, int len);
 
-/* Device workspace needed by a plan for an [m x n] output: 0 when
- * split_k == 1, else a 16384-byte block of per-tile counters followed by
- * split_k partial int32 [m x n] tiles.  A split-K plan may cover at most 4096
- * output tiles and its partial tiles must total less than 2 GiB.  Errors: NM_ERR_ARG (bad plan or NULL bytes). */
+/* Device workspace needed by a plan for an [m x n] output: 0 when split_k == 1
+ * and expand == 0; else a 16384-byte block of per-tile counters, followed with
+ * split_k > 1 by split_k partial int32 [m x n] tiles, and with expand = 1 by
+ * plan->expand_bytes for the expanded weight (256-byte aligned).  A split-K plan may cover at most
+ * 4096 output tiles and its partial tiles must total less than 2 GiB.  The
+ * planners fill expand_bytes; for a plan built by hand, the GEMM entry points
+ * check the workspace against their own sizing.  Errors: NM_ERR_ARG (bad plan
+ * or NULL bytes). */
 nm_status nm_workspace_size(const nm_plan *plan, int m, int n, size_t *bytes);
 
 /* Zero-fills a workspace on `stream` with a kernel (no memset node, so it
@@ -188,7 +245,8 @@ nm_status nm_workspace_init(void *ws, size_t bytes, void *stream);
  * Yh = fp16(fp32(Y) * scale[j]).
  *   X      device int8 [m x k], row-major (k = desc->k)
  *   vals   device copy of nm_compress's vals (desc->vals_bytes)
- *   meta   device copy of nm_compress's meta (desc->meta_bytes)
+ *   meta   device copy of nm_compress's meta (desc->meta_bytes; NULL allowed
+ *          when that is 0, i.e. for NM_LAYOUT_DENSE)
  *   desc   host descriptor from nm_compress
  *   Y      device int32 [m x n] or NULL
  *   scale  device float32 [n], required when Yh != NULL, else ignored
@@ -205,7 +263,7 @@ nm_status nm_spmm(const int8_t *X, int m, const int8_t *vals, const uint8_t *met
                   void *ws, size_t ws_bytes, void *stream);
 
 /* nm_spmm with an explicit plan (NULL = the planner's); the plan's kind must
- * match the descriptor (NM_KIND_SP42 for one stream, NM_KIND_SP42X2 for two). */
+ * be the descriptor's kind (nm_spmm_plan returns such plans). */
 nm_status nm_spmm_ex(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
                      const nm_desc *desc, int32_t *Y, const float *scale, uint16_t *Yh,
                      void *ws, size_t ws_bytes, void *stream, const nm_plan *plan);

@@ -39,10 +39,13 @@ nm_outputs outputs_of(int32_t *Y, const float *scale, uint16_t *Yh) {
 constexpr int64_t kGroupWeightBytes = (int64_t)7 << 19;  // 3.5 MiB
 constexpr int kGroupRows = 8;
 
+int64_t stored_weight_bytes(int kind, int n, int k, int n_frags, int k_steps) {
+    return kind == NM_KIND_DENSE ? (int64_t)n * k
+                                 : (int64_t)n_frags * k_steps * 64 * (layout_lane_vbytes(kind) + layout_lane_mbytes(kind));
+}
+
 int group_rows_for(int kind, int n, int k, int n_frags, int k_steps, int tiles_m) {
-    const int streams = kind == NM_KIND_SP42X2 ? 2 : 1;
-    const int64_t stored =
-        kind == NM_KIND_DENSE ? (int64_t)n * k : (int64_t)n_frags * k_steps * streams * (kVBlock + kMBlock);
+    const int64_t stored = stored_weight_bytes(kind, n, k, n_frags, k_steps);
     return stored >= kGroupWeightBytes && tiles_m >= 8 * kGroupRows ? kGroupRows : 0;
 }
 
@@ -67,25 +70,34 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
     // outputs, X and the weight are addressed with 32-bit byte offsets
     if ((int64_t)m * n >= ((int64_t)1 << 29)) return NM_ERR_SHAPE;
     if ((int64_t)m * k >= ((int64_t)1 << 32)) return NM_ERR_SHAPE;
-    const int64_t w_bytes = kind == NM_KIND_DENSE ? (int64_t)n * k : (int64_t)n_frags * k_steps * 2 * kVBlock;
-    if (w_bytes >= ((int64_t)1 << 32)) return NM_ERR_SHAPE;
+    if (stored_weight_bytes(kind, n, k, n_frags, k_steps) >= ((int64_t)1 << 32)) return NM_ERR_SHAPE;
     nm_plan plan;
     if (forced) {
         plan = *forced;
-        nm_status st = complete_plan(kind, m, n, k_steps, &plan);
+        nm_status st = complete_plan(kind, m, n, k, &plan);
         if (st != NM_OK) return st;
     } else {
-        nm_status st = make_plan(kind, m, n, k_steps, out_mode_of(o), &plan);
+        nm_status st = make_plan(kind, m, n, k, out_mode_of(o), &plan);
         if (st != NM_OK) return st;
     }
-    const int tiles = plan.grid / plan.split_k;
-    const size_t need = workspace_bytes(plan.split_k, tiles, m, n);
+    const size_t need = workspace_bytes(plan, m, n);
     if (need > 0 && ws_fn) {
         nm_status st = ws_fn(need, stream, &ws, &ws_bytes);
         if (st != NM_OK) return st;
     }
     if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return NM_ERR_WORKSPACE;
 
+    // With expand = 1 the compact weight is first expanded into the workspace
+    // (after the split-K area), and the 4:2-operand or dense kernel runs on it.
+    int run_kind = kind;
+    if (plan.expand) {
+        int8_t *exp = (int8_t *)ws + expand_offset(plan.split_k, m, n);
+        if (launch_expand(kind, A, meta, n, k, exp, stream) != 0) return NM_ERR_HIP;
+        run_kind = expanded_kind(kind);
+        A = exp;
+        meta = run_kind == NM_KIND_SP42 ? (const uint8_t *)(exp + (int64_t)n_frags * k_steps * kVBlock) : nullptr;
+    }
+    const bool split = plan.split_k > 1;
     GemmArgs a;
     a.X = X;
     a.A = A;
@@ -95,8 +107,8 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
     a.scale = o.scale;
     a.Yq = o.yq;
     a.qscale = o.qscale;
-    a.counters = need ? (int32_t *)ws : nullptr;
-    a.partials = need ? (int32_t *)((char *)ws + kCounterBytes) : nullptr;
+    a.counters = split ? (int32_t *)ws : nullptr;
+    a.partials = split ? (int32_t *)((char *)ws + kCounterBytes) : nullptr;
     a.m = m;
     a.n = n;
     a.k = k;
@@ -105,20 +117,22 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
     a.tiles_n = (n + plan.tile_n - 1) / plan.tile_n;
     a.tiles_m = (m + plan.tile_m - 1) / plan.tile_m;
     a.split_k = plan.split_k;
-    a.group_rows = group_rows_for(kind, n, k, n_frags, k_steps, a.tiles_m);
-    int err = launch_gemm(kind, plan.tile, a, plan.grid, stream);
+    a.group_rows = group_rows_for(run_kind, n, k, n_frags, k_steps, a.tiles_m);
+    int err = launch_gemm(run_kind, plan.tile, a, plan.grid, stream);
     return err == 0 ? NM_OK : NM_ERR_HIP;
 }
 
 nm_status check_desc(const nm_desc *d) {
-    if (!d || d->layout != NM_LAYOUT_SP42) return NM_ERR_ARG;
+    if (!d) return NM_ERR_ARG;
     nm_desc chk;
     if (nm_compress_size(d->n, d->k, d->nm_n, d->nm_m, &chk) != NM_OK) return NM_ERR_ARG;
-    if (chk.streams != d->streams || chk.n_frags != d->n_frags || chk.k_steps != d->k_steps) return NM_ERR_ARG;
+    if (chk.kind != d->kind || chk.layout != d->layout || chk.n_frags != d->n_frags || chk.k_steps != d->k_steps ||
+        chk.vals_bytes != d->vals_bytes || chk.meta_bytes != d->meta_bytes)
+        return NM_ERR_ARG;
     return NM_OK;
 }
 
-int kind_of(const nm_desc *d) { return d->streams == 1 ? NM_KIND_SP42 : NM_KIND_SP42X2; }
+int kind_of(const nm_desc *d) { return d->kind; }
 
 }  // namespace nmspmm
 
@@ -146,34 +160,41 @@ extern "C" nm_status nm_tile_info(int tile, int *tile_n, int *tile_m) {
 
 extern "C" nm_status nm_plan_kernel_name(const nm_plan *plan, char *buf, int len) {
     if (!plan || !buf || len <= 0 || plan->tile < 0 || plan->tile >= kNumTiles) return NM_ERR_ARG;
-    if (plan->kind != NM_KIND_SP42 && plan->kind != NM_KIND_SP42X2 && plan->kind != NM_KIND_DENSE) return NM_ERR_ARG;
+    if (!kind_is_valid(plan->kind)) return NM_ERR_ARG;
     const TileCfg &t = kTiles[plan->tile];
+    const int kind = plan->expand == 1 && kind_is_compact(plan->kind) ? expanded_kind(plan->kind) : plan->kind;
     int w;
     if (t.layout == kKSliced)
-        w = std::snprintf(buf, (size_t)len, "k_gemm_ks<%d, %d, %d, %d>", plan->kind, t.fn, t.fm, t.nst);
+        w = std::snprintf(buf, (size_t)len, "k_gemm_ks<%d, %d, %d, %d>", kind, t.fn, t.fm, t.nst);
     else
-        w = std::snprintf(buf, (size_t)len, "k_gemm<%d, %d, %d, %d, %d, %d>", plan->kind, t.wn, t.wm, t.fn, t.fm, t.nst);
+        w = std::snprintf(buf, (size_t)len, "k_gemm<%d, %d, %d, %d, %d, %d>", kind, t.wn, t.wm, t.fn, t.fm, t.nst);
     return (w > 0 && w < len) ? NM_OK : NM_ERR_ARG;
 }
 
 extern "C" nm_status nm_spmm_plan(const nm_desc *desc, int m, int out_mode, nm_plan *plan) {
     nm_status st = check_desc(desc);
     if (st != NM_OK) return st;
-    return make_plan(kind_of(desc), m, desc->n, desc->k_steps, out_mode, plan);
+    return make_plan(kind_of(desc), m, desc->n, desc->k, out_mode, plan);
+}
+
+extern "C" nm_status nm_spmm_plan_complete(const nm_desc *desc, int m, nm_plan *plan) {
+    nm_status st = check_desc(desc);
+    if (st != NM_OK) return st;
+    if (!plan || m < 0) return NM_ERR_ARG;
+    return complete_plan(kind_of(desc), m, desc->n, desc->k, plan);
 }
 
 extern "C" nm_status nm_gemm_i8_dense_plan(int m, int n, int k, int out_mode, nm_plan *plan) {
     if (n < 1 || k < 1) return NM_ERR_ARG;
     if (k % 16 != 0 || n % 4 != 0) return NM_ERR_SHAPE;
-    return make_plan(NM_KIND_DENSE, m, n, (k + kKStep - 1) / kKStep, out_mode, plan);
+    return make_plan(NM_KIND_DENSE, m, n, k, out_mode, plan);
 }
 
 extern "C" nm_status nm_workspace_size(const nm_plan *plan, int m, int n, size_t *bytes) {
-    if (!plan || !bytes || m < 0 || n < 1 || plan->split_k < 1 || plan->tile < 0 || plan->tile >= kNumTiles)
+    if (!plan || !bytes || m < 0 || n < 1 || plan->split_k < 1 || plan->tile < 0 || plan->tile >= kNumTiles ||
+        (plan->expand != 0 && plan->expand != 1) || plan->expand_bytes < 0)
         return NM_ERR_ARG;
-    const int tn = kTiles[plan->tile].tile_n(), tm = kTiles[plan->tile].tile_m();
-    const int64_t tiles = (int64_t)((n + tn - 1) / tn) * (((m > 0 ? m : 1) + tm - 1) / tm);
-    *bytes = workspace_bytes(plan->split_k, (int)tiles, m, n);
+    *bytes = workspace_bytes(*plan, m, n);
     return NM_OK;
 }
 

@@ -13,9 +13,29 @@ namespace nmspmm {
 // Fixed geometry of the packed weight and of the matrix instructions.
 constexpr int kFragRows = 16;    // rows (output channels) per MFMA fragment
 constexpr int kKStep = 128;      // dense-equivalent k per structured-sparse MFMA
-constexpr int kVBlock = 1024;    // packed value bytes per (fragment, k-step, stream)
-constexpr int kMBlock = 256;     // packed position bytes per (fragment, k-step, stream)
+constexpr int kVBlock = 1024;    // bytes of the 4:2 operand values per (fragment, k-step)
+constexpr int kMBlock = 256;     // bytes of the 4:2 operand positions per (fragment, k-step)
 constexpr int kThreads = 256;    // threads of a k-sliced workgroup (4 waves of 64)
+
+// Per-lane bytes of a packed block (include/nmspmm.h): value bytes VB and
+// position bytes MB of one lane of one (16-row fragment, k-step) block, for
+// every layout but DENSE; and the values per window of a mask layout.
+constexpr int layout_mask_values(int lay) {
+    return lay == NM_LAYOUT_MK3 ? 3 : lay == NM_LAYOUT_MK4 ? 4 : lay == NM_LAYOUT_MK5 ? 5 : 0;
+}
+constexpr int layout_lane_vbytes(int lay) {
+    return lay == NM_LAYOUT_SP42 ? 16 : lay == NM_LAYOUT_C14 ? 8 : lay == NM_LAYOUT_C18 ? 4 : lay == NM_LAYOUT_C28 ? 8
+                                                                                             : 4 * layout_mask_values(lay);
+}
+constexpr int layout_lane_mbytes(int lay) {
+    return lay == NM_LAYOUT_C14 || lay == NM_LAYOUT_C18 ? 2 : 4;
+}
+// Kernel families whose weight operand is the structured-sparse 4:2 form
+// (the others run the dense matrix instruction on a dense weight tile).
+constexpr bool kind_is_sp42(int kind) {
+    return kind == NM_KIND_SP42 || kind == NM_KIND_C14 || kind == NM_KIND_C18 || kind == NM_KIND_C28;
+}
+constexpr bool kind_is_valid(int kind) { return kind >= NM_KIND_SP42 && kind <= NM_KIND_MK5; }
 
 // Kernel layouts of a workgroup tile.
 //   kOutSplit:  WN x WM waves (4 or 8), each owning FN x FM fragments of
@@ -68,16 +88,27 @@ struct GemmArgs {
     int group_rows;         // tile order: 0 row by row, else groups of this many tile rows
 };
 
-// Workspace of a split-K plan: a fixed block of per-tile arrival counters,
-// then split_k partial [m x n] int32 tiles.  The counter block never overlaps
-// partial sums, whatever the plan, so counters left at zero by one call are
-// still zero for the next call with another plan.
+// Workspace of a plan: with split_k > 1 a fixed block of per-tile arrival
+// counters, then split_k partial [m x n] int32 tiles; then, with expand = 1,
+// the expanded weight.  The counter block never overlaps partial sums or an
+// expanded weight, whatever the plan, so counters left at zero by one call
+// are still zero for the next call with another plan.
 constexpr size_t kCounterBytes = 16384;
 constexpr int kMaxSplitTiles = (int)(kCounterBytes / 4);
 // Static scratch of nm_spmm_noalloc: the counter block plus 32 MiB of partial
 // tiles, held by every device the library runs on until the process ends.
 constexpr size_t kNoAllocScratchBytes = kCounterBytes + ((size_t)32 << 20);
-size_t workspace_bytes(int split_k, int tiles, int m, int n);
+size_t split_workspace_bytes(int split_k, int m, int n);     // counters + partials (0 without split)
+size_t expand_offset(int split_k, int m, int n);             // where the expanded weight starts
+size_t workspace_bytes(const nm_plan &plan, int m, int n);   // the whole workspace of a completed plan
+
+// Expansion of a compact weight once per call (plan.expand == 1): the kernel
+// family that then runs, and the bytes of the expanded weight (the 4:2
+// operand, 1280 bytes per fragment and k-step, or dense W [n x k]).
+constexpr bool kind_is_compact(int kind) { return kind != NM_KIND_SP42 && kind != NM_KIND_DENSE && kind_is_valid(kind); }
+constexpr int expanded_kind(int kind) { return kind_is_sp42(kind) ? NM_KIND_SP42 : NM_KIND_DENSE; }
+int64_t expanded_bytes(int kind, int n, int k);
+int launch_expand(int kind, const int8_t *vals, const uint8_t *meta, int n, int k, int8_t *out, void *stream);
 
 int device_cu_count();     // cached per device; 256 when no device is visible
 
@@ -97,7 +128,7 @@ nm_status check_desc(const nm_desc *d);
 int kind_of(const nm_desc *d);
 
 // Planner shared by both GEMM families.
-nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *plan);
-nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *plan);
+nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan);
+nm_status complete_plan(int kind, int m, int n, int k, nm_plan *plan);
 
 }  // namespace nmspmm

@@ -279,40 +279,227 @@ __device__ inline bool arrive_last(const GemmArgs &a, int tile, int *s_flag) {
     return *s_flag != 0;
 }
 
+// ---------------------------------------------------------------------------
+// Weight kinds.  The weight reaches LDS either as stored (DMA: the 4:2 operand
+// of 2:4, or plain rows of a dense W) or in a compact packed form that every
+// workgroup loads into registers one k-step ahead, expands, and writes to LDS
+// in the form the matrix instruction reads (paper Sec. 4.2: decoding
+// overlapped with shared-memory placement and matrix issue): the 4:2 operand
+// for 1:4, 1:8 and 2:8, a dense tile for the mask layouts of 3:8, 4:8 and 5:8.
+
+template <int KIND>
+struct Kind {
+    static constexpr bool kSp = kind_is_sp42(KIND);                         // smfmac on the 4:2 operand
+    static constexpr bool kDecode = KIND != NM_KIND_SP42 && KIND != NM_KIND_DENSE;
+    static constexpr int VB = KIND == NM_KIND_DENSE ? 0 : layout_lane_vbytes(KIND);  // value bytes per lane
+    static constexpr int MB = KIND == NM_KIND_DENSE ? 0 : layout_lane_mbytes(KIND);  // position bytes per lane
+    static constexpr int NV = layout_mask_values(KIND);                     // values per window (mask layouts)
+    static constexpr int VW = VB / 4 > 0 ? VB / 4 : 1;                       // value dwords per lane
+    // vector-memory loads per lane and block (as wload issues them): values
+    // (one vector for 8 and 16 bytes, else one per dword) and positions
+    static constexpr int LOADS = !kDecode ? 0 : (VB == 8 || VB == 16 ? 1 : VB / 4) + 1;
+    // LDS lookup table: 2:8 position codes (64) and window masks (256)
+    static constexpr int LUT = KIND == NM_KIND_C28 ? 64 : NV > 0 ? 256 : 1;
+};
+
+// One lane's compact bytes of one block, in registers.
+template <int KIND>
+struct WRegs {
+    uint32_t v[Kind<KIND>::VW];
+    uint32_t m;
+};
+
+// Lane values sit at L * VB bytes of a 16-byte aligned block: 8 and 16 bytes
+// per lane keep 8- and 16-byte alignment and load as one vector; 4, 12 and 20
+// bytes are only 4-byte aligned and load as dwords (never as a wider vector,
+// which could read past the end of the buffer).
+template <int KIND>
+__device__ __forceinline__ void wload(WRegs<KIND> &r, const int8_t *vals, const uint8_t *meta) {
+    constexpr int VB = Kind<KIND>::VB;
+    if constexpr (VB == 8) {
+        const v2u t = *(const v2u *)vals;
+        r.v[0] = t[0];
+        r.v[1] = t[1];
+    } else if constexpr (VB == 16) {
+        const v4u t = *(const v4u *)vals;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) r.v[i] = t[i];
+    } else {
+        static_assert(VB % 4 == 0 && VB <= 20, "value bytes per lane");
+#pragma unroll
+        for (int i = 0; i < VB / 4; ++i) r.v[i] = ((const uint32_t *)vals)[i];
+    }
+    if constexpr (Kind<KIND>::MB == 2)
+        r.m = *(const uint16_t *)meta;
+    else
+        r.m = *(const uint32_t *)meta;
+}
+
+// 2:8 table: position code c = o0 | o1 << 3 of a window (its two slots) ->
+// {byte selector placing the window's two values (source bytes 0 and 1) in
+// the 4:2 slots of its two 4-groups, position byte of those groups}.  Both
+// slots in one half: that group takes them in order, the other group holds
+// zeros at the same positions; one slot per half: each group takes its value
+// in slot 0 and a zero at the position next to it (p ^ 1) in slot 1.
+__device__ inline uint2 c28_entry(int c) {
+    const int o0 = c & 7, o1 = c >> 3;
+    const int h0 = o0 >> 2, h1 = o1 >> 2, p0 = o0 & 3, p1 = o1 & 3;
+    uint32_t sel = 0x0C0C0C0Cu, ib;
+    if (h0 == h1) {
+        sel = (sel & ~(0xFFFFu << (16 * h0))) | (0x0100u << (16 * h0));
+        const uint32_t nib = (uint32_t)(p0 | (p1 << 2));
+        ib = nib | (nib << 4);
+    } else {
+        sel = (sel & ~(0xFFu << (16 * h0))) | (0x00u << (16 * h0));
+        sel = (sel & ~(0xFFu << (16 * h1))) | (0x01u << (16 * h1));
+        ib = ((uint32_t)(p0 | ((p0 ^ 1) << 2)) << (4 * h0)) | ((uint32_t)(p1 | ((p1 ^ 1) << 2)) << (4 * h1));
+    }
+    return uint2{sel, ib};
+}
+
+// Mask table: window mask mu -> byte selectors of its 8 positions (low and
+// high 4): the rank of the position among the set bits (which source byte
+// holds its value) for a set bit, the zero selector 0x0C otherwise.
+__device__ inline uint2 mask_entry(int mu) {
+    uint32_t s[2] = {0, 0};
+    int rank = 0;
+    for (int p = 0; p < 8; ++p) {
+        const uint32_t b = ((mu >> p) & 1) ? (uint32_t)rank++ : 0x0Cu;
+        s[p >> 2] |= b << (8 * (p & 3));
+    }
+    return uint2{s[0], s[1]};
+}
+
+template <int KIND>
+__device__ inline void fill_lut(uint2 *lut, int tid, int nthreads) {
+    if constexpr (KIND == NM_KIND_C28) {
+        for (int e = tid; e < 64; e += nthreads) lut[e] = c28_entry(e);
+    } else if constexpr (Kind<KIND>::NV > 0) {
+        for (int e = tid; e < 256; e += nthreads) lut[e] = mask_entry(e);
+    }
+}
+
+// Expands one lane's compact block into its 4:2 operand: 16 value bytes
+// (two slots per 4-group) and the position word (nibble g: slot 0 position,
+// slot 1 position << 2).
+template <int KIND>
+__device__ __forceinline__ void expand_sp42(const WRegs<KIND> &r, const uint2 *lut, v4i &vals, uint32_t &idx) {
+    if constexpr (KIND == NM_KIND_C14) {
+        // group g: its value in slot 0 at position o, a zero in slot 1 at o ^ 1
+        vals[0] = (int)__builtin_amdgcn_perm(r.v[1], r.v[0], 0x0C010C00u);
+        vals[1] = (int)__builtin_amdgcn_perm(r.v[1], r.v[0], 0x0C030C02u);
+        vals[2] = (int)__builtin_amdgcn_perm(r.v[1], r.v[0], 0x0C050C04u);
+        vals[3] = (int)__builtin_amdgcn_perm(r.v[1], r.v[0], 0x0C070C06u);
+        uint32_t x = r.m;                               // 2-bit positions -> one per nibble
+        x = (x | (x << 8)) & 0x00FF00FFu;
+        x = (x | (x << 4)) & 0x0F0F0F0Fu;
+        x = (x | (x << 2)) & 0x33333333u;
+        idx = x | ((x ^ 0x11111111u) << 2);
+    } else if constexpr (KIND == NM_KIND_C18) {
+        // window w: 3-bit position o = 4 h + p -> byte w of ob; its value goes
+        // to slot 0 of group h (byte 2 h of the window's dword) at position p,
+        // a zero at p ^ 1; the empty group holds zeros at the same positions
+        uint32_t x = (r.m & 0x3Fu) | ((r.m & 0xFC0u) << 10);
+        const uint32_t ob = (x & 0x00070007u) | ((x & 0x00380038u) << 5);
+        idx = __builtin_amdgcn_perm(0xBBEE1144u, 0xBBEE1144u, ob);   // byte: (p | (p ^ 1) << 2) * 0x11
+        const uint32_t sh = (ob & 0x04040404u) << 2;                  // byte w: 16 h
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+            vals[w] = (int)(__builtin_amdgcn_perm(0u, r.v[0], 0x0C0C0C00u | (uint32_t)w) << ((sh >> (8 * w)) & 16u));
+    } else {
+        static_assert(KIND == NM_KIND_C28, "4:2 expansion");
+        idx = 0;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const uint2 e = lut[(r.m >> (6 * w)) & 63u];
+            const uint32_t src = r.v[w >> 1] >> (16 * (w & 1));     // the window's two values in bytes 0, 1
+            vals[w] = (int)__builtin_amdgcn_perm(0u, src, e.x);
+            idx |= e.y << (8 * w);
+        }
+    }
+}
+
+// Expands one lane's mask-layout block into its 32 dense weights (two
+// 16-byte chunks: windows 0-1 and 2-3).
+template <int KIND>
+__device__ __forceinline__ void expand_dense(const WRegs<KIND> &r, const uint2 *lut, v4i &c0, v4i &c1) {
+    constexpr int NV = Kind<KIND>::NV, VW = Kind<KIND>::VW;
+    uint32_t out[8];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const int b = NV * w;                                    // first value byte of the window
+        const uint32_t d0 = r.v[b / 4];
+        const uint32_t d1 = b / 4 + 1 < VW ? r.v[b / 4 + 1] : 0u;
+        const uint32_t d2 = b / 4 + 2 < VW ? r.v[b / 4 + 2] : 0u;
+        const uint32_t lo = __builtin_amdgcn_alignbyte(d1, d0, (uint32_t)(b % 4));   // bytes b .. b+3
+        const uint32_t hi = __builtin_amdgcn_alignbyte(d2, d1, (uint32_t)(b % 4));   // bytes b+4 .. b+7
+        const uint2 e = lut[(r.m >> (8 * w)) & 0xFFu];
+        out[2 * w] = __builtin_amdgcn_perm(hi, lo, e.x);
+        out[2 * w + 1] = __builtin_amdgcn_perm(hi, lo, e.y);
+    }
+    c0 = v4i{(int)out[0], (int)out[1], (int)out[2], (int)out[3]};
+    c1 = v4i{(int)out[4], (int)out[5], (int)out[6], (int)out[7]};
+}
+
+// Expands lane `lane`'s part of a compact block and writes it to the LDS
+// weight area of a slot: block bl of the tile (16 rows), in the layout the
+// compute stage reads (4:2 operand, or swizzled dense rows).
+template <int KIND, int WVB>
+__device__ __forceinline__ void expand_to_lds(const WRegs<KIND> &r, const uint2 *lut, int8_t *wslot, int bl,
+                                              int lane) {
+    if constexpr (Kind<KIND>::kSp) {
+        v4i vals;
+        uint32_t idx;
+        expand_sp42<KIND>(r, lut, vals, idx);
+        *(v4i *)(wslot + bl * kVBlock + lane * 16) = vals;
+        *(uint32_t *)(wslot + WVB + bl * kMBlock + lane * 4) = idx;
+    } else {
+        v4i c0, c1;
+        expand_dense<KIND>(r, lut, c0, c1);
+        const int row = bl * 16 + (lane & 15);
+        const int ch = 2 * (lane >> 4);                          // the lane's first 16-byte chunk of the row
+        int8_t *rowp = wslot + row * 128;
+        *(v4i *)(rowp + ((ch ^ (row & 7)) << 4)) = c0;
+        *(v4i *)(rowp + (((ch + 1) ^ (row & 7)) << 4)) = c1;
+    }
+}
+
 template <int KIND, int WN_, int WM_, int FN_, int FM_, int NST>
 struct Geometry {
+    using K = Kind<KIND>;
     static constexpr int WN = WN_, WM = WM_, FN = FN_, FM = FM_;
     static constexpr int NW = WN * WM;                               // waves per workgroup (4 or 8)
     static constexpr int BN = WN * FN * 16;
     static constexpr int BM = WM * FM * 16;
-    static constexpr bool kSparse = KIND != NM_KIND_DENSE;
-    static constexpr int S = KIND == NM_KIND_SP42X2 ? 2 : 1;
     static constexpr int XB = BM * 128;                              // X bytes per slot
-    static constexpr int WVB = kSparse ? (BN / 16) * S * kVBlock : BN * 128;  // weight value bytes
-    static constexpr int WMB = kSparse ? (BN / 16) * S * kMBlock : 0;         // weight position bytes
+    static constexpr int WVB = K::kSp ? (BN / 16) * kVBlock : BN * 128;  // weight value bytes per slot
+    static constexpr int WMB = K::kSp ? (BN / 16) * kMBlock : 0;         // weight position bytes per slot
     static constexpr int SLOT = XB + WVB + WMB;
     static constexpr int XI = BM / (8 * NW);                         // X loads per wave per k-step
-    static constexpr int WI = kSparse ? (BN / 16) * S / NW * 2 : BN / (8 * NW);  // weight loads per wave
-    static constexpr int DMA = XI + WI;
+    static constexpr int WB = (BN / 16) / NW;                        // weight blocks per wave (compact kinds)
+    static constexpr int WI = K::kDecode ? WB * K::LOADS                          // weight loads per wave
+                              : KIND == NM_KIND_SP42 ? (BN / 16) / NW * 2 : BN / (8 * NW);
+    static constexpr int DMA = XI + WI;                              // vector-memory loads per wave per k-step
     static constexpr int CPR = FN * 4;                               // 4-channel chunks per staged row
     static constexpr int RPI = 64 / CPR;                             // staged rows read per instruction
     static constexpr int ROWB = FN * 64 + 16;                        // padded bytes per staged int32 row
     static constexpr int EPI = NW * 16 * ROWB;
     // ring depth: as asked, or as deep as 160 KB of LDS allows
-    static constexpr int RING = NST * SLOT <= 160 * 1024 - 1024 ? NST : (160 * 1024 - 1024) / SLOT;
+    static constexpr int RING = NST * SLOT <= 160 * 1024 - 4096 ? NST : (160 * 1024 - 4096) / SLOT;
     static constexpr int LDSB = RING * SLOT > EPI ? RING * SLOT : EPI;
     static_assert((NW == 4 || NW == 8) && RING >= 2 && 64 % CPR == 0 && BM % (8 * NW) == 0, "tile shape");
-    static_assert(kSparse ? ((BN / 16) * S) % NW == 0 : BN % (8 * NW) == 0, "weight loads split evenly over the waves");
-    static_assert(LDSB <= 160 * 1024, "LDS budget");
+    static_assert(KIND == NM_KIND_DENSE ? BN % (8 * NW) == 0 : (BN / 16) % NW == 0,
+                  "weight loads split evenly over the waves");
+    static_assert(LDSB + K::LUT * 8 <= 160 * 1024, "LDS budget");
 };
 
 // The stages of an output-split tile (WN x WM waves, each FN x FM
 // accumulators).
-template <class G>
+template <class G, int KIND>
 struct OutSplit {
-    static constexpr int BN = G::BN, BM = G::BM, S = G::S, FN = G::FN, FM = G::FM, NW = G::NW;
-
-    static constexpr int WJ = G::kSparse ? (BN / 16) * S / NW : BN / (8 * NW);  // weight loads per wave
+    using K = Kind<KIND>;
+    static constexpr int BN = G::BN, BM = G::BM, FN = G::FN, FM = G::FM, NW = G::NW;
+    static constexpr int WJ = KIND == NM_KIND_SP42 ? (BN / 16) / NW : K::kDecode ? G::WB : BN / (8 * NW);
 
     // Per-lane byte offsets of one tile's loads at k-step 0: the X row chunks
     // and the weight blocks (or dense weight row chunks).  A k-step adds the
@@ -323,7 +510,7 @@ struct OutSplit {
     struct Cursor {
         uint32_t x[G::XI];
         uint32_t w[WJ];
-        uint32_t m[G::kSparse ? WJ : 1];
+        uint32_t m[KIND == NM_KIND_DENSE ? 1 : WJ];
     };
 
     static __device__ __forceinline__ Cursor cursor(const GemmArgs &a, int wave, int lane, int tok0, int ch0) {
@@ -335,16 +522,17 @@ struct OutSplit {
             const int tok = tok0 + r < a.m ? tok0 + r : a.m - 1;
             c.x[j] = (uint32_t)tok * (uint32_t)a.k + (uint32_t)cc * 16;
         }
-        if constexpr (G::kSparse) {
+        if constexpr (KIND == NM_KIND_SP42 || K::kDecode) {
             const int f0 = ch0 >> 4;
+            constexpr int VB = KIND == NM_KIND_SP42 ? 16 : K::VB, MB = KIND == NM_KIND_SP42 ? 4 : K::MB;
 #pragma unroll
             for (int j = 0; j < WJ; ++j) {
-                const int bl = NW * j + wave;              // weight block of the slot: fragment bl / S, stream bl % S
-                int f = f0 + bl / S;
+                const int bl = NW * j + wave;              // weight block of the slot
+                int f = f0 + bl;
                 f = f < a.n_frags ? f : a.n_frags - 1;
-                const uint32_t b0 = (uint32_t)f * (uint32_t)a.k_steps * S + bl % S;
-                c.w[j] = b0 * kVBlock + lane * 16;
-                c.m[j] = b0 * kMBlock + lane * 4;
+                const uint32_t b0 = (uint32_t)f * (uint32_t)a.k_steps;
+                c.w[j] = (b0 * 64 + lane) * VB;
+                c.m[j] = (b0 * 64 + lane) * MB;
             }
         } else {
 #pragma unroll
@@ -358,10 +546,10 @@ struct OutSplit {
         return c;
     }
 
-    // Fill ring slot st with k-step s of the tile of cursor c.  Past k the
-    // packed weight is zero, so X may hold anything there (its loads are
-    // clamped to the row); for a dense weight the tail k-step is staged with
-    // zeros instead.
+    // Fill ring slot st with k-step s of the tile of cursor c: the X slice,
+    // and for the stored kinds the weight slice.  Past k the packed weight is
+    // zero, so X may hold anything there (its loads are clamped to the row);
+    // for a dense weight the tail k-step is staged with zeros instead.
     static __device__ __forceinline__ void issue(const GemmArgs &a, const Cursor &c, int8_t *lds, uint32_t lds0,
                                                  int wave, int lane, int s, int st) {
         const uint32_t slot = lds0 + st * G::SLOT;
@@ -380,16 +568,16 @@ struct OutSplit {
                 dma16o(a.X, c.x[j] - cc16 + kk, slot + (NW * j + wave) * 1024);
             }
         }
-        if constexpr (G::kSparse) {
-            const int8_t *vb = a.A + (size_t)s * S * kVBlock;
-            const uint8_t *mb = a.meta + (size_t)s * S * kMBlock;
+        if constexpr (KIND == NM_KIND_SP42) {
+            const int8_t *vb = a.A + (size_t)s * kVBlock;
+            const uint8_t *mb = a.meta + (size_t)s * kMBlock;
 #pragma unroll
             for (int j = 0; j < WJ; ++j) {
                 const int bl = NW * j + wave;
                 dma16o(vb, c.w[j], slot + G::XB + bl * kVBlock);
                 dma4o(mb, c.m[j], slot + G::XB + G::WVB + bl * kMBlock);
             }
-        } else {
+        } else if constexpr (KIND == NM_KIND_DENSE) {
             if (s * 128 + 128 <= a.k) {
                 const int8_t *wb = a.A + (size_t)s * 128;
 #pragma unroll
@@ -409,23 +597,42 @@ struct OutSplit {
         }
     }
 
+    // Compact kinds: this wave's compact blocks of k-step s into registers.
+    static __device__ __forceinline__ void wload_step(const GemmArgs &a, const Cursor &c, int s,
+                                                      WRegs<KIND> (&r)[WJ]) {
+        if constexpr (K::kDecode) {
+            const int8_t *vb = a.A + (size_t)s * 64 * K::VB;
+            const uint8_t *mb = a.meta + (size_t)s * 64 * K::MB;
+#pragma unroll
+            for (int j = 0; j < WJ; ++j) wload<KIND>(r[j], vb + c.w[j], mb + c.m[j]);
+        }
+    }
+
+    // Compact kinds: expand the registers into the weight area of slot st.
+    static __device__ __forceinline__ void expand_step(int8_t *lds, const uint2 *lut, int wave, int lane, int st,
+                                                       const WRegs<KIND> (&r)[WJ]) {
+        if constexpr (K::kDecode) {
+#pragma unroll
+            for (int j = 0; j < WJ; ++j)
+                expand_to_lds<KIND, G::WVB>(r[j], lut, lds + st * G::SLOT + G::XB, NW * j + wave, lane);
+        }
+    }
+
     // One k-step of the wave's FN x FM accumulators from ring slot st.
     static __device__ __forceinline__ void compute(const int8_t *lds, int wn, int wm, int lane, int st,
                                                    v4i (&acc)[FN][FM]) {
         const int lg = lane >> 4;
         const int8_t *xs = lds + st * G::SLOT;
         const int8_t *ws = xs + G::XB;
-        if constexpr (G::kSparse) {
-            v4i av[FN][S];
-            int ai[FN][S];
+        if constexpr (K::kSp) {
+            v4i av[FN];
+            int ai[FN];
 #pragma unroll
-            for (int i = 0; i < FN; ++i)
-#pragma unroll
-                for (int q = 0; q < S; ++q) {
-                    const int bl = (wn * FN + i) * S + q;
-                    av[i][q] = *(const v4i *)(ws + bl * kVBlock + lane * 16);
-                    ai[i][q] = *(const int *)(ws + G::WVB + bl * kMBlock + lane * 4);
-                }
+            for (int i = 0; i < FN; ++i) {
+                const int bl = wn * FN + i;
+                av[i] = *(const v4i *)(ws + bl * kVBlock + lane * 16);
+                ai[i] = *(const int *)(ws + G::WVB + bl * kMBlock + lane * 4);
+            }
 #pragma unroll
             for (int j = 0; j < FM; ++j) {
                 const int r = (wm * FM + j) * 16 + (lane & 15);
@@ -435,9 +642,7 @@ struct OutSplit {
                 const v8i b = {blo[0], blo[1], blo[2], blo[3], bhi[0], bhi[1], bhi[2], bhi[3]};
 #pragma unroll
                 for (int i = 0; i < FN; ++i)
-#pragma unroll
-                    for (int q = 0; q < S; ++q)
-                        acc[i][j] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(av[i][q], b, acc[i][j], ai[i][q], 0, 0);
+                    acc[i][j] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(av[i], b, acc[i][j], ai[i], 0, 0);
             }
         } else {
             v4i alo[FN], ahi[FN];
@@ -504,11 +709,13 @@ struct OutSplit {
 template <int KIND, int WN, int WM, int FN, int FM, int NST>
 __global__ __launch_bounds__(64 * WN * WM) void k_gemm(GemmArgs a) {
     using G = Geometry<KIND, WN, WM, FN, FM, NST>;
-    using O = OutSplit<G>;
+    using O = OutSplit<G, KIND>;
+    using K = Kind<KIND>;
     constexpr int BN = G::BN, BM = G::BM;
     constexpr int R = G::RING;
 
     __shared__ __attribute__((aligned(1024))) int8_t lds[G::LDSB];
+    __shared__ uint2 lut[K::LUT];
     __shared__ int s_last;
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
 
@@ -533,16 +740,42 @@ __global__ __launch_bounds__(64 * WN * WM) void k_gemm(GemmArgs a) {
         for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
 
     const typename O::Cursor cur = O::cursor(a, wave, lane, tok0, ch0);
+    WRegs<KIND> wr[O::WJ];
+    if constexpr (K::kDecode) {
+        fill_lut<KIND>(lut, tid, 64 * WN * WM);
+        __syncthreads();
+    }
 #pragma unroll
     for (int i = 0; i < R - 1; ++i)
         if (i < nsteps) O::issue(a, cur, lds, lds0, wave, lane, s_begin + i, i);
+    if constexpr (K::kDecode) {
+        // the compact weights of the first R - 1 k-steps, expanded in order,
+        // and the next k-step's loaded into registers
+        if (nsteps > 0) O::wload_step(a, cur, s_begin, wr);
+#pragma unroll
+        for (int i = 0; i < R - 1; ++i)
+            if (i < nsteps) {
+                O::expand_step(lds, lut, wave, lane, i, wr);
+                if (i + 1 < nsteps) O::wload_step(a, cur, s_begin + i + 1, wr);
+            }
+    }
     for (int it = 0; it < nsteps; ++it) {
         // k-step it was issued NST-1 iterations ago; only the loads of later
         // k-steps may remain in flight.  The barrier then publishes every
-        // wave's slot and frees the slot computed in the previous iteration.
+        // wave's slot (X and expanded weights) and frees the slot computed in
+        // the previous iteration.
         const int later = nsteps - 1 - it < R - 2 ? nsteps - 1 - it : R - 2;
         wait_later_then_barrier<R - 2, G::DMA>(later);
-        if (it + R - 1 < nsteps) O::issue(a, cur, lds, lds0, wave, lane, s_begin + it + R - 1, (it + R - 1) % R);
+        const int nx = it + R - 1;
+        if (nx < nsteps) {
+            if constexpr (K::kDecode) {
+                O::expand_step(lds, lut, wave, lane, nx % R, wr);      // k-step nx, loaded one iteration ago
+                O::issue(a, cur, lds, lds0, wave, lane, s_begin + nx, nx % R);
+                if (nx + 1 < nsteps) O::wload_step(a, cur, s_begin + nx + 1, wr);
+            } else {
+                O::issue(a, cur, lds, lds0, wave, lane, s_begin + nx, nx % R);
+            }
+        }
         O::compute(lds, wn, wm, lane, it % R, acc);
     }
 
@@ -578,18 +811,17 @@ __global__ __launch_bounds__(64 * WN * WM) void k_gemm(GemmArgs a) {
 
 template <int KIND, int FN, int FM, int NST>
 struct GeometryKS {
+    using K = Kind<KIND>;
     static constexpr int BN = FN * 16;
     static constexpr int BM = FM * 16;
-    static constexpr bool kSparse = KIND != NM_KIND_DENSE;
-    static constexpr int S = KIND == NM_KIND_SP42X2 ? 2 : 1;
     static constexpr int XB = BM * 128;
-    static constexpr int WVB = kSparse ? (BN / 16) * S * kVBlock : BN * 128;
-    static constexpr int WMB = kSparse ? (BN / 16) * S * kMBlock : 0;
+    static constexpr int WVB = K::kSp ? (BN / 16) * kVBlock : BN * 128;
+    static constexpr int WMB = K::kSp ? (BN / 16) * kMBlock : 0;
     static constexpr int SLOT = XB + WVB + WMB;
     static constexpr int XI = BM / 8;                                  // X loads per k-step (one wave)
-    static constexpr int WI = kSparse ? (BN / 16) * S * 2 : BN / 8;    // weight loads per k-step
+    static constexpr int WI = K::kDecode ? FN * K::LOADS : KIND == NM_KIND_SP42 ? FN * 2 : BN / 8;
     static constexpr int DMA = XI + WI;
-    static constexpr int RING = 4 * NST * SLOT <= 160 * 1024 - 1024 ? NST : (160 * 1024 - 1024) / (4 * SLOT);
+    static constexpr int RING = 4 * NST * SLOT <= 160 * 1024 - 4096 ? NST : (160 * 1024 - 4096) / (4 * SLOT);
     static constexpr int ROWB = BN * 4 + 16;                           // padded staged row (int32)
     static constexpr int RED = 4 * BM * ROWB;
     static constexpr int LDSB = 4 * RING * SLOT > RED ? 4 * RING * SLOT : RED;
@@ -600,10 +832,11 @@ struct GeometryKS {
 template <int KIND, int FN, int FM, int NST>
 __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
     using G = GeometryKS<KIND, FN, FM, NST>;
-    constexpr int BN = G::BN, BM = G::BM, S = G::S, R = G::RING;
-    constexpr bool kSparse = G::kSparse;
+    using K = Kind<KIND>;
+    constexpr int BN = G::BN, BM = G::BM, R = G::RING;
 
     __shared__ __attribute__((aligned(1024))) int8_t lds[G::LDSB];
+    __shared__ uint2 lut[K::LUT];
     __shared__ int s_last;
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
 
@@ -630,7 +863,8 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < FM; ++j) acc[i][j] = v4i{0, 0, 0, 0};
 
-    // k-step s into slot st of this wave's ring (same clamping rules as above)
+    // k-step s into slot st of this wave's ring (same clamping rules as above):
+    // X, and the stored weight kinds
     auto issue = [&](int s, int st) {
         const uint32_t slot = ring + st * G::SLOT;
 #pragma unroll
@@ -641,16 +875,16 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
             const int kk = s * 128 + c * 16 < a.k ? s * 128 + c * 16 : a.k - 16;
             dma16(a.X + (size_t)tok * a.k + kk, slot + j * 1024);
         }
-        if constexpr (kSparse) {
+        if constexpr (KIND == NM_KIND_SP42) {
 #pragma unroll
-            for (int bl = 0; bl < (BN / 16) * S; ++bl) {
-                int f = f0 + bl / S;
+            for (int bl = 0; bl < BN / 16; ++bl) {
+                int f = f0 + bl;
                 f = f < a.n_frags ? f : a.n_frags - 1;
-                const size_t b = ((size_t)f * a.k_steps + s) * S + bl % S;
+                const size_t b = (size_t)f * a.k_steps + s;
                 dma16(a.A + b * kVBlock + lane * 16, slot + G::XB + bl * kVBlock);
                 dma4(a.meta + b * kMBlock + lane * 4, slot + G::XB + G::WVB + bl * kMBlock);
             }
-        } else {
+        } else if constexpr (KIND == NM_KIND_DENSE) {
 #pragma unroll
             for (int j = 0; j < BN / 8; ++j) {
                 const int r = 8 * j + (lane >> 3);
@@ -667,19 +901,37 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
             }
         }
     };
+    // compact kinds: the FN blocks of k-step s into registers, and their
+    // expansion into slot st
+    WRegs<KIND> wr[FN];
+    auto wload_step = [&](int s) {
+        if constexpr (K::kDecode) {
+#pragma unroll
+            for (int bl = 0; bl < FN; ++bl) {
+                int f = f0 + bl;
+                f = f < a.n_frags ? f : a.n_frags - 1;
+                const size_t b = (size_t)f * a.k_steps + s;
+                wload<KIND>(wr[bl], a.A + (b * 64 + lane) * K::VB, a.meta + (b * 64 + lane) * K::MB);
+            }
+        }
+    };
+    auto expand_step = [&](int st) {
+        if constexpr (K::kDecode) {
+#pragma unroll
+            for (int bl = 0; bl < FN; ++bl) expand_to_lds<KIND, G::WVB>(wr[bl], lut, ringp + st * G::SLOT + G::XB, bl, lane);
+        }
+    };
     auto compute = [&](int st) {
         const int8_t *xs = ringp + st * G::SLOT;
         const int8_t *ws = xs + G::XB;
-        if constexpr (kSparse) {
-            v4i av[FN][S];
-            int ai[FN][S];
+        if constexpr (K::kSp) {
+            v4i av[FN];
+            int ai[FN];
 #pragma unroll
-            for (int i = 0; i < FN; ++i)
-#pragma unroll
-                for (int q = 0; q < S; ++q) {
-                    av[i][q] = *(const v4i *)(ws + (i * S + q) * kVBlock + lane * 16);
-                    ai[i][q] = *(const int *)(ws + G::WVB + (i * S + q) * kMBlock + lane * 4);
-                }
+            for (int i = 0; i < FN; ++i) {
+                av[i] = *(const v4i *)(ws + i * kVBlock + lane * 16);
+                ai[i] = *(const int *)(ws + G::WVB + i * kMBlock + lane * 4);
+            }
 #pragma unroll
             for (int j = 0; j < FM; ++j) {
                 const int r = j * 16 + (lane & 15);
@@ -689,9 +941,7 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
                 const v8i b = {blo[0], blo[1], blo[2], blo[3], bhi[0], bhi[1], bhi[2], bhi[3]};
 #pragma unroll
                 for (int i = 0; i < FN; ++i)
-#pragma unroll
-                    for (int q = 0; q < S; ++q)
-                        acc[i][j] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(av[i][q], b, acc[i][j], ai[i][q], 0, 0);
+                    acc[i][j] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(av[i], b, acc[i][j], ai[i], 0, 0);
             }
         } else {
             v4i alo[FN], ahi[FN];
@@ -717,14 +967,36 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
         }
     };
 
+    if constexpr (K::kDecode) {
+        fill_lut<KIND>(lut, tid, 256);
+        __syncthreads();
+    }
     // k-step t of this wave is s_begin + wave + 4 t
 #pragma unroll
     for (int i = 0; i < R - 1; ++i)
         if (i < nsteps) issue(s_begin + wave + 4 * i, i);
+    if constexpr (K::kDecode) {
+        if (nsteps > 0) wload_step(s_begin + wave);
+#pragma unroll
+        for (int i = 0; i < R - 1; ++i)
+            if (i < nsteps) {
+                expand_step(i);
+                if (i + 1 < nsteps) wload_step(s_begin + wave + 4 * (i + 1));
+            }
+    }
     for (int t = 0; t < nsteps; ++t) {
         const int later = nsteps - 1 - t < R - 2 ? nsteps - 1 - t : R - 2;
         wait_later<R - 2, G::DMA>(later);  // this wave's slot t is in LDS, its reads of slot t-1 done
-        if (t + R - 1 < nsteps) issue(s_begin + wave + 4 * (t + R - 1), (t + R - 1) % R);
+        const int nx = t + R - 1;
+        if (nx < nsteps) {
+            if constexpr (K::kDecode) {
+                expand_step(nx % R);
+                issue(s_begin + wave + 4 * nx, nx % R);
+                if (nx + 1 < nsteps) wload_step(s_begin + wave + 4 * (nx + 1));
+            } else {
+                issue(s_begin + wave + 4 * nx, nx % R);
+            }
+        }
         compute(t % R);
     }
 
@@ -763,6 +1035,44 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Expansion of a compact weight once per call (plan.expand = 1): one thread
+// per lane of every (fragment, k-step) block, the same expansion as inside the
+// GEMM kernels, written out as the 4:2 operand blocks of the SP42 layout
+// (C14, C18, C28) or as dense W [n x k] row-major (mask layouts; rows >= n and
+// columns >= k of the padded blocks are not written).  4 blocks per
+// workgroup; blocks = n_frags * k_steps.
+template <int KIND>
+__global__ __launch_bounds__(256) void k_expand(const int8_t *__restrict__ vals, const uint8_t *__restrict__ meta,
+                                               int n, int k, int blocks, int k_steps, int8_t *out) {
+    __shared__ uint2 lut[Kind<KIND>::LUT];
+    fill_lut<KIND>(lut, threadIdx.x, 256);
+    __syncthreads();
+    const int b = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (b >= blocks) return;
+    WRegs<KIND> r;
+    const int64_t o = (int64_t)b * 64 + lane;
+    wload<KIND>(r, vals + o * Kind<KIND>::VB, meta + o * Kind<KIND>::MB);
+    if constexpr (Kind<KIND>::kSp) {
+        v4i v;
+        uint32_t idx;
+        expand_sp42<KIND>(r, lut, v, idx);
+        *(v4i *)(out + o * 16) = v;
+        *(uint32_t *)(out + (int64_t)blocks * kVBlock + o * 4) = idx;
+    } else {
+        v4i c0, c1;
+        expand_dense<KIND>(r, lut, c0, c1);
+        const int f = b / k_steps, s = b - f * k_steps;
+        const int row = f * kFragRows + (lane & 15);
+        const int col = s * kKStep + 32 * (lane >> 4);
+        if (row < n) {
+            int8_t *dst = out + (int64_t)row * k + col;
+            if (col < k) *(v4i *)dst = c0;          // k is a multiple of 16: a chunk is wholly in or out
+            if (col + 16 < k) *(v4i *)(dst + 16) = c1;
+        }
+    }
+}
+
 __global__ void k_zero(int *p, size_t n4, unsigned char *tail, int tail_bytes) {
     const size_t stride = (size_t)gridDim.x * blockDim.x;
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) p[i] = 0;
@@ -792,11 +1102,36 @@ int launch_kind(int tile, const GemmArgs &args, int grid, void *stream) {
 
 }  // namespace
 
+template <int KIND>
+int launch_expand_kind(const int8_t *vals, const uint8_t *meta, int n, int k, int8_t *out, void *stream) {
+    const int blocks = ((n + kFragRows - 1) / kFragRows) * ((k + kKStep - 1) / kKStep);
+    hipLaunchKernelGGL(k_expand<KIND>, dim3((blocks + 3) / 4), dim3(256), 0, (hipStream_t)stream, vals, meta, n, k,
+                       blocks, (k + kKStep - 1) / kKStep, out);
+    return (int)hipGetLastError();
+}
+
+int launch_expand(int kind, const int8_t *vals, const uint8_t *meta, int n, int k, int8_t *out, void *stream) {
+    switch (kind) {
+        case NM_KIND_C14: return launch_expand_kind<NM_KIND_C14>(vals, meta, n, k, out, stream);
+        case NM_KIND_C18: return launch_expand_kind<NM_KIND_C18>(vals, meta, n, k, out, stream);
+        case NM_KIND_C28: return launch_expand_kind<NM_KIND_C28>(vals, meta, n, k, out, stream);
+        case NM_KIND_MK3: return launch_expand_kind<NM_KIND_MK3>(vals, meta, n, k, out, stream);
+        case NM_KIND_MK4: return launch_expand_kind<NM_KIND_MK4>(vals, meta, n, k, out, stream);
+        case NM_KIND_MK5: return launch_expand_kind<NM_KIND_MK5>(vals, meta, n, k, out, stream);
+    }
+    return (int)hipErrorInvalidValue;
+}
+
 int launch_gemm(int kind, int tile, const GemmArgs &args, int grid, void *stream) {
     switch (kind) {
         case NM_KIND_SP42: return launch_kind<NM_KIND_SP42>(tile, args, grid, stream);
-        case NM_KIND_SP42X2: return launch_kind<NM_KIND_SP42X2>(tile, args, grid, stream);
+        case NM_KIND_C14: return launch_kind<NM_KIND_C14>(tile, args, grid, stream);
         case NM_KIND_DENSE: return launch_kind<NM_KIND_DENSE>(tile, args, grid, stream);
+        case NM_KIND_C18: return launch_kind<NM_KIND_C18>(tile, args, grid, stream);
+        case NM_KIND_C28: return launch_kind<NM_KIND_C28>(tile, args, grid, stream);
+        case NM_KIND_MK3: return launch_kind<NM_KIND_MK3>(tile, args, grid, stream);
+        case NM_KIND_MK4: return launch_kind<NM_KIND_MK4>(tile, args, grid, stream);
+        case NM_KIND_MK5: return launch_kind<NM_KIND_MK5>(tile, args, grid, stream);
     }
     return (int)hipErrorInvalidValue;
 }

@@ -20,10 +20,27 @@ namespace nmspmm {
 
 static const int kSplitSet[] = {1, 2, 4, 8};
 
-size_t workspace_bytes(int split_k, int tiles, int m, int n) {
-    (void)tiles;
+size_t split_workspace_bytes(int split_k, int m, int n) {
     if (split_k <= 1) return 0;
     return kCounterBytes + (size_t)split_k * (size_t)m * (size_t)n * 4;
+}
+
+// The expanded weight always starts past the counter block (also without
+// split-K), so no plan ever writes over the counters another plan relies on.
+size_t expand_offset(int split_k, int m, int n) {
+    const size_t used = split_k > 1 ? split_workspace_bytes(split_k, m, n) : kCounterBytes;
+    return (used + 255) & ~(size_t)255;
+}
+
+size_t workspace_bytes(const nm_plan &p, int m, int n) {
+    if (!p.expand) return split_workspace_bytes(p.split_k, m, n);
+    return expand_offset(p.split_k, m, n) + (size_t)p.expand_bytes;
+}
+
+int64_t expanded_bytes(int kind, int n, int k) {
+    if (!kind_is_compact(kind)) return 0;
+    const int64_t F = (n + kFragRows - 1) / kFragRows, S = (k + kKStep - 1) / kKStep;
+    return kind_is_sp42(kind) ? F * S * (kVBlock + kMBlock) : (int64_t)n * k;
 }
 
 int device_cu_count() {
@@ -53,8 +70,12 @@ int device_cu_count() {
 
 static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *p) {
+nm_status complete_plan(int kind, int m, int n, int k, nm_plan *p) {
     if (!p || p->kind != kind || p->tile < 0 || p->tile >= kNumTiles) return NM_ERR_ARG;
+    if (p->expand != 0 && (p->expand != 1 || !kind_is_compact(kind))) return NM_ERR_ARG;
+    const int k_steps = (k + kKStep - 1) / kKStep;
+    p->reserved = 0;
+    p->expand_bytes = p->expand ? expanded_bytes(kind, n, k) : 0;
     bool ok_split = false;
     for (int s : kSplitSet) ok_split |= (p->split_k == s);
     if (!ok_split || p->split_k > (k_steps > 0 ? k_steps : 1)) return NM_ERR_ARG;
@@ -71,6 +92,9 @@ nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *p) {
     return NM_OK;
 }
 
+// Rows of output tiles from which a compact weight is expanded once per call.
+constexpr int64_t kExpandTileRows = 32;
+
 // Tile indices used by the rules below (see kTiles).
 constexpr int kT128x128r2 = 0, kT128x64r2 = 1, kT64x128r2 = 2, kT64x64r2 = 3, kT256x256w8 = 4;
 constexpr int kT128x32r2 = 5, kT128x128w8 = 6;
@@ -80,13 +104,16 @@ static int64_t tiles_of(int t, int m, int n) {
     return ceil_div(n, kTiles[t].tile_n()) * ceil_div(m, kTiles[t].tile_m());
 }
 
-nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *plan) {
-    if (!plan || m < 0 || n < 1 || k_steps < 1) return NM_ERR_ARG;
+nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) {
+    if (!plan || m < 0 || n < 1 || k < 1) return NM_ERR_ARG;
+    const int k_steps = (k + kKStep - 1) / kKStep;
     if ((out_mode & (NM_OUT_I32 | NM_OUT_F16 | NM_OUT_I8)) == 0) return NM_ERR_ARG;
     const int64_t cus = device_cu_count();
     const int mm = m > 0 ? m : 1;
-    // Operands twice as heavy per k-step: dense weights and two 4:2 streams.
-    const bool heavy = kind != NM_KIND_SP42;
+    // Operands twice as heavy per k-step in matrix work: the kinds that run the
+    // dense instruction (dense weights, and the mask layouts expanded to a
+    // dense tile).
+    const bool heavy = !kind_is_sp42(kind);
     // Rules fitted to an exhaustive timing of every tile on the ViT, DeiT and
     // Swin shapes (the paper's Table 1 methodology): above a few hundred
     // tokens the two-slot rings win -- their smaller LDS footprint keeps three
@@ -153,7 +180,11 @@ nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *
     plan->kind = kind;
     plan->tile = tile;
     plan->split_k = 1;
-    return complete_plan(kind, m, n, k_steps, plan);
+    // A compact weight is expanded inside every workgroup, ahead of its use,
+    // when few rows of output tiles share it; with many rows the expansion
+    // repeated per row costs more than one expansion pass per call.
+    plan->expand = kind_is_compact(kind) && ceil_div(mm, kTiles[tile].tile_m()) >= kExpandTileRows ? 1 : 0;
+    return complete_plan(kind, m, n, k, plan);
 }
 
 }  // namespace nmspmm

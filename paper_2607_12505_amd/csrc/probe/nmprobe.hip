@@ -135,9 +135,10 @@ extern "C" nm_status nm_probe_store_only(const nm_plan *plan, int m, int n, cons
         return NM_ERR_ARG;
     if (plan->tile < 0 || plan->tile >= kNumTiles || kTiles[plan->tile].layout != kOutSplit || plan->split_k != 1)
         return NM_ERR_ARG;
-    if (plan->kind != NM_KIND_SP42 && plan->kind != NM_KIND_SP42X2 && plan->kind != NM_KIND_DENSE) return NM_ERR_ARG;
+    if (!kind_is_valid(plan->kind)) return NM_ERR_ARG;
     nm_plan p = *plan;
-    nm_status st = complete_plan(p.kind, m, n, 1, &p);
+    p.expand = 0;
+    nm_status st = complete_plan(p.kind, m, n, 128, &p);
     if (st != NM_OK) return st;
     // Zero k-steps: the kernel issues no operand loads and no matrix
     // instructions; the epilogue stores the zero accumulators.  No operand

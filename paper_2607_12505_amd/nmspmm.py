@@ -22,13 +22,16 @@ LIB_PATH = os.path.join(_HERE, "libnmspmm.so")
 
 NM_OK, NM_ERR_ARG, NM_ERR_SHAPE, NM_ERR_PATTERN, NM_ERR_UNSUPPORTED, NM_ERR_WORKSPACE, NM_ERR_HIP = range(7)
 NM_OUT_I32, NM_OUT_F16, NM_OUT_I8 = 1, 2, 4
-NM_KIND_SP42, NM_KIND_SP42X2, NM_KIND_DENSE = 1, 2, 3
-NM_LAYOUT_SP42 = 1
+# kernel families; a packed layout and the family that consumes it share a number
+NM_KIND_SP42, NM_KIND_C14, NM_KIND_DENSE, NM_KIND_C18, NM_KIND_C28, NM_KIND_MK3, NM_KIND_MK4, NM_KIND_MK5 = range(1, 9)
+(NM_LAYOUT_SP42, NM_LAYOUT_C14, NM_LAYOUT_DENSE, NM_LAYOUT_C18, NM_LAYOUT_C28, NM_LAYOUT_MK3, NM_LAYOUT_MK4,
+ NM_LAYOUT_MK5) = range(1, 9)
+ALL_KINDS = tuple(range(1, 9))
 
 # Every symbol the header declares (checked by the CPU tests).
 EXPORTED = (
     "nm_status_string", "nm_compress_size", "nm_compress", "nm_decompress", "nm_num_tiles",
-    "nm_tile_info", "nm_plan_kernel_name", "nm_spmm_plan", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
+    "nm_tile_info", "nm_plan_kernel_name", "nm_spmm_plan", "nm_spmm_plan_complete", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
     "nm_spmm", "nm_spmm_ex", "nm_gemm_i8_dense", "nm_gemm_i8_dense_ex", "nm_spmm_out", "nm_gemm_i8_dense_out",
     "nm_quantize_f16", "nm_spmm_noalloc",
 )
@@ -37,14 +40,15 @@ NM_NOALLOC_SCRATCH_BYTES = 16384 + (32 << 20)
 
 class NmDesc(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int32), ("k", ctypes.c_int32), ("nm_n", ctypes.c_int32), ("nm_m", ctypes.c_int32),
-                ("streams", ctypes.c_int32), ("layout", ctypes.c_int32), ("n_frags", ctypes.c_int32),
+                ("kind", ctypes.c_int32), ("layout", ctypes.c_int32), ("n_frags", ctypes.c_int32),
                 ("k_steps", ctypes.c_int32), ("vals_bytes", ctypes.c_int64), ("meta_bytes", ctypes.c_int64),
                 ("bad_row", ctypes.c_int32), ("bad_group", ctypes.c_int32)]
 
 
 class NmPlan(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("tile", ctypes.c_int32), ("tile_n", ctypes.c_int32),
-                ("tile_m", ctypes.c_int32), ("split_k", ctypes.c_int32), ("grid", ctypes.c_int32)]
+                ("tile_m", ctypes.c_int32), ("split_k", ctypes.c_int32), ("grid", ctypes.c_int32),
+                ("expand", ctypes.c_int32), ("reserved", ctypes.c_int32), ("expand_bytes", ctypes.c_int64)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -95,6 +99,7 @@ def lib() -> ctypes.CDLL:
             "nm_tile_info": ([i32, ctypes.POINTER(i32), ctypes.POINTER(i32)], i32),
             "nm_plan_kernel_name": ([pp, ctypes.c_char_p, i32], i32),
             "nm_spmm_plan": ([pd, i32, i32, pp], i32),
+            "nm_spmm_plan_complete": ([pd, i32, pp], i32),
             "nm_gemm_i8_dense_plan": ([i32, i32, i32, i32, pp], i32),
             "nm_workspace_size": ([pp, i32, i32, ctypes.POINTER(sz)], i32),
             "nm_workspace_init": ([vp, sz, vp], i32),
@@ -137,12 +142,12 @@ class Packed:
 # ---------------------------------------------------------------------------
 # Packed-weight files: nm_compress runs once offline, so its output is kept on
 # disk.  Layout (little-endian): 8-byte magic, u32 version, u32 header bytes,
-# the descriptor's fields (8 x i32: n, k, nm_n, nm_m, streams, layout,
+# the descriptor's fields (8 x i32: n, k, nm_n, nm_m, kind, layout,
 # n_frags, k_steps; 2 x i64: vals_bytes, meta_bytes), CRC-32 of the values
 # and of the positions (2 x u32), then the values and the positions.
 
 PACKED_MAGIC = b"NMSPMM\x00\x01"
-PACKED_VERSION = 1
+PACKED_VERSION = 2
 _PACKED_HEAD = struct.Struct("<8sII8i2q2I")
 
 
@@ -151,7 +156,7 @@ def save_packed(path: str, p: "Packed") -> None:
     vals, meta = np.ascontiguousarray(p.vals).view(np.uint8), np.ascontiguousarray(p.meta).view(np.uint8)
     if vals.size != d.vals_bytes or meta.size != d.meta_bytes:
         raise ValueError("packed arrays do not match their descriptor")
-    head = _PACKED_HEAD.pack(PACKED_MAGIC, PACKED_VERSION, _PACKED_HEAD.size, d.n, d.k, d.nm_n, d.nm_m, d.streams,
+    head = _PACKED_HEAD.pack(PACKED_MAGIC, PACKED_VERSION, _PACKED_HEAD.size, d.n, d.k, d.nm_n, d.nm_m, d.kind,
                              d.layout, d.n_frags, d.k_steps, d.vals_bytes, d.meta_bytes,
                              zlib.crc32(vals.tobytes()), zlib.crc32(meta.tobytes()))
     with open(path, "wb") as f:
@@ -168,13 +173,13 @@ def load_packed(path: str) -> "Packed":
         raw = f.read()
     if len(raw) < _PACKED_HEAD.size:
         raise ValueError(f"{path}: truncated header")
-    (magic, version, hsize, n, k, nm_n, nm_m, streams, layout, n_frags, k_steps, vb, mb, cv,
+    (magic, version, hsize, n, k, nm_n, nm_m, kind, layout, n_frags, k_steps, vb, mb, cv,
      cm) = _PACKED_HEAD.unpack_from(raw)
     if magic != PACKED_MAGIC or version != PACKED_VERSION or hsize != _PACKED_HEAD.size:
         raise ValueError(f"{path}: not a packed-weight file of version {PACKED_VERSION}")
     want = compress_size(n, k, nm_n, nm_m)
-    got = (streams, layout, n_frags, k_steps, vb, mb)
-    if got != (want.streams, want.layout, want.n_frags, want.k_steps, want.vals_bytes, want.meta_bytes):
+    got = (kind, layout, n_frags, k_steps, vb, mb)
+    if got != (want.kind, want.layout, want.n_frags, want.k_steps, want.vals_bytes, want.meta_bytes):
         raise ValueError(f"{path}: descriptor does not match nm_compress_size({n}, {k}, {nm_n}, {nm_m})")
     if len(raw) != hsize + vb + mb:
         raise ValueError(f"{path}: {len(raw)} bytes, expected {hsize + vb + mb}")
@@ -243,15 +248,22 @@ def spmm_plan(desc: NmDesc, m: int, out_mode: int = NM_OUT_I32) -> NmPlan:
     return p
 
 
+def spmm_plan_complete(desc: NmDesc, m: int, plan: NmPlan) -> NmPlan:
+    """nm_spmm_plan_complete: a copy of a caller-built plan with the library's fields filled."""
+    p = NmPlan.from_buffer_copy(plan)
+    _check(lib().nm_spmm_plan_complete(ctypes.byref(desc), m, ctypes.byref(p)), "nm_spmm_plan_complete")
+    return p
+
+
 def dense_plan(m: int, n: int, k: int, out_mode: int = NM_OUT_I32) -> NmPlan:
     p = NmPlan()
     _check(lib().nm_gemm_i8_dense_plan(m, n, k, out_mode, ctypes.byref(p)), "nm_gemm_i8_dense_plan")
     return p
 
 
-def make_plan(kind: int, tile: int, split_k: int) -> NmPlan:
+def make_plan(kind: int, tile: int, split_k: int, expand: int = 0) -> NmPlan:
     p = NmPlan()
-    p.kind, p.tile, p.split_k = kind, tile, split_k
+    p.kind, p.tile, p.split_k, p.expand = kind, tile, split_k, expand
     return p
 
 
@@ -389,7 +401,7 @@ def spmm(X, w: DeviceWeight, Y=None, scale=None, Yh=None, plan: Optional[NmPlan]
     _on_device((("X", X), ("w.vals", w.vals), ("w.meta", w.meta), ("Y", Y), ("Yh", Yh), ("Yq", Yq),
                 ("scale", scale), ("qscale", qscale), ("ws", ws)))
     mode = _out_mode(Y, Yh, Yq)
-    p = plan if plan is not None else spmm_plan(w.desc, m, mode or NM_OUT_I32)
+    p = spmm_plan_complete(w.desc, m, plan) if plan is not None else spmm_plan(w.desc, m, mode or NM_OUT_I32)
     need = workspace_size(p, m, w.desc.n)
     if ws is None:
         ws, ws_bytes = _WS.get(need, X.device)

@@ -16,8 +16,8 @@
 #include "nmspmm.h"
 
 namespace nmspmm {
-nm_status make_plan(int kind, int m, int n, int k_steps, int out_mode, nm_plan *plan);
-nm_status complete_plan(int kind, int m, int n, int k_steps, nm_plan *plan);
+nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan);
+nm_status complete_plan(int kind, int m, int n, int k, nm_plan *plan);
 }
 
 #define CHECK(c)                                                      \
@@ -79,11 +79,11 @@ static void pack_round_trips() {
 }
 
 static void planner() {
-    for (int kind : {NM_KIND_SP42, NM_KIND_SP42X2, NM_KIND_DENSE})
+    for (int kind = NM_KIND_SP42; kind <= NM_KIND_MK5; ++kind)
         for (int rep = 0; rep < 400; ++rep) {
             const int m = rep % 7 == 0 ? 0 : uni(1, 200000), n = 4 * uni(1, 4096), ks = uni(1, 64);
             nm_plan p;
-            const nm_status s = nmspmm::make_plan(kind, m, n, ks, NM_OUT_I32 | NM_OUT_F16, &p);
+            const nm_status s = nmspmm::make_plan(kind, m, n, 128 * ks, NM_OUT_I32 | NM_OUT_F16, &p);
             CHECK(s == NM_OK || s == NM_ERR_SHAPE);
             if (s != NM_OK) continue;
             CHECK(p.split_k == 1 && p.grid >= 1 && p.tile_n >= 16 && p.tile_m >= 16);
@@ -93,7 +93,8 @@ static void planner() {
                     q.kind = kind;
                     q.tile = t;
                     q.split_k = split;
-                    const nm_status c = nmspmm::complete_plan(kind, m, n, ks, &q);
+                    q.expand = (t & 1) && kind != NM_KIND_SP42 && kind != NM_KIND_DENSE;
+                    const nm_status c = nmspmm::complete_plan(kind, m, n, 128 * ks, &q);
                     CHECK(c == NM_OK || c == NM_ERR_ARG || c == NM_ERR_SHAPE);
                     if (split == 3) CHECK(c == NM_ERR_ARG);
                 }

@@ -64,9 +64,9 @@ def test_status_strings():
 
 
 def test_struct_sizes_match_header():
-    # nm_desc: 8 int32 + 2 int64 + 2 int32 = 56 bytes; nm_plan: 6 int32
+    # nm_desc: 8 int32 + 2 int64 + 2 int32 = 56 bytes; nm_plan: 8 int32 + 1 int64
     assert ctypes.sizeof(nmspmm.NmDesc) == 56
-    assert ctypes.sizeof(nmspmm.NmPlan) == 24
+    assert ctypes.sizeof(nmspmm.NmPlan) == 40
     # nm_outputs: 5 pointers; nm_search_params: 4 int32 + 1 uint64
     assert ctypes.sizeof(nmspmm.NmOutputs) == 40
     assert ctypes.sizeof(nmsearch.NmSearchParams) == 24
@@ -96,13 +96,13 @@ def test_host_side_argument_checks_need_no_gpu():
     assert L.nm_quantize_f16(misaligned, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_ARG
     P = nmprobe.lib()
     assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, nul, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
-    assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42X2, fake, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
+    assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_C14, fake, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
     assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 0, 1, fake, nul, nul) == nmspmm.NM_ERR_ARG
     assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_DENSE, fake, 1, 0, fake, nul, nul) == nmspmm.NM_ERR_ARG
     assert P.nm_wall_clock_khz(None) == nmspmm.NM_ERR_ARG
     assert P.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, nul, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
     assert P.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42, fake, fake, nul, fake, nul) == nmspmm.NM_ERR_ARG
-    assert P.nm_probe_mfma_layout(nmspmm.NM_KIND_SP42X2, fake, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
+    assert P.nm_probe_mfma_layout(nmspmm.NM_KIND_C14, fake, fake, fake, fake, nul) == nmspmm.NM_ERR_ARG
     ok_plan = nmspmm.make_plan(nmspmm.NM_KIND_SP42, 0, 1)
     y_only = nmspmm.NmOutputs(fake.value, None, None, None, None)
     assert P.nm_probe_store_only(None, 64, 64, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_ARG
@@ -115,7 +115,7 @@ def test_host_side_argument_checks_need_no_gpu():
     assert P.nm_probe_store_only(ctypes.byref(ok_plan), 64, 64, ctypes.byref(fp16_no_scale), nul) == nmspmm.NM_ERR_ARG
     for bad in (nmspmm.make_plan(nmspmm.NM_KIND_SP42, 10, 1),      # k-sliced layout
                 nmspmm.make_plan(nmspmm.NM_KIND_SP42, 0, 2),       # split_k != 1
-                nmspmm.make_plan(7, 0, 1)):                         # unknown kind
+                nmspmm.make_plan(99, 0, 1)):                        # unknown kind
         assert P.nm_probe_store_only(ctypes.byref(bad), 64, 64, ctypes.byref(y_only), nul) == nmspmm.NM_ERR_ARG
 
 

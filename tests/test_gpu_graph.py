@@ -1,7 +1,7 @@
 """The GEMM entry points under HIP graph capture: a DeiT-Base layer's four
 linears at batch 1 (one sparse pattern each, plus the dense baseline and a
-split-K plan with its workspace cleared by the library's fill kernel) are
-captured once and replayed several times, with eager work and
+split-K plan with its workspace cleared by the library's fill kernel, and a
+compact weight expanded once per call into its workspace) are captured once and replayed several times, with eager work and
 synchronisations between replays; every replay must reproduce the eager
 outputs bit for bit, and the eager outputs match the oracle."""
 import numpy as np
@@ -55,6 +55,21 @@ def test_captured_layer_replays_bit_exactly():
     calls.append(split_call)
     outs.append(Ys)
     refs.append(oracle.matmul_i8(Xs, Ws))
+
+    # a compact weight expanded once per call into the workspace (the
+    # expansion kernel and the 4:2-operand kernel are both captured)
+    k, n = 1024, 768
+    Xe = rng.integers(-127, 128, (m, k), dtype=np.int8)
+    We = wl.random_nm(n, k, 2, 8, rng, full=True)
+    Xed = torch.from_numpy(Xe).cuda()
+    dwe = nmspmm.DeviceWeight.from_packed(nmspmm.compress(We, 2, 8))
+    plan_e = nmspmm.spmm_plan_complete(dwe.desc, m, nmspmm.make_plan(dwe.desc.kind, 0, 1, expand=1))
+    ws_e = torch.empty(nmspmm.workspace_size(plan_e, m, n), dtype=torch.uint8, device="cuda")
+    nmspmm.workspace_init(ws_e)
+    Ye = torch.empty((m, n), dtype=torch.int32, device="cuda")
+    calls.append(lambda: nmspmm.spmm(Xed, dwe, Y=Ye, ws=ws_e, plan=plan_e))
+    outs.append(Ye)
+    refs.append(oracle.matmul_i8(Xe, We))
 
     for c in calls:                      # eager run
         c()

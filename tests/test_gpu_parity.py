@@ -7,6 +7,8 @@ caught.  Small cases are compared element by element over every pattern, tile
 and split-K; the benchmark workloads are run at full size in the planner's
 launch configuration and compared at sampled positions.
 """
+import itertools
+
 import numpy as np
 import pytest
 
@@ -97,27 +99,36 @@ def test_extreme_values_and_fp16_overflow():
 
 # ---------------------------------------------------------------- schedule invariance
 
-@pytest.mark.parametrize("kind", [nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_SP42X2, nmspmm.NM_KIND_DENSE])
-def test_every_tile_and_split_is_bit_identical(kind):
-    # spans several tiles of every size plus ragged tails in m and n
-    m, n, k = 333, 404, 1024
-    N, M = {nmspmm.NM_KIND_SP42: (2, 8), nmspmm.NM_KIND_SP42X2: (4, 8), nmspmm.NM_KIND_DENSE: (8, 8)}[kind]
-    X, W, scale = _case(m, n, k, N, M, seed=kind)
+# one pattern per kernel family (the family nm_compress picks for it)
+KIND_PATTERN = {nmspmm.NM_KIND_SP42: (2, 4), nmspmm.NM_KIND_C14: (1, 4), nmspmm.NM_KIND_DENSE: (8, 8),
+                nmspmm.NM_KIND_C18: (1, 8), nmspmm.NM_KIND_C28: (2, 8), nmspmm.NM_KIND_MK3: (3, 8),
+                nmspmm.NM_KIND_MK4: (4, 8), nmspmm.NM_KIND_MK5: (5, 8)}
+
+
+@pytest.mark.parametrize("kind", nmspmm.ALL_KINDS)
+@pytest.mark.parametrize("m,n,k", [(333, 404, 1024), (130, 68, 320)])
+def test_every_tile_and_split_is_bit_identical(kind, m, n, k):
+    # spans several tiles of every size plus ragged tails in m, n and k
+    N, M = KIND_PATTERN[kind]
+    X, W, scale = _case(m, n, k, N, M, seed=kind + k)
     ref = oracle.matmul_i8(X, W)
     ref_h = oracle.dequant_f16(ref, scale)
     packed = nmspmm.compress(W, N, M)
+    assert packed.desc.kind == kind
     dw = nmspmm.DeviceWeight.from_packed(packed)
-    for tile in range(nmspmm.num_tiles()):
-        for split in (1, 2, 4, 8):
-            plan = nmspmm.make_plan(kind, tile, split)
-            nmspmm.workspace_size(plan, m, n)
-            print(f"kind {kind} tile {tile} split {split}", flush=True)
-            if kind == nmspmm.NM_KIND_DENSE:
-                Y, Yh = gu.run_dense(X, W, scale, True, True, plan=plan)
-            else:
-                Y, Yh = gu.run_sparse(X, packed, scale, True, True, plan=plan, dw=dw)
-            assert np.array_equal(Y, ref), (tile, split)
-            gu.assert_f16_close(Yh, ref_h)
+    compact = kind not in (nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_DENSE)
+    expands = (0, 1) if compact else (0,)
+    for tile, split, expand in itertools.product(range(nmspmm.num_tiles()), (1, 2, 4, 8), expands):
+        if split > max(1, -(-k // 128)):
+            continue  # more splits than k-steps
+        plan = nmspmm.make_plan(kind, tile, split, expand)
+        print(f"kind {kind} tile {tile} split {split} expand {expand} m={m} n={n} k={k}", flush=True)
+        if kind == nmspmm.NM_KIND_DENSE:
+            Y, Yh = gu.run_dense(X, W, scale, True, True, plan=plan)
+        else:
+            Y, Yh = gu.run_sparse(X, packed, scale, True, True, plan=plan, dw=dw)
+        assert np.array_equal(Y, ref), (tile, split, expand)
+        gu.assert_f16_close(Yh, ref_h)
 
 
 def test_repeated_split_k_runs_are_identical():

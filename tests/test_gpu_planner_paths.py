@@ -1,6 +1,7 @@
 """GPU parity along every branch of the adaptive-parallelism planner (Sec.
-4.3): one seeded shape per rule, for one-stream (2:4), two-stream (4:8) and
-dense weights, compared element by element with the oracle in the launch
+4.3): one seeded shape per rule, for 2:4 (stored 4:2 operand), 1:4, 1:8 and
+2:8 (compact, expanded to the 4:2 operand), 4:8 (mask layout expanded to a
+dense tile) and dense weights, compared element by element with the oracle in the launch
 configuration the planner picks (int32 and fp16 outputs, guard bands after
 both).  The expected tile of each case documents the rule it exercises; the
 last cases launch with the grouped tile order that large weights take."""
@@ -19,7 +20,7 @@ CASES = [
     (100, 256, 256, "sp", (32, 32), True),      # few tokens: k-sliced 32 x 32
     (100, 256, 128, "sp", (32, 32), True),      # ... also with a single k-step
     (512, 1024, 256, "dn", (32, 64), True),     # heavier operands past one tile per CU: 64 tokens
-    (512, 1024, 256, "x2", (32, 64), True),
+    (512, 1024, 256, "mk", (32, 64), True),
     (197, 2304, 256, "dn", (64, 32), True),     # ... or 64 channels when 64 tokens pad m too much
     (512, 1024, 128, "dn", (64, 64), False),    # ... and 64 x 64 with a single k-step
     (400, 4096, 128, "sp", (64, 64), False),    # more than 2 k-sliced tiles per CU: 64 x 64
@@ -27,19 +28,29 @@ CASES = [
     (3000, 256, 128, "sp", (64, 64), False),    # ... narrower: 64 x 64
     (3000, 512, 256, "sp", (64, 64), False),    # two k-steps: 64 x 64
     (2000, 768, 384, "sp", (128, 32), False),   # three k-steps, one stream: 128 x 32
-    (2000, 768, 384, "x2", (64, 64), False),    # ... heavier operands: 64 x 64
+    (2000, 768, 384, "mk", (64, 64), False),    # ... heavier operands: 64 x 64
     (4000, 1024, 1024, "sp", (128, 128), False),  # medium, long reduction: 128 x 128
     (1600, 2304, 768, "sp", (128, 64), False),  # medium: half-height tiles
     (1600, 2304, 768, "dn", (64, 128), False),  # ... narrower for the heavier operands
     (6272, 1536, 512, "sp", (64, 64), False),   # ... 64 x 64 past 4 half-height tiles per CU
     (8192, 2048, 512, "sp", (128, 128), False),  # large: 128 x 128
-    (4096, 4096, 3072, "x2", (256, 256), False),  # large, heavier operands, 4096 wide, long reduction: 256 x 256
-    (4096, 4096, 512, "x2", (128, 128), False),   # ... shorter reduction: 128 x 128 on 8 waves
+    (4096, 4096, 3072, "mk", (256, 256), False),  # large, heavier operands, 4096 wide, long reduction: 256 x 256
+    (4096, 4096, 512, "mk", (128, 128), False),   # ... shorter reduction: 128 x 128 on 8 waves
     # weights of 3.5 MiB or more over at least 64 rows of tiles: tiles walked in groups of 8 rows
     (8300, 3072, 2048, "sp", (128, 128), False),  # 65 tile rows: the last group has one row
-    (8192, 3072, 1024, "x2", (128, 128), False),
+    (8192, 3072, 1024, "mk", (128, 128), False),
     (8192, 2048, 2048, "dn", (128, 128), False),
+    # the compact kinds on the same rules
+    (100, 256, 256, "c14", (32, 32), True),
+    (100, 256, 256, "c18", (32, 32), True),
+    (197, 2304, 256, "c28", (32, 32), True),
+    (3000, 512, 128, "c18", (128, 32), False),
+    (2000, 768, 384, "c28", (128, 32), False),
+    (1600, 2304, 768, "c14", (128, 64), False),
+    (8192, 2048, 512, "c28", (128, 128), False),
+    (8300, 3072, 2048, "c18", (128, 128), False),
 ]
+PATTERN = {"sp": (2, 4), "mk": (4, 8), "c14": (1, 4), "c18": (1, 8), "c28": (2, 8)}
 
 
 @pytest.mark.parametrize("m,n,k,kind,tile,ks", CASES)
@@ -53,7 +64,7 @@ def test_planner_branch_matches_oracle(m, n, k, kind, tile, ks):
         plan = nmspmm.dense_plan(m, n, k, nmspmm.NM_OUT_I32 | nmspmm.NM_OUT_F16)
     else:
         from paper_2607_12505_amd import workloads as wl
-        N, M = (2, 4) if kind == "sp" else (4, 8)
+        N, M = PATTERN[kind]
         W = wl.random_nm(n, k, N, M, rng, full=True)
         packed = nmspmm.compress(W, N, M)
         plan = nmspmm.spmm_plan(packed.desc, m, nmspmm.NM_OUT_I32 | nmspmm.NM_OUT_F16)

@@ -55,7 +55,7 @@ def test_bench_reports_positive_rates():
 
 @pytest.mark.parametrize("m,n", [(1000, 260), (12608, 1152), (33, 4)])
 def test_store_only_probe_writes_zeros_exactly_in_the_outputs(m, n):
-    # every output-split tile of all three kinds, on ragged shapes, with and
+    # every output-split tile of every kind, on ragged shapes, with and
     # without the multiplier arrays: the probe writes the empty-sum values into
     # [m x n] and nothing past it
     import torch
@@ -64,7 +64,7 @@ def test_store_only_probe_writes_zeros_exactly_in_the_outputs(m, n):
     bigQ = torch.full((m * n + 4096,), 7, dtype=torch.int8, device="cuda")
     scale = torch.full((n,), 0.5, dtype=torch.float32, device="cuda")
     Y, Yh, Yq = bigY[:m * n].view(m, n), bigH[:m * n].view(m, n), bigQ[:m * n].view(m, n)
-    for kind in (nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_SP42X2, nmspmm.NM_KIND_DENSE):
+    for kind in nmspmm.ALL_KINDS:
         for tile in range(nmspmm.num_tiles()):
             for with_scales in (True, False):
                 plan = nmspmm.make_plan(kind, tile, 1)

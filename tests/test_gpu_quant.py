@@ -105,7 +105,7 @@ def test_requant_epilogue(kind, plan):
         N, M = map(int, kind.split(":"))
         W = wl.random_nm(n, k, N, M, rng, full=True)
         packed = nmspmm.compress(W, N, M)
-        kid = nmspmm.NM_KIND_SP42 if packed.desc.streams == 1 else nmspmm.NM_KIND_SP42X2
+        kid = packed.desc.kind
     ref = oracle.matmul_i8(X, W)
     qs = qscales(ref, rng)
     scale = rng.uniform(1e-6, 1e-3, n).astype(np.float32)

@@ -18,7 +18,7 @@ def test_packed_file_round_trip(tmp_path, N, M):
     nmspmm.save_packed(str(f), p)
     q = nmspmm.load_packed(str(f))
     assert np.array_equal(q.vals, p.vals) and np.array_equal(q.meta, p.meta)
-    assert (q.desc.n, q.desc.k, q.desc.nm_n, q.desc.nm_m, q.desc.streams) == (64, 256, N, M, p.desc.streams)
+    assert (q.desc.n, q.desc.k, q.desc.nm_n, q.desc.nm_m, q.desc.kind) == (64, 256, N, M, p.desc.kind)
     # and it still decodes to W
     assert np.array_equal(nmspmm.decompress(q), W)
 

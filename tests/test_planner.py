@@ -28,17 +28,25 @@ def test_plan_rules(shape):
     d = nmspmm.compress_size(n, k, N, M)
     for out in (nmspmm.NM_OUT_I32, nmspmm.NM_OUT_F16, nmspmm.NM_OUT_I32 | nmspmm.NM_OUT_F16):
         p = nmspmm.spmm_plan(d, m, out)
-        assert p.kind == (nmspmm.NM_KIND_SP42 if N <= 2 else nmspmm.NM_KIND_SP42X2)
+        assert p.kind == d.kind
         assert p.split_k in (1, 2, 4, 8)
         tn, tm = nmspmm.tile_info(p.tile)
         tiles = -(-n // tn) * -(-m // tm)
-        if "k_gemm_rs" in nmspmm.plan_kernel_name(p):
-            # row-stationary: a fixed grid, each workgroup walking several tiles
-            assert 0 < p.grid <= tiles and p.grid % CUS == 0
+        assert p.grid == tiles * p.split_k
+        # the reduction is split inside workgroups, never across them; a
+        # compact weight shared by many rows of output tiles is expanded once
+        # per call into the workspace, past the counter block
+        assert p.split_k == 1
+        rows = -(-m // tm)
+        compact = d.layout not in (nmspmm.NM_LAYOUT_SP42, nmspmm.NM_LAYOUT_DENSE)
+        assert p.expand == int(compact and rows >= 32)
+        if p.expand:
+            F, S = -(-n // 16), -(-k // 128)
+            want = F * S * 1280 if d.kind in (nmspmm.NM_KIND_C14, nmspmm.NM_KIND_C18, nmspmm.NM_KIND_C28) else n * k
+            assert p.expand_bytes == want
+            assert nmspmm.workspace_size(p, m, n) == 16384 + want
         else:
-            assert p.grid == tiles * p.split_k
-        # the reduction is split inside workgroups, never across them
-        assert p.split_k == 1 and nmspmm.workspace_size(p, m, n) == 0
+            assert p.expand_bytes == 0 and nmspmm.workspace_size(p, m, n) == 0
         # deterministic
         q = nmspmm.spmm_plan(d, m, out)
         assert q.as_dict() == p.as_dict()
@@ -80,8 +88,9 @@ def test_large_shapes_use_large_tiles():
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # DeiT-Base fc1 at batch 128
     assert nmspmm.plan_kernel_name(p) == "k_gemm<1, 4, 2, 2, 4, 2>"   # 128 x 128 on 8 waves, 2-slot ring
     d = nmspmm.compress_size(3072, 1024, 4, 8)
-    p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)    # ViT-L qkv, two-stream weight
-    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 4, 2, 2, 4, 2>"
+    p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)    # ViT-L qkv, 4:8 weight: expanded once, dense kernel
+    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<3, 4, 2, 2, 4, 2>"
+    assert p.expand == 1
     # one-stream weights on the widest outputs or with long reductions: the
     # 4-wave 128 x 128 tile (ViT-L fc1, DeiT-B fc2 at batch 128)
     d = nmspmm.compress_size(4096, 1024, 2, 4)
@@ -93,13 +102,13 @@ def test_large_shapes_use_large_tiles():
     # the widest outputs of the heavier operands with long reductions: 256 x 256 on 8 waves
     d = nmspmm.compress_size(4096, 4096, 4, 8)
     p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)
-    assert (p.tile_n, p.tile_m) == (256, 256) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 2, 4, 8, 4, 3>"
+    assert (p.tile_n, p.tile_m) == (256, 256) and nmspmm.plan_kernel_name(p) == "k_gemm<3, 2, 4, 8, 4, 3>"
     p = nmspmm.dense_plan(18464, 8192, 3072, nmspmm.NM_OUT_I32)
     assert (p.tile_n, p.tile_m) == (256, 256)
     # ... and 128 x 128 on 8 waves for shorter ones (ViT-L fc1, 4:8 and its dense baseline)
     d = nmspmm.compress_size(4096, 1024, 4, 8)
     p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)
-    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<2, 4, 2, 2, 4, 2>"
+    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<3, 4, 2, 2, 4, 2>"
     p = nmspmm.dense_plan(18464, 4096, 1024, nmspmm.NM_OUT_I32)
     assert nmspmm.plan_kernel_name(p) == "k_gemm<3, 4, 2, 2, 4, 2>"
     d = nmspmm.compress_size(4096, 1024, 2, 4)           # one-stream weight: 128 x 128
@@ -108,14 +117,14 @@ def test_large_shapes_use_large_tiles():
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # fc2 at batch 128
     assert (p.tile_n, p.tile_m) == (128, 128)
     # three k-steps (DeiT-Small, k = 384): 128 channels x 32 tokens for
-    # one-stream weights, 64 x 64 for two streams
+    # 4:2-operand weights, 64 x 64 for the dense-tile ones
     d = nmspmm.compress_size(1152, 384, 2, 4)
     assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 12608, 1)) == "k_gemm<1, 2, 2, 4, 1, 2>"
     d = nmspmm.compress_size(1152, 384, 4, 8)
-    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 12608, 1)) == "k_gemm<2, 2, 2, 2, 2, 2>"
+    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 12608, 1)) == "k_gemm<3, 2, 2, 2, 2, 2>"  # expanded once
     d = nmspmm.compress_size(384, 384, 2, 4)
     assert (nmspmm.spmm_plan(d, 12608, 1).tile_n, nmspmm.spmm_plan(d, 12608, 1).tile_m) == (128, 32)
-    # medium token counts: half-height tiles, narrower for two-stream weights
+    # medium token counts: half-height tiles, narrower for the dense-tile weights
     # (DeiT-B qkv at batch 8, k = 768)
     d = nmspmm.compress_size(2304, 768, 2, 4)
     assert (nmspmm.spmm_plan(d, 1576, 1).tile_n, nmspmm.spmm_plan(d, 1576, 1).tile_m) == (128, 64)
@@ -149,6 +158,25 @@ def test_large_shapes_use_large_tiles():
     assert nmspmm.dense_plan(100352, 384, 128, 1).tile_m == 64
     d = nmspmm.compress_size(768, 256, 2, 4)
     assert (nmspmm.spmm_plan(d, 25088, 1).tile_n, nmspmm.spmm_plan(d, 25088, 1).tile_m) == (64, 64)
+
+
+def test_forced_plan_completion():
+    d = nmspmm.compress_size(768, 1024, 1, 8)
+    p = nmspmm.spmm_plan_complete(d, 5000, nmspmm.make_plan(nmspmm.NM_KIND_C18, 0, 2, expand=1))
+    assert p.expand_bytes == 48 * 8 * 1280 and (p.tile_n, p.tile_m) == (128, 128)
+    # expanded weight after the counters and the split-K partials, 256-aligned
+    part = 16384 + 2 * 5000 * 768 * 4
+    assert nmspmm.workspace_size(p, 5000, 768) == -(-part // 256) * 256 + 48 * 8 * 1280
+    with pytest.raises(nmspmm.NmError):      # only compact kinds expand
+        nmspmm.spmm_plan_complete(nmspmm.compress_size(768, 1024, 2, 4), 100,
+                                  nmspmm.make_plan(nmspmm.NM_KIND_SP42, 0, 1, expand=1))
+    with pytest.raises(nmspmm.NmError):      # the descriptor's kind
+        nmspmm.spmm_plan_complete(d, 100, nmspmm.make_plan(nmspmm.NM_KIND_C14, 0, 1))
+    with pytest.raises(nmspmm.NmError):      # expand is 0 or 1
+        nmspmm.spmm_plan_complete(d, 100, nmspmm.make_plan(nmspmm.NM_KIND_C18, 0, 1, expand=2))
+    dm = nmspmm.compress_size(768, 1024, 4, 8)
+    p = nmspmm.spmm_plan_complete(dm, 100, nmspmm.make_plan(nmspmm.NM_KIND_MK4, 3, 1, expand=1))
+    assert p.expand_bytes == 768 * 1024
 
 
 def test_forced_plan_validation():

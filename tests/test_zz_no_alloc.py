@@ -29,8 +29,9 @@ def _outputs(torch, m, n):
             torch.full((m, n), 99, dtype=torch.int8, device="cuda"))
 
 
-# (plan as (tile, split_k) or None for the planner's, pattern)
-CASES = [((3, 2), (2, 4)), ((10, 4), (2, 4)), ((0, 8), (1, 8)), ((7, 2), (4, 8)), (None, (2, 4))]
+# (plan as (tile, split_k, expand) or None for the planner's, pattern)
+CASES = [((3, 2, 0), (2, 4)), ((10, 4, 0), (2, 4)), ((0, 8, 0), (1, 8)), ((7, 2, 0), (4, 8)), (None, (2, 4)),
+         ((0, 2, 1), (2, 8)), ((3, 1, 1), (4, 8))]
 
 
 @pytest.mark.parametrize("plan,pat", CASES)
@@ -43,8 +44,8 @@ def test_noalloc_matches_workspace_call(plan, pat):
     X2 = np.random.default_rng(6).integers(-128, 128, (second[0], second[2])).astype(np.int8)
     packed = nmspmm.compress(W, N, M)
     dw = nmspmm.DeviceWeight.from_packed(packed)
-    kind = nmspmm.NM_KIND_SP42 if packed.desc.streams == 1 else nmspmm.NM_KIND_SP42X2
-    p = None if plan is None else nmspmm.make_plan(kind, plan[0], plan[1])
+    kind = packed.desc.kind
+    p = None if plan is None else nmspmm.make_plan(kind, *plan)
     sd, qd = torch.from_numpy(scale).cuda(), torch.from_numpy(qscale).cuda()
     for X in (X1, X2):
         m, n = X.shape[0], W.shape[0]
