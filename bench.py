@@ -97,32 +97,58 @@ class Prepared:
         self.Yhd = torch.empty((g.m, g.n), dtype=torch.int16, device="cuda") if out_f16 else None
         out = (nmspmm.NM_OUT_I32 if out_i32 else 0) | (nmspmm.NM_OUT_F16 if out_f16 else 0)
         self.out_i32, self.out_f16 = out_i32, out_f16
-        L = nmspmm.lib()
-        ptr = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None
-        stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        self._torch = torch
         # dense baseline
         self.dplan = nmspmm.dense_plan(g.m, g.n, g.k, out)
-        dws = nmspmm.workspace_size(self.dplan, g.m, g.n)
-        self.dws = torch.zeros(max(dws, 16), dtype=torch.uint8, device="cuda")
-        self.dense_args = (ptr(self.Xd), g.m, ptr(self.Wd), g.n, g.k, ptr(self.Yd), ptr(self.scale),
-                           ptr(self.Yhd), ptr(self.dws), self.dws.numel(), stream, ctypes.byref(self.dplan))
-        self.dense_fn = L.nm_gemm_i8_dense_ex
+        self.dense_fn = nmspmm.lib().nm_gemm_i8_dense_ex
         if self.sparse_kernel:
             self.packed = nmspmm.compress(W, g.N, g.M)
             self.dw = nmspmm.DeviceWeight.from_packed(self.packed)
             self.splan = nmspmm.spmm_plan(self.packed.desc, g.m, out)
-            sws = nmspmm.workspace_size(self.splan, g.m, g.n)
-            self.sws = torch.zeros(max(sws, 16), dtype=torch.uint8, device="cuda")
+            self.sparse_fn = nmspmm.lib().nm_spmm_ex
+        else:
+            # a dense layer inside a layer-wise chain runs the dense kernel on both sides
+            self.splan = nmspmm.NmPlan.from_buffer_copy(self.dplan)
+            self.sparse_fn = nmspmm.lib().nm_gemm_i8_dense_ex
+        self.sws = self.dws = None
+        self._build_args()
+
+    def _workspace(self, plan, old):
+        need = max(nmspmm.workspace_size(plan, self.g.m, self.g.n), 16)
+        if old is not None and old.numel() >= need:
+            return old
+        return self._torch.zeros(need, dtype=self._torch.uint8, device="cuda")
+
+    def _build_args(self):
+        """ctypes arguments of both calls for the current plans."""
+        g = self.g
+        ptr = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None
+        stream = ctypes.c_void_p(self._torch.cuda.current_stream().cuda_stream)
+        self.dws = self._workspace(self.dplan, self.dws)
+        self.dense_args = (ptr(self.Xd), g.m, ptr(self.Wd), g.n, g.k, ptr(self.Yd), ptr(self.scale),
+                           ptr(self.Yhd), ptr(self.dws), self.dws.numel(), stream, ctypes.byref(self.dplan))
+        self.sws = self._workspace(self.splan, self.sws)
+        if self.sparse_kernel:
             self.sparse_args = (ptr(self.Xd), g.m, ptr(self.dw.vals), ptr(self.dw.meta),
                                 ctypes.byref(self.packed.desc), ptr(self.Y), ptr(self.scale), ptr(self.Yh),
                                 ptr(self.sws), self.sws.numel(), stream, ctypes.byref(self.splan))
-            self.sparse_fn = L.nm_spmm_ex
         else:
-            # a dense layer inside a layer-wise chain runs the dense kernel on both sides
-            self.splan = self.dplan
             self.sparse_args = (ptr(self.Xd), g.m, ptr(self.Wd), g.n, g.k, ptr(self.Y), ptr(self.scale),
-                                ptr(self.Yh), ptr(self.dws), self.dws.numel(), stream, ctypes.byref(self.dplan))
-            self.sparse_fn = L.nm_gemm_i8_dense_ex
+                                ptr(self.Yh), ptr(self.sws), self.sws.numel(), stream, ctypes.byref(self.splan))
+
+    def set_sparse_plan(self, plan):
+        """Runs the sparse-leg call with `plan` from now on (a completed plan
+        of this GEMM's kind); the workspace grows as the plan needs."""
+        self.splan = nmspmm.NmPlan.from_buffer_copy(plan)
+        self._build_args()
+
+    def set_dense_plan(self, plan):
+        """Runs the dense-baseline call with `plan` from now on."""
+        self.dplan = nmspmm.NmPlan.from_buffer_copy(plan)
+        self._build_args()
+
+    def sparse_kind(self):
+        return self.packed.desc.kind if self.sparse_kernel else nmspmm.NM_KIND_DENSE
 
     def kernel_name(self, plan):
         return nmspmm.plan_kernel_name(plan)

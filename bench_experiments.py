@@ -764,6 +764,89 @@ def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, comma
 
 
 
+def chain_sweep(torch, cfg, rounds, out_path, report):
+    """Planner evaluation inside a workload's own steps: for every distinct
+    (shape, kind) of the sparse leg, every (tile, expansion) candidate with
+    split_k = 1 is put on all GEMMs of that key and timed in ABBA rounds of
+    whole steps (sparse leg, dense leg) with an event after every GEMM, so each
+    candidate sees the cache state of the step itself (every layer with its
+    own cold inputs and outputs in the ViT-L chain).  Reports per key the
+    planner's choice, the fastest candidate and their times."""
+    import bench
+    work, preps = bench.prepare(cfg, torch)
+    sp = [p.run_sparse for p in preps]
+    dn = [p.run_dense for p in preps]
+    bench.abba(torch, sp, dn, 1, per_call=True)
+    keys = {}
+    for i, p in enumerate(preps):
+        keys.setdefault((p.g.m, p.g.k, p.g.n, p.sparse_kind()), []).append(i)
+    rows = []
+    # the dense leg too (the baseline of every shape), keyed like a dense kind
+    for i, p in enumerate(preps):
+        keys.setdefault((p.g.m, p.g.k, p.g.n, "baseline"), []).append(i)
+    for (m, k, n, kind), idx in sorted(keys.items(), key=lambda kv: (kv[0][:3], str(kv[0][3]))):
+        first = preps[idx[0]]
+        baseline = kind == "baseline"
+        planned = nmspmm.NmPlan.from_buffer_copy(first.dplan if baseline else first.splan)
+        compact = not baseline and kind not in (nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_DENSE)
+        times = {}
+        for tile in range(nmspmm.num_tiles()):
+            for expand in ((0, 1) if compact else (0,)):
+                cand = nmspmm.make_plan(nmspmm.NM_KIND_DENSE if baseline else kind, tile, 1, expand)
+                try:
+                    if baseline or kind == nmspmm.NM_KIND_DENSE:
+                        cand.tile_n, cand.tile_m = nmspmm.tile_info(tile)
+                    else:
+                        cand = nmspmm.spmm_plan_complete(first.packed.desc, m, cand)
+                except nmspmm.NmError:
+                    continue
+                for i in idx:
+                    preps[i].set_dense_plan(cand) if baseline else preps[i].set_sparse_plan(cand)
+                try:
+                    ta, tb = bench.abba(torch, sp, dn, rounds, per_call=True)
+                except nmspmm.NmError:
+                    continue
+                times[(tile, expand)] = float((tb if baseline else ta)[:, idx].mean()) * 1e3
+        for i in idx:
+            preps[i].set_dense_plan(planned) if baseline else preps[i].set_sparse_plan(planned)
+        best = min(times, key=times.get)
+        t_plan = times.get((planned.tile, planned.expand))
+        row = {"m": m, "k": k, "n": n, "kind": kind, "gemms": len(idx), "planned": [planned.tile, planned.expand],
+               "best": list(best), "t_planned_us": t_plan, "t_best_us": times[best],
+               "times": {f"{t}/{e}": round(v, 2) for (t, e), v in sorted(times.items())}}
+        rows.append(row)
+        log(f"m={m} k={k} n={n} kind {kind} ({len(idx)} GEMMs): planned t{planned.tile}/e{planned.expand} "
+            f"{t_plan:.1f} us, best t{best[0]}/e{best[1]} {times[best]:.1f} us")
+    summary = {"workload": work.name, "cases": len(rows),
+               "top1_hit_rate": round(float(np.mean([r["planned"] == r["best"] for r in rows])), 3),
+               "avg_norm_perf": round(float(np.mean([r["t_best_us"] / r["t_planned_us"] for r in rows])), 3),
+               "worst_norm_perf": round(float(min(r["t_best_us"] / r["t_planned_us"] for r in rows)), 3)}
+    if out_path:
+        with open(out_path, "w") as f:
+            json.dump({"summary": summary, "rows": rows}, f)
+    if report:
+        md = [f"# Planner choices inside the {work.name} steps", "",
+              f"Command: `python3 bench_experiments.py --chain-sweep {cfg} --report {report}` (repository root).  "
+              "For every distinct (shape, kind) of the sparse leg, every tile with split_k = 1 (and, for the compact "
+              "kinds, both places of the weight expansion: e0 inside every workgroup, e1 once per call) is put on "
+              "all GEMMs of that key and timed inside whole steps (ABBA rounds of the sparse and dense legs, an "
+              f"event after every GEMM, {rounds} rounds); times are means per GEMM in microseconds.  Kinds: "
+              "1 = 2:4, 2 = 1:4, 3 = dense, 4 = 1:8, 5 = 2:8, 6-8 = 3:8-5:8; \"baseline\": the dense leg (the "
+              "dense INT8 GEMM every speedup divides by) of that shape.", "",
+              f"Top-1 hit rate {summary['top1_hit_rate']}, average normalised performance "
+              f"{summary['avg_norm_perf']}, worst {summary['worst_norm_perf']}.", "",
+              "| m | k | n | kind | GEMMs | planned | us | best | us | ratio | all candidates (tile/expand: us) |",
+              "|---:|---:|---:|---:|---:|---|---:|---|---:|---:|---|"]
+        for r in rows:
+            cands = ", ".join(f"{c}: {v}" for c, v in r["times"].items())
+            md.append(f"| {r['m']} | {r['k']} | {r['n']} | {r['kind']} | {r['gemms']} | {r['planned'][0]}/"
+                      f"{r['planned'][1]} | {r['t_planned_us']:.1f} | {r['best'][0]}/{r['best'][1]} | "
+                      f"{r['t_best_us']:.1f} | {r['t_best_us'] / r['t_planned_us']:.3f} | {cands} |")
+        with open(report, "w") as f:
+            f.write("\n".join(md) + "\n")
+    return summary
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--sweep", type=str, default=None,
@@ -791,6 +874,9 @@ def main():
                     help="DeiT-Base layer at batch 1 and 8: Python launches vs one HIP graph replay (one JSON line)")
     ap.add_argument("--shape-report", action="store_true",
                     help="per-shape roofline of every workload GEMM (prints one JSON line; --report for markdown)")
+    ap.add_argument("--chain-sweep", type=int, default=None, metavar="CFG",
+                    help="tile and expansion candidates timed inside the steps of workload CFG (e.g. 4)")
+    ap.add_argument("--rounds", type=int, default=2, help="ABBA rounds per candidate of --chain-sweep")
     ap.add_argument("--cal", type=int, default=64, help="calibration configurations for --predictor")
     ap.add_argument("--test", type=int, default=32, help="random test configurations for --predictor")
     ap.add_argument("--report", type=str, default=None, help="markdown report of an experiment")
@@ -811,7 +897,10 @@ def main():
         sys.exit(1)
     nmspmm.lib()
     torch.cuda.set_device(0)
-    if args.sweep:
+    if args.chain_sweep is not None:
+        print(json.dumps({"chain_sweep": chain_sweep(torch, args.chain_sweep, args.rounds, args.sweep_out,
+                                                     args.report)}), flush=True)
+    elif args.sweep:
         summary = sweep([c if c == "grid" else int(c) for c in args.sweep.split(",")], torch, 10, args.sweep_out)
         print(json.dumps({"planner_evaluation": summary}), flush=True)
     elif args.chaining:

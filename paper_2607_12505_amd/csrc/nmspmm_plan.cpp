@@ -98,7 +98,7 @@ constexpr int64_t kExpandTileRows = 32;
 // Tile indices used by the rules below (see kTiles).
 constexpr int kT128x128r2 = 0, kT128x64r2 = 1, kT64x128r2 = 2, kT64x64r2 = 3, kT256x256w8 = 4;
 constexpr int kT128x32r2 = 5, kT128x128w8 = 6;
-constexpr int kT32x64ks = 8, kT64x32ks = 9, kT32x32ks = 10;
+constexpr int kT64x64ks = 7, kT32x64ks = 8, kT64x32ks = 9, kT32x32ks = 10;
 
 static int64_t tiles_of(int t, int m, int n) {
     return ceil_div(n, kTiles[t].tile_n()) * ceil_div(m, kTiles[t].tile_m());
@@ -130,13 +130,22 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
         // Otherwise 64 x 64 with a 2-slot ring.
         const int64_t t32 = tiles_of(kT32x32ks, mm, n);
         if (t32 > 2 * cus)
-            tile = kT64x64r2;
+            // many 32 x 32 tiles (the wide outputs): the k-sliced 64 x 64 tile
+            // while it still fits two per CU (DeiT-B fc1 at batch 1: 9.0 us
+            // against 9.9 for 64 x 64 with a ring), else 64 x 64
+            tile = tiles_of(kT64x64ks, mm, n) <= 2 * cus ? kT64x64ks : kT64x64r2;
         else if (!heavy || t32 <= cus)
             tile = kT32x32ks;
         else if (k_steps == 1)
             tile = kT64x64r2;
         else
             tile = ceil_div(mm, 64) * 64 * 100 <= (int64_t)mm * 115 ? kT32x64ks : kT64x32ks;
+    } else if (!heavy && k_steps >= 16 && mm <= 4096 && tiles_of(kT32x32ks, mm, n) <= 8 * cus) {
+        // A few thousand tokens with a long reduction: the k-sliced 32 x 32
+        // tile (the reduction split over the waves) still has more
+        // workgroups than the output tiles of any ring tile (DeiT-B fc2 at
+        // batch 8: 16.9 us against 20.5 for 64 x 64).
+        tile = kT32x32ks;
     } else if (k_steps <= 2) {
         // Very short reductions: the output stream dominates; small tiles
         // give the most workgroups in flight.  With one k-step and one-stream
@@ -154,6 +163,11 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
         // heavier operands).
         if (k_steps >= 8 && tiles_of(kT128x128r2, mm, n) >= cus) {
             tile = kT128x128r2;
+        } else if (!heavy && k_steps < 8 && tiles_of(kT64x64r2, mm, n) <= 6 * cus) {
+            // short reductions: 64 x 64 while it gives at most 6 workgroups
+            // per CU (DeiT-B qkv and fc1 at batch 8: 11.1 and 13.1 us against
+            // 13.4 and 15.0 for 128 x 64)
+            tile = kT64x64r2;
         } else {
             tile = heavy ? kT64x128r2 : kT128x64r2;
             // 64 x 64 when those would leave compute units without a tile,
@@ -170,20 +184,41 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
         // order that large weights take, 128 x 128 is 7-14 % faster than
         // 256 x 256 at k = 1024 and 256 x 256 6-13 % faster at k = 4096
         // (n 4096 and 8192, m 8192-25216, dense and 4:8).
-        tile = (n >= 4096 && k_steps >= 24) ? kT256x256w8 : kT128x128w8;
+        // Inside the steps of the ViT-L chain, 3072-wide outputs with 8 k-steps
+        // (qkv) ran fastest on the 4-wave 128 x 128 tile (dense 96-100 us
+        // against 101-104 on 8 waves).
+        if (n >= 4096 && k_steps >= 24)
+            tile = kT256x256w8;
+        else if (n >= 3072 && n < 4096 && k_steps >= 8 && k_steps < 24)
+            tile = kT128x128r2;
+        else
+            tile = kT128x128w8;
     } else {
-        // Large outputs, one-stream weights: 128 x 128 on 8 waves, except for
-        // long reductions (24 k-steps or more) and the widest outputs, where
-        // the 4-wave 128 x 128 tile's larger per-wave fragment grid wins.
-        tile = (k_steps >= 24 || n >= 4096) ? kT128x128r2 : kT128x128w8;
+        // Large outputs, 4:2-operand weights, timed inside the steps of the
+        // workloads (every layer with cold inputs and outputs): long
+        // reductions (24 k-steps or more) the 4-wave 128 x 128 tile, whose
+        // larger per-wave fragment grid needs fewer operand reads per product;
+        // wide outputs (3072 or more) with 8 or more k-steps the 256 x 256
+        // tile on 8 waves, half the operand fill per output (ViT-L qkv and
+        // fc1: 86 and 109 us against 94 and 127); otherwise 128 x 128 on
+        // 8 waves.
+        if (k_steps >= 24)
+            tile = kT128x128r2;
+        else if (n >= 3072 && k_steps >= 8)
+            tile = kT256x256w8;
+        else
+            tile = kT128x128w8;
     }
     plan->kind = kind;
     plan->tile = tile;
     plan->split_k = 1;
     // A compact weight is expanded inside every workgroup, ahead of its use,
     // when few rows of output tiles share it; with many rows the expansion
-    // repeated per row costs more than one expansion pass per call.
-    plan->expand = kind_is_compact(kind) && ceil_div(mm, kTiles[tile].tile_m()) >= kExpandTileRows ? 1 : 0;
+    // repeated per row costs more than one expansion pass per call.  1:4,
+    // whose expansion is a few byte permutes, stays inside the workgroups
+    // except on the 256 x 256 tile (whose 8 waves then need fewer registers).
+    const bool many_rows = ceil_div(mm, kTiles[tile].tile_m()) >= kExpandTileRows;
+    plan->expand = kind_is_compact(kind) && many_rows && (kind != NM_KIND_C14 || tile == kT256x256w8) ? 1 : 0;
     return complete_plan(kind, m, n, k, plan);
 }
 

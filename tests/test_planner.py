@@ -39,7 +39,8 @@ def test_plan_rules(shape):
         assert p.split_k == 1
         rows = -(-m // tm)
         compact = d.layout not in (nmspmm.NM_LAYOUT_SP42, nmspmm.NM_LAYOUT_DENSE)
-        assert p.expand == int(compact and rows >= 32)
+        on_256 = (tn, tm) == (256, 256)
+        assert p.expand == int(compact and rows >= 32 and (d.kind != nmspmm.NM_KIND_C14 or on_256))
         if p.expand:
             F, S = -(-n // 16), -(-k // 128)
             want = F * S * 1280 if d.kind in (nmspmm.NM_KIND_C14, nmspmm.NM_KIND_C18, nmspmm.NM_KIND_C28) else n * k
@@ -65,10 +66,19 @@ def test_small_token_counts_split_the_reduction_inside_workgroups():
     d = nmspmm.compress_size(768, 192, 2, 4)
     p = nmspmm.spmm_plan(d, 197, nmspmm.NM_OUT_I32)
     assert (p.tile_n, p.tile_m) == (32, 32)
-    # but not when 32 x 32 tiles would oversubscribe (DeiT-Base fc1 at batch 1)
+    # but the k-sliced 64 x 64 tile when 32 x 32 tiles would oversubscribe
+    # (DeiT-Base fc1 at batch 1), while it fits twice per compute unit
     d = nmspmm.compress_size(3072, 768, 2, 4)
     p = nmspmm.spmm_plan(d, 197, nmspmm.NM_OUT_I32)
+    assert (p.tile_n, p.tile_m) == (64, 64) and nmspmm.plan_kernel_name(p) == "k_gemm_ks<1, 4, 4, 3>"
+    d = nmspmm.compress_size(8192, 768, 2, 4)       # ... and 64 x 64 with a ring beyond that
+    p = nmspmm.spmm_plan(d, 512, nmspmm.NM_OUT_I32)
     assert (p.tile_n, p.tile_m) == (64, 64) and nmspmm.plan_kernel_name(p) == "k_gemm<1, 2, 2, 2, 2, 2>"
+    # a few thousand tokens with a long reduction: k-sliced 32 x 32 too
+    # (DeiT-Base fc2 at batch 8), not for the heavier operands
+    d = nmspmm.compress_size(768, 3072, 2, 4)
+    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 1576, 1)) == "k_gemm_ks<1, 2, 2, 3>"
+    assert "k_gemm_ks" not in nmspmm.plan_kernel_name(nmspmm.dense_plan(1576, 768, 3072, 1))
     # a single k-step splits too (the paper's grid at k = 128)
     d = nmspmm.compress_size(1024, 128, 2, 4)
     assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 256, 1)) == "k_gemm_ks<1, 2, 2, 3>"
@@ -89,12 +99,18 @@ def test_large_shapes_use_large_tiles():
     assert nmspmm.plan_kernel_name(p) == "k_gemm<1, 4, 2, 2, 4, 2>"   # 128 x 128 on 8 waves, 2-slot ring
     d = nmspmm.compress_size(3072, 1024, 4, 8)
     p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)    # ViT-L qkv, 4:8 weight: expanded once, dense kernel
-    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<3, 4, 2, 2, 4, 2>"
+    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<3, 2, 2, 4, 4, 2>"
     assert p.expand == 1
-    # one-stream weights on the widest outputs or with long reductions: the
-    # 4-wave 128 x 128 tile (ViT-L fc1, DeiT-B fc2 at batch 128)
+    # 4:2-operand weights: wide outputs with 8 or more k-steps, 256 x 256 on
+    # 8 waves (ViT-L qkv and fc1); long reductions, the 4-wave 128 x 128 tile
+    # (DeiT-B fc2 at batch 128)
     d = nmspmm.compress_size(4096, 1024, 2, 4)
-    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 18464, 1)) == "k_gemm<1, 2, 2, 4, 4, 2>"
+    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 18464, 1)) == "k_gemm<1, 2, 4, 8, 4, 3>"
+    d = nmspmm.compress_size(3072, 1024, 1, 4)         # 1:4 on that tile: expanded once, 4:2 kernel
+    p = nmspmm.spmm_plan(d, 18464, 1)
+    assert nmspmm.plan_kernel_name(p) == "k_gemm<1, 2, 4, 8, 4, 3>" and p.expand == 1
+    p = nmspmm.spmm_plan(d, 197, 1)                     # ... expanded inside the workgroups at batch 1
+    assert p.expand == 0 and nmspmm.plan_kernel_name(p).startswith("k_gemm_ks<2,")
     d = nmspmm.compress_size(768, 3072, 2, 4)
     assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 25216, 1)) == "k_gemm<1, 2, 2, 4, 4, 2>"
     # the dense baseline of DeiT-B fc2 at batch 128: 8 waves
@@ -111,8 +127,8 @@ def test_large_shapes_use_large_tiles():
     assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<3, 4, 2, 2, 4, 2>"
     p = nmspmm.dense_plan(18464, 4096, 1024, nmspmm.NM_OUT_I32)
     assert nmspmm.plan_kernel_name(p) == "k_gemm<3, 4, 2, 2, 4, 2>"
-    d = nmspmm.compress_size(4096, 1024, 2, 4)           # one-stream weight: 128 x 128
-    assert (nmspmm.spmm_plan(d, 18464, 1).tile_n, nmspmm.spmm_plan(d, 18464, 1).tile_m) == (128, 128)
+    d = nmspmm.compress_size(4096, 1024, 2, 4)           # 4:2-operand weight: 256 x 256
+    assert (nmspmm.spmm_plan(d, 18464, 1).tile_n, nmspmm.spmm_plan(d, 18464, 1).tile_m) == (256, 256)
     d = nmspmm.compress_size(768, 3072, 2, 4)
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # fc2 at batch 128
     assert (p.tile_n, p.tile_m) == (128, 128)
@@ -124,9 +140,14 @@ def test_large_shapes_use_large_tiles():
     assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 12608, 1)) == "k_gemm<3, 2, 2, 2, 2, 2>"  # expanded once
     d = nmspmm.compress_size(384, 384, 2, 4)
     assert (nmspmm.spmm_plan(d, 12608, 1).tile_n, nmspmm.spmm_plan(d, 12608, 1).tile_m) == (128, 32)
-    # medium token counts: half-height tiles, narrower for the dense-tile weights
-    # (DeiT-B qkv at batch 8, k = 768)
+    # medium token counts, short reductions: 64 x 64 while it gives at most 4
+    # workgroups per CU (DeiT-B qkv at batch 8, k = 768), else half-height
+    # tiles (DeiT-B fc1 at batch 8), narrower for the dense-tile weights
     d = nmspmm.compress_size(2304, 768, 2, 4)
+    assert (nmspmm.spmm_plan(d, 1576, 1).tile_n, nmspmm.spmm_plan(d, 1576, 1).tile_m) == (64, 64)
+    d = nmspmm.compress_size(3072, 768, 2, 4)
+    assert (nmspmm.spmm_plan(d, 1576, 1).tile_n, nmspmm.spmm_plan(d, 1576, 1).tile_m) == (64, 64)
+    d = nmspmm.compress_size(4608, 768, 2, 4)
     assert (nmspmm.spmm_plan(d, 1576, 1).tile_n, nmspmm.spmm_plan(d, 1576, 1).tile_m) == (128, 64)
     d = nmspmm.compress_size(2304, 768, 4, 8)
     assert (nmspmm.spmm_plan(d, 1576, 1).tile_n, nmspmm.spmm_plan(d, 1576, 1).tile_m) == (64, 128)
@@ -144,10 +165,8 @@ def test_large_shapes_use_large_tiles():
     d = nmspmm.compress_size(512, 2048, 2, 4)
     assert (nmspmm.spmm_plan(d, 6272, 1).tile_n, nmspmm.spmm_plan(d, 6272, 1).tile_m) == (128, 64)
     # ... or 64 x 64 when half-height tiles would leave compute units idle
-    # (DeiT-Base fc2 at batch 8: 150 tiles of 128 x 64 on 256 compute units)
-    d = nmspmm.compress_size(768, 3072, 2, 4)
-    assert (nmspmm.spmm_plan(d, 1576, 1).tile_n, nmspmm.spmm_plan(d, 1576, 1).tile_m) == (64, 64)
-    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 1576, 1)) == "k_gemm<1, 2, 2, 2, 2, 2>"
+    # (Swin-B stage 4 fc2 of the dense baseline: 96 tiles of 64 x 128)
+    assert nmspmm.plan_kernel_name(nmspmm.dense_plan(1568, 1024, 4096, 1)) == "k_gemm<3, 2, 2, 2, 2, 2>"
     # one or two k-steps: 64 x 64 tiles (Swin-B stage 2 qkv, k = 256), and
     # 128 x 32 for one k-step of one-stream weights at least 384 wide (Swin-B
     # stage 1 qkv, k = 128; its proj, 128 wide, stays at 64 x 64)
