@@ -26,28 +26,25 @@ nm_outputs outputs_of(int32_t *Y, const float *scale, uint16_t *Yh) {
     return o;
 }
 
-// Tile order of the launch.  Row by row, the tiles in flight on one XCD sweep
-// the whole weight operand once per row of tiles; once the weight as stored
-// (packed values and positions, or dense W) no longer fits in most of the
-// XCD's 4 MB L2, every row reads it again from the last-level cache or HBM.
-// Walking groups of 8 tile rows column by column reads it once per group
-// instead.  Measured over m 4096-25216, n 1024-8192, k 768-4096, for dense,
-// one- and two-stream weights, with operands resident in or evicted from the
-// last-level cache: up to 23 % faster on large weights and at most 5 % slower
-// on any shape this rule groups.  Smaller weights, and launches with fewer
-// than 64 rows of tiles, keep the row order: grouping them cost up to 20 %.
-constexpr int64_t kGroupWeightBytes = (int64_t)7 << 19;  // 3.5 MiB
-constexpr int kGroupRows = 8;
+// Tile order of the launch.  Row by row, the tiles in flight on one XCD share
+// two or three rows of X and sweep the whole weight; when X arrives cold from
+// HBM -- as it does inside a network's sequence of layers, where the layers
+// before have streamed far more than the last-level cache holds -- all of
+// them wait on the same few rows, one k-step at a time.  Walking groups of 16
+// tile rows column by column puts 16 distinct rows of X in flight per XCD
+// (2 MB of X and a few column tiles of the weight stay in its 4 MB L2).  Timed
+// with a 75 MB read before every launch (ViT-L/16-384 batch 32, m = 18464):
+// 2:4 fc1 on 128 x 128 tiles 125 -> 82-86 us, qkv 93 -> 65-68, fc2 84 -> 77-79,
+// proj 36 -> 32; groups of 4 or 8 rows gained less, 32 lost.  Launches with
+// fewer than 32 rows of tiles keep the row order.
+constexpr int kGroupRows = 16;
 
 int64_t stored_weight_bytes(int kind, int n, int k, int n_frags, int k_steps) {
     return kind == NM_KIND_DENSE ? (int64_t)n * k
                                  : (int64_t)n_frags * k_steps * 64 * (layout_lane_vbytes(kind) + layout_lane_mbytes(kind));
 }
 
-int group_rows_for(int kind, int n, int k, int n_frags, int k_steps, int tiles_m) {
-    const int64_t stored = stored_weight_bytes(kind, n, k, n_frags, k_steps);
-    return stored >= kGroupWeightBytes && tiles_m >= 8 * kGroupRows ? kGroupRows : 0;
-}
+int group_rows_for(int tiles_m) { return tiles_m >= 2 * kGroupRows ? kGroupRows : 0; }
 
 }  // namespace
 
@@ -117,7 +114,7 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
     a.tiles_n = (n + plan.tile_n - 1) / plan.tile_n;
     a.tiles_m = (m + plan.tile_m - 1) / plan.tile_m;
     a.split_k = plan.split_k;
-    a.group_rows = group_rows_for(run_kind, n, k, n_frags, k_steps, a.tiles_m);
+    a.group_rows = group_rows_for(a.tiles_m);
     int err = launch_gemm(run_kind, plan.tile, a, plan.grid, stream);
     return err == 0 ? NM_OK : NM_ERR_HIP;
 }

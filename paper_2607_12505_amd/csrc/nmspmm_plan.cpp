@@ -177,37 +177,25 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
         }
     } else if (heavy) {
         // Large outputs, heavier operands: 128 x 128 on 8 waves (4 along the
-        // channels x 2 along the tokens, twice the waves to overlap the
-        // operand reads with the stores), or, on the widest outputs with long
-        // reductions (24 k-steps or more), the 256 x 256 tile on 8 waves,
-        // which halves the operand fill per output.  With the grouped tile
-        // order that large weights take, 128 x 128 is 7-14 % faster than
-        // 256 x 256 at k = 1024 and 256 x 256 6-13 % faster at k = 4096
-        // (n 4096 and 8192, m 8192-25216, dense and 4:8).
-        // Inside the steps of the ViT-L chain, 3072-wide outputs with 8 k-steps
-        // (qkv) ran fastest on the 4-wave 128 x 128 tile (dense 96-100 us
-        // against 101-104 on 8 waves).
-        if (n >= 4096 && k_steps >= 24)
-            tile = kT256x256w8;
-        else if (n >= 3072 && n < 4096 && k_steps >= 8 && k_steps < 24)
-            tile = kT128x128r2;
-        else
-            tile = kT128x128w8;
+        // channels x 2 along the tokens, twice the waves of the 4-wave tile to
+        // overlap operand reads, matrix work and stores), except on the widest
+        // outputs with long reductions (4096 channels or more, 24 k-steps or
+        // more), where the 256 x 256 tile on 8 waves halves the operand fill
+        // per output (6-13 % faster at k = 4096, n 4096 and 8192, m 8192-25216,
+        // dense and 4:8).  Timed inside the steps of the ViT-L and DeiT-B
+        // workloads with the 16-row tile groups (cold operands), 128 x 128 on
+        // 8 waves won every other large shape (ViT-L qkv dense 82.7 us against
+        // 88.4 on 4 waves, fc1 103.5 against 110.5) or tied within 2 %.
+        tile = n >= 4096 && k_steps >= 24 ? kT256x256w8 : kT128x128w8;
     } else {
-        // Large outputs, 4:2-operand weights, timed inside the steps of the
-        // workloads (every layer with cold inputs and outputs): long
+        // Large outputs, 4:2-operand weights, timed the same way: long
         // reductions (24 k-steps or more) the 4-wave 128 x 128 tile, whose
-        // larger per-wave fragment grid needs fewer operand reads per product;
-        // wide outputs (3072 or more) with 8 or more k-steps the 256 x 256
-        // tile on 8 waves, half the operand fill per output (ViT-L qkv and
-        // fc1: 86 and 109 us against 94 and 127); otherwise 128 x 128 on
-        // 8 waves.
-        if (k_steps >= 24)
-            tile = kT128x128r2;
-        else if (n >= 3072 && k_steps >= 8)
-            tile = kT256x256w8;
-        else
-            tile = kT128x128w8;
+        // larger per-wave fragment grid needs fewer operand reads per product
+        // (ViT-L fc2 2:4 78.6 us, DeiT-B b128 fc2 60-62); otherwise 128 x 128
+        // on 8 waves (ViT-L qkv and fc1 2:4: 70.4 and 87.2 us against 87.1
+        // and 104.1 on the 256 x 256 tile, which the 16-row groups no longer
+        // favour).
+        tile = k_steps >= 24 ? kT128x128r2 : kT128x128w8;
     }
     plan->kind = kind;
     plan->tile = tile;
@@ -216,9 +204,13 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
     // when few rows of output tiles share it; with many rows the expansion
     // repeated per row costs more than one expansion pass per call.  1:4,
     // whose expansion is a few byte permutes, stays inside the workgroups
-    // except on the 256 x 256 tile (whose 8 waves then need fewer registers).
+    // unless the reduction is long (24 k-steps or more: ViT-L fc2 81.5 us
+    // expanded once against 87.3) or the output wide (4096 channels or more:
+    // ViT-L fc1 86.2 against 89.7), or on the 256 x 256 tile (whose 8 waves
+    // then need fewer registers).
     const bool many_rows = ceil_div(mm, kTiles[tile].tile_m()) >= kExpandTileRows;
-    plan->expand = kind_is_compact(kind) && many_rows && (kind != NM_KIND_C14 || tile == kT256x256w8) ? 1 : 0;
+    const bool c14_once = k_steps >= 24 || n >= 4096 || tile == kT256x256w8;
+    plan->expand = kind_is_compact(kind) && many_rows && (kind != NM_KIND_C14 || c14_once) ? 1 : 0;
     return complete_plan(kind, m, n, k, plan);
 }
 

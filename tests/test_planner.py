@@ -39,8 +39,8 @@ def test_plan_rules(shape):
         assert p.split_k == 1
         rows = -(-m // tm)
         compact = d.layout not in (nmspmm.NM_LAYOUT_SP42, nmspmm.NM_LAYOUT_DENSE)
-        on_256 = (tn, tm) == (256, 256)
-        assert p.expand == int(compact and rows >= 32 and (d.kind != nmspmm.NM_KIND_C14 or on_256))
+        c14_once = -(-k // 128) >= 24 or n >= 4096 or (tn, tm) == (256, 256)
+        assert p.expand == int(compact and rows >= 32 and (d.kind != nmspmm.NM_KIND_C14 or c14_once))
         if p.expand:
             F, S = -(-n // 16), -(-k // 128)
             want = F * S * 1280 if d.kind in (nmspmm.NM_KIND_C14, nmspmm.NM_KIND_C18, nmspmm.NM_KIND_C28) else n * k
@@ -99,16 +99,22 @@ def test_large_shapes_use_large_tiles():
     assert nmspmm.plan_kernel_name(p) == "k_gemm<1, 4, 2, 2, 4, 2>"   # 128 x 128 on 8 waves, 2-slot ring
     d = nmspmm.compress_size(3072, 1024, 4, 8)
     p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)    # ViT-L qkv, 4:8 weight: expanded once, dense kernel
-    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<3, 2, 2, 4, 4, 2>"
+    assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<3, 4, 2, 2, 4, 2>"
     assert p.expand == 1
-    # 4:2-operand weights: wide outputs with 8 or more k-steps, 256 x 256 on
-    # 8 waves (ViT-L qkv and fc1); long reductions, the 4-wave 128 x 128 tile
-    # (DeiT-B fc2 at batch 128)
+    # 4:2-operand weights: 128 x 128 on 8 waves up to 23 k-steps (ViT-L qkv
+    # and fc1); long reductions, the 4-wave 128 x 128 tile (DeiT-B fc2 at
+    # batch 128)
     d = nmspmm.compress_size(4096, 1024, 2, 4)
-    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 18464, 1)) == "k_gemm<1, 2, 4, 8, 4, 3>"
-    d = nmspmm.compress_size(3072, 1024, 1, 4)         # 1:4 on that tile: expanded once, 4:2 kernel
+    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 18464, 1)) == "k_gemm<1, 4, 2, 2, 4, 2>"
+    d = nmspmm.compress_size(3072, 1024, 1, 4)         # 1:4 on 3072 channels: expanded inside the workgroups
     p = nmspmm.spmm_plan(d, 18464, 1)
-    assert nmspmm.plan_kernel_name(p) == "k_gemm<1, 2, 4, 8, 4, 3>" and p.expand == 1
+    assert nmspmm.plan_kernel_name(p) == "k_gemm<2, 4, 2, 2, 4, 2>" and p.expand == 0
+    d = nmspmm.compress_size(4096, 1024, 1, 4)         # ... on 4096 channels expanded once, 4:2 kernel
+    p = nmspmm.spmm_plan(d, 18464, 1)
+    assert nmspmm.plan_kernel_name(p) == "k_gemm<1, 4, 2, 2, 4, 2>" and p.expand == 1
+    d = nmspmm.compress_size(1024, 4096, 1, 4)         # ... and with 32 k-steps too
+    p = nmspmm.spmm_plan(d, 18464, 1)
+    assert nmspmm.plan_kernel_name(p) == "k_gemm<1, 2, 2, 4, 4, 2>" and p.expand == 1
     p = nmspmm.spmm_plan(d, 197, 1)                     # ... expanded inside the workgroups at batch 1
     assert p.expand == 0 and nmspmm.plan_kernel_name(p).startswith("k_gemm_ks<2,")
     d = nmspmm.compress_size(768, 3072, 2, 4)
@@ -127,8 +133,8 @@ def test_large_shapes_use_large_tiles():
     assert (p.tile_n, p.tile_m) == (128, 128) and nmspmm.plan_kernel_name(p) == "k_gemm<3, 4, 2, 2, 4, 2>"
     p = nmspmm.dense_plan(18464, 4096, 1024, nmspmm.NM_OUT_I32)
     assert nmspmm.plan_kernel_name(p) == "k_gemm<3, 4, 2, 2, 4, 2>"
-    d = nmspmm.compress_size(4096, 1024, 2, 4)           # 4:2-operand weight: 256 x 256
-    assert (nmspmm.spmm_plan(d, 18464, 1).tile_n, nmspmm.spmm_plan(d, 18464, 1).tile_m) == (256, 256)
+    d = nmspmm.compress_size(4096, 1024, 2, 4)           # 4:2-operand weight: 128 x 128 too
+    assert (nmspmm.spmm_plan(d, 18464, 1).tile_n, nmspmm.spmm_plan(d, 18464, 1).tile_m) == (128, 128)
     d = nmspmm.compress_size(768, 3072, 2, 4)
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # fc2 at batch 128
     assert (p.tile_n, p.tile_m) == (128, 128)
