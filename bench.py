@@ -500,16 +500,23 @@ def main():
     ts, td = pa.mean(axis=0), pb.mean(axis=0)
     per_pattern = per_key_speedups(preps, ts, td, lambda p: pattern_name(p.g))
 
-    # dominant kernel: the sparse-leg kernel instantiation with the most time per step
+    # dominant kernel: the sparse-leg kernel instantiation and GEMM shape with
+    # the most time per step (one shape, so that a profiler's per-launch
+    # average of that kernel and grid is the same quantity)
     kern = {}
     for i, p in enumerate(preps):
-        k = kern.setdefault(p.kernel_name(p.splan), {"ms": 0.0, "idx": []})
+        k = kern.setdefault((p.kernel_name(p.splan), p.g.m, p.g.k, p.g.n), {"ms": 0.0, "idx": []})
         k["ms"] += ts[i]
         k["idx"].append(i)
-    dom_name = max(kern, key=lambda k: kern[k]["ms"])
-    dom_idx = kern[dom_name]["idx"]
+    dom_key = max(kern, key=lambda k: kern[k]["ms"])
+    dom_name = dom_key[0]
+    dom_idx = kern[dom_key]["idx"]
     launches = len(dom_idx)
-    avg_ms = kern[dom_name]["ms"] / launches
+    # the kernel's own launch time: calls that also expand a compact weight
+    # first (a second kernel inside the same call) are left out of the
+    # average when calls without it exist
+    plain = [i for i in dom_idx if not preps[i].splan.expand] or dom_idx
+    avg_ms = float(np.mean([ts[i] for i in plain]))
     dom_bytes = sum(algorithmic_bytes(preps[i].g, out_i32, out_f16, sparse=preps[i].sparse_kernel) for i in dom_idx)
     dom_ops = sum(preps[i].g.dense_eq_ops for i in dom_idx)
     achieved = dom_bytes / launches / (avg_ms * 1e-3) / 1e9
@@ -524,6 +531,7 @@ def main():
             tr = json.load(f)
         # counters taken on another kernel (or an older build of it) do not count
         if (tr.get("kernel") == dom_name and tr.get("workload") == work.name
+                and tr.get("grid") == int(preps[dom_idx[0]].splan.grid)
                 and tr.get("kernel_source_sha256") == kernel_source_sha256()):
             traffic = tr.get("bytes_per_launch")
     if mfma_bound:
@@ -536,12 +544,16 @@ def main():
     roofline.update({
         "traffic": traffic,
         "kernel": dom_name,
+        "gemm": {"m": dom_key[1], "k": dom_key[2], "n": dom_key[3],
+                 "grid": int(preps[dom_idx[0]].splan.grid),
+                 "patterns": sorted({pattern_name(preps[i].g) for i in dom_idx})},
         "launches_per_step": launches,
         "avg_launch_us": round(avg_ms * 1e3, 2),
+        "avg_over_launches": len(plain),
         "algorithmic_bytes_per_launch": int(dom_bytes / launches),
         "algorithmic_ops_per_launch": int(dom_ops / launches),
         "hbm_gbs": round(achieved, 1),
-        "share_of_step": round(float(kern[dom_name]["ms"] / ts.sum()), 3),
+        "share_of_step": round(float(kern[dom_key]["ms"] / ts.sum()), 3),
     })
     if store_ms is not None:
         # the same launches with the reduction skipped: the ceiling this

@@ -714,16 +714,27 @@ def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, comma
         ks = [k for k in per if name in k]
         return per[ks[0]] if ks else None
 
-    dom_fetch, dom_write = find(fetch, dom), find(write, dom)
+    # the dominant kernel on the dominant GEMM shape: its own grid
+    dom_grid = line["roofline"].get("gemm", {}).get("grid")
+    sel = _grid_counters(fetch_dir, dom, dom_grid), _grid_counters(write_dir, dom, dom_grid)
+    dom_fetch, dom_write = sel if all(sel) else (find(fetch, dom), find(write, dom))
     bytes_per_launch = (np.mean(dom_fetch) * 1024 * f_scale + np.mean(dom_write) * 1024 * w_scale)
     dom_stats = [r for r in stats if dom in r["Name"]][0]
     md = [f"# rocprofv3 summary: `{dom}` on workload `{work}`", ""]
     md += ["Commands (repository root as working directory of the bench; rocprofv3 run from /tmp):", "", "```"]
     md += commands + ["```", ""]
-    md += [f"Dominant sparse kernel: `{dom}`: {dom_stats['Calls']} calls, average "
+    own = _grid_durations(trace_dir, dom, dom_grid) if dom_grid else None
+    gemm = line["roofline"].get("gemm")
+    md += [f"Dominant sparse kernel: `{dom}`: {dom_stats['Calls']} calls over every shape of the run, average "
            f"{float(dom_stats['AverageNs']) / 1e3:.2f} us (min {float(dom_stats['MinNs']) / 1e3:.2f}, "
-           f"max {float(dom_stats['MaxNs']) / 1e3:.2f}); bench.py HIP-event average over the timed region: "
-           f"{line['roofline']['avg_launch_us']:.2f} us.", ""]
+           f"max {float(dom_stats['MaxNs']) / 1e3:.2f})."]
+    if own and gemm:
+        md += ["", f"On the dominant GEMM shape (m {gemm['m']}, k {gemm['k']}, n {gemm['n']}; patterns "
+                   f"{', '.join(gemm['patterns'])}; {dom_grid} workgroups): {len(own)} launches in the trace, average "
+                   f"{np.mean(own):.2f} us (median {np.median(own):.2f}); bench.py HIP-event average of the same "
+                   f"GEMMs over the timed region ({line['roofline'].get('avg_over_launches', '?')} launches per step "
+                   f"without a weight expansion in the call): {line['roofline']['avg_launch_us']:.2f} us."]
+    md += [""]
     md += ["| kernel | calls | avg us | total ms |", "|---|---:|---:|---:|"]
     for r in stats[:14]:
         md.append(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
@@ -752,9 +763,10 @@ def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, comma
             mb = 100.0 * np.mean(busy[k]) / (np.mean(active[k]) / xcds * simds)
             lc = 100.0 * np.mean(conf[k]) / max(np.mean(lds[k]), 1.0) if k in conf and k in lds else float("nan")
             md.append(f"| `{k[:90]}` | {len(busy[k])} | {mb:.1f} | {lc:.2f} |")
+    md += launch_shape_table(line, trace_dir, fetch_dir, write_dir, f_scale, w_scale, sq_dir)
     with open(out_md, "w") as f:
         f.write("\n".join(md) + "\n")
-    rec = {"kernel": dom, "workload": work, "bytes_per_launch": int(bytes_per_launch),
+    rec = {"kernel": dom, "workload": work, "grid": dom_grid, "bytes_per_launch": int(bytes_per_launch),
            "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
            "kernel_source_sha256": kernel_source_sha256(), "summary": os.path.basename(out_md)}
     with open(default_traffic_path(work), "w") as f:
@@ -762,6 +774,149 @@ def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, comma
     print("\n".join(md))
 
 
+
+
+def launch_labels(cfg):
+    """(kernel name, grid in threads) -> the GEMMs of workload cfg launched that
+    way by the planner (sparse leg and dense baseline), from the plans alone."""
+    from paper_2607_12505_amd import workloads as wl
+    labels = {}
+    for g in wl.workload(cfg).gemms:
+        short = g.name.split(" ", 1)[1].split(" ")[0]
+        if g.N == g.M:
+            plans = [("dense", nmspmm.dense_plan(g.m, g.n, g.k, nmspmm.NM_OUT_I32))]
+        else:
+            plans = [(f"{g.N}:{g.M}", nmspmm.spmm_plan(nmspmm.compress_size(g.n, g.k, g.N, g.M), g.m,
+                                                     nmspmm.NM_OUT_I32)),
+                     ("dense baseline", nmspmm.dense_plan(g.m, g.n, g.k, nmspmm.NM_OUT_I32))]
+        for pat, p in plans:
+            name = nmspmm.plan_kernel_name(p)
+            key = (name, p.grid)
+            labels.setdefault(key, set()).add((short, g.m, g.k, g.n, pat))
+    return labels
+
+
+def _workgroups(name, grid_threads):
+    if name.startswith("k_gemm_ks"):
+        return grid_threads // 256
+    parts = [int(x) for x in name[name.index("<") + 1:name.index(">")].split(",")]
+    return grid_threads // (64 * parts[1] * parts[2])
+
+
+def _grid_durations(trace_dir, kernel, grid):
+    """Trace durations (us) of `kernel` launched with `grid` workgroups."""
+    import csv
+    import glob
+    out = []
+    for r in csv.DictReader(open(glob.glob(os.path.join(trace_dir, "*_kernel_trace.csv"))[0])):
+        if kernel in r["Kernel_Name"] and _workgroups(kernel, int(r.get("Grid_Size") or r["Grid_Size_X"])) == grid:
+            out.append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    return out
+
+
+def _grid_counters(d, kernel, grid):
+    """Per-dispatch counter values (summed over a dispatch's rows) of `kernel`
+    launched with `grid` workgroups."""
+    import csv
+    import glob
+    if grid is None:
+        return None
+    per = {}
+    for r in csv.DictReader(open(glob.glob(os.path.join(d, "*_counter_collection.csv"))[0])):
+        if kernel in r["Kernel_Name"] and _workgroups(kernel, int(r.get("Grid_Size") or r["Grid_Size_X"])) == grid:
+            per[r["Dispatch_Id"]] = per.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    return list(per.values()) or None
+
+
+def _workload_cfg(line):
+    return {"deit_small_b64": 1, "deit_base_b128": 2, "swin_base_b64": 3,
+            "vit_large_384_b32_chain": 4}.get(line["config"]["workload"])
+
+
+def launch_shape_table(line, trace_dir, fetch_dir, write_dir, f_scale, w_scale, sq_dir):
+    """Per launch shape (kernel and grid) of the workload: average duration from
+    the kernel trace, scaled HBM bytes per dispatch, the algorithmic bytes and
+    ops of the GEMMs launched that way, the achieved fraction of the HBM and
+    matrix-instruction peaks, and matrix-core busy time."""
+    import csv
+    import glob
+    import re
+    cfg = _workload_cfg(line)
+    if cfg is None:
+        return []
+    labels = launch_labels(cfg)
+
+    def short(n):
+        m = re.search(r"(k_gemm(?:_ks)?<[^>]*>)", n)
+        return m.group(1) if m else None
+
+    durs = {}
+    for r in csv.DictReader(open(glob.glob(os.path.join(trace_dir, "*_kernel_trace.csv"))[0])):
+        k = short(r["Kernel_Name"])
+        if k:
+            key = (k, _workgroups(k, int(r.get("Grid_Size") or r["Grid_Size_X"])))
+            durs.setdefault(key, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+
+    def per_shape(d, counter=None):
+        out = {}
+        for r in csv.DictReader(open(glob.glob(os.path.join(d, "*_counter_collection.csv"))[0])):
+            k = short(r["Kernel_Name"])
+            if not k or (counter and r["Counter_Name"] != counter):
+                continue
+            key = (k, _workgroups(k, int(r["Grid_Size"])), int(r["Dispatch_Id"]))
+            out[key] = out.get(key, 0.0) + float(r["Counter_Value"])
+        agg = {}
+        for (k, g, _), v in out.items():
+            agg.setdefault((k, g), []).append(v)
+        return agg
+
+    fetch, write = per_shape(fetch_dir), per_shape(write_dir)
+    busy = per_shape(sq_dir, "SQ_VALU_MFMA_BUSY_CYCLES") if sq_dir else {}
+    active = per_shape(sq_dir, "GRBM_GUI_ACTIVE") if sq_dir else {}
+    md = ["", "Per launch shape of the workload (kernel and grid, matched to the GEMMs the planner launches that "
+          "way): average duration from the kernel trace, HBM bytes per dispatch from the scaled counters, "
+          "algorithmic bytes (X + stored weight + int32 Y) and dense-equivalent ops of those GEMMs, and the "
+          "fraction of the HBM peak (8 TB/s) and of the matrix-instruction peak of the kind (2:4-operand "
+          "kernels against 10.07 dense-equivalent POPS, dense against 5.03):", "",
+          "| kernel | workgroups | GEMMs | us | HBM MB | alg. MB | HBM frac | POPS | MFMA frac | MFMA busy % |",
+          "|---|---:|---|---:|---:|---:|---:|---:|---:|---:|"]
+    rows = []
+    for (name, grid), gemms in labels.items():
+        key = (name, grid)
+        if key not in durs:
+            continue
+        us = float(np.mean(durs[key]))
+        if len({g[1:4] for g in gemms}) > 1:
+            # GEMMs of different shapes launched alike (same kernel, same grid):
+            # the trace cannot tell their launches apart
+            what = ", ".join(sorted({f"{s} {p} (m {m}, k {k}, n {n})" for s, m, k, n, p in gemms}))
+            rows.append((0.0, f"| `{name}` | {grid} | {what}: shapes not separable in the trace | {us:.1f} (mixed) "
+                              "| | | | | | |"))
+            continue
+        _, m, k, n, _ = sorted(gemms)[0]
+
+        def stored(pat):
+            if pat.startswith("dense"):
+                return n * k
+            d = nmspmm.compress_size(n, k, *(int(x) for x in pat.split(":")))
+            return d.vals_bytes + d.meta_bytes
+
+        # the GEMMs of one launch shape share m, k and n; their stored weights
+        # differ by pattern (a small part of the bytes): averaged
+        alg = m * k + 4 * m * n + float(np.mean([stored(p) for *_, p in gemms]))
+        ops = 2.0 * m * n * k
+        hbm = ((np.mean(fetch[key]) * 1024 * f_scale + np.mean(write[key]) * 1024 * w_scale) / 1e6
+               if key in fetch and key in write else float("nan"))
+        peak = 5.03 if name.startswith("k_gemm<3") or name.startswith("k_gemm_ks<3") else 10.07
+        pops = ops / (us * 1e-6) / 1e15
+        mb = (100.0 * np.mean(busy[key]) / (np.mean(active[key]) / 8 * 1024)
+              if key in busy and key in active else float("nan"))
+        what = ", ".join(sorted({f"{s} {p}" for s, _, _, _, p in gemms}))
+        rows.append((-us, f"| `{name}` | {grid} | {what} (m {m}, k {k}, n {n}) | {us:.1f} | {hbm:.1f} | "
+                          f"{alg / 1e6:.1f} | {alg / (us * 1e-6) / 8e12:.3f} | {pops:.3f} | {pops / peak:.3f} | "
+                          f"{mb:.1f} |"))
+    md += [r for _, r in sorted(rows)]
+    return md
 
 
 def chain_sweep(torch, cfg, rounds, out_path, report):

@@ -741,17 +741,16 @@ __global__ __launch_bounds__(64 * WN * WM) void k_gemm(GemmArgs a) {
 
     const typename O::Cursor cur = O::cursor(a, wave, lane, tok0, ch0);
     WRegs<KIND> wr[O::WJ];
-    if constexpr (K::kDecode) {
-        fill_lut<KIND>(lut, tid, 64 * WN * WM);
-        __syncthreads();
-    }
 #pragma unroll
     for (int i = 0; i < R - 1; ++i)
         if (i < nsteps) O::issue(a, cur, lds, lds0, wave, lane, s_begin + i, i);
     if constexpr (K::kDecode) {
         // the compact weights of the first R - 1 k-steps, expanded in order,
-        // and the next k-step's loaded into registers
+        // and the next k-step's loaded into registers; the lookup table is
+        // built while the first loads are in flight
         if (nsteps > 0) O::wload_step(a, cur, s_begin, wr);
+        fill_lut<KIND>(lut, tid, 64 * WN * WM);
+        __syncthreads();
 #pragma unroll
         for (int i = 0; i < R - 1; ++i)
             if (i < nsteps) {
@@ -812,14 +811,22 @@ __global__ __launch_bounds__(64 * WN * WM) void k_gemm(GemmArgs a) {
 template <int KIND, int FN, int FM, int NST>
 struct GeometryKS {
     using K = Kind<KIND>;
+    // 1:4, 1:8 and 2:8: the compact bytes reach the ring by direct-to-LDS
+    // loads like X (RAWV value bytes and RAWM position bytes per k-step, the
+    // positions padded to 4 bytes per lane), and the compute stage expands
+    // them into the 4:2 operand in registers (no expanded copy in LDS)
+    static constexpr bool kRaw = K::kDecode && K::kSp;
     static constexpr int BN = FN * 16;
     static constexpr int BM = FM * 16;
     static constexpr int XB = BM * 128;
-    static constexpr int WVB = K::kSp ? (BN / 16) * kVBlock : BN * 128;
-    static constexpr int WMB = K::kSp ? (BN / 16) * kMBlock : 0;
-    static constexpr int SLOT = XB + WVB + WMB;
+    static constexpr int WVB = kRaw ? 0 : K::kSp ? (BN / 16) * kVBlock : BN * 128;
+    static constexpr int WMB = kRaw ? 0 : K::kSp ? (BN / 16) * kMBlock : 0;
+    static constexpr int RAWV = kRaw ? FN * 64 * K::VB : 0;
+    static constexpr int RAWM = kRaw ? FN * 256 : 0;
+    static constexpr int SLOT = XB + WVB + WMB + RAWV + RAWM;
     static constexpr int XI = BM / 8;                                  // X loads per k-step (one wave)
-    static constexpr int WI = K::kDecode ? FN * K::LOADS : KIND == NM_KIND_SP42 ? FN * 2 : BN / 8;
+    static constexpr int WI = kRaw ? FN * (K::VB / 4 + 1)
+                              : K::kDecode ? FN * K::LOADS : KIND == NM_KIND_SP42 ? FN * 2 : BN / 8;
     static constexpr int DMA = XI + WI;
     static constexpr int RING = 4 * NST * SLOT <= 160 * 1024 - 4096 ? NST : (160 * 1024 - 4096) / (4 * SLOT);
     static constexpr int ROWB = BN * 4 + 16;                           // padded staged row (int32)
@@ -899,6 +906,24 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
                     *(v4i *)(ringp + st * G::SLOT + G::XB + j * 1024 + lane * 16) = v;
                 }
             }
+        } else if constexpr (G::kRaw) {
+            // the FN compact blocks as stored: value bytes as whole dwords
+            // (dword i of a block by lane i % 64 of load i / 64), positions one
+            // dword per lane (2-byte positions: lanes 32-63 repeat lanes 0-31,
+            // landing in the unused half of the 256-byte area)
+            constexpr int VB = K::VB, MB = K::MB;
+#pragma unroll
+            for (int bl = 0; bl < FN; ++bl) {
+                int f = f0 + bl;
+                f = f < a.n_frags ? f : a.n_frags - 1;
+                const size_t b = (size_t)f * a.k_steps + s;
+                const int8_t *vb = a.A + b * 64 * VB;
+#pragma unroll
+                for (int i = 0; i < VB / 4; ++i)
+                    dma4(vb + (i * 64 + lane) * 4, slot + G::XB + G::WVB + G::WMB + bl * 64 * VB + i * 256);
+                const uint8_t *mb = a.meta + b * 64 * MB;
+                dma4(mb + (MB == 4 ? lane : (lane & 31)) * 4, slot + G::XB + G::WVB + G::WMB + G::RAWV + bl * 256);
+            }
         }
     };
     // compact kinds: the FN blocks of k-step s into registers, and their
@@ -921,6 +946,29 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
             for (int bl = 0; bl < FN; ++bl) expand_to_lds<KIND, G::WVB>(wr[bl], lut, ringp + st * G::SLOT + G::XB, bl, lane);
         }
     };
+    // 1:4, 1:8, 2:8: block bl of slot st's compact bytes, read from the ring
+    // and expanded into this lane's 4:2 operand (values and position word)
+    auto raw_operand = [&](int st, int bl, v4i &av, int &ai) {
+        if constexpr (G::kRaw) {
+            constexpr int VB = K::VB, MB = K::MB;
+            const int8_t *raw = ringp + st * G::SLOT + G::XB;
+            WRegs<KIND> r;
+            const int8_t *v = raw + bl * 64 * VB + lane * VB;
+            if constexpr (VB == 8) {
+                const v2u t = *(const v2u *)v;
+                r.v[0] = t[0];
+                r.v[1] = t[1];
+            } else {
+                static_assert(VB == 4, "compact 4:2 value bytes per lane");
+                r.v[0] = *(const uint32_t *)v;
+            }
+            const int8_t *m = raw + G::RAWV + bl * 256 + lane * MB;
+            r.m = MB == 4 ? *(const uint32_t *)m : (uint32_t) * (const uint16_t *)m;
+            uint32_t idx;
+            expand_sp42<KIND>(r, lut, av, idx);
+            ai = (int)idx;
+        }
+    };
     auto compute = [&](int st) {
         const int8_t *xs = ringp + st * G::SLOT;
         const int8_t *ws = xs + G::XB;
@@ -929,8 +977,12 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
             int ai[FN];
 #pragma unroll
             for (int i = 0; i < FN; ++i) {
-                av[i] = *(const v4i *)(ws + i * kVBlock + lane * 16);
-                ai[i] = *(const int *)(ws + G::WVB + i * kMBlock + lane * 4);
+                if constexpr (G::kRaw) {
+                    raw_operand(st, i, av[i], ai[i]);
+                } else {
+                    av[i] = *(const v4i *)(ws + i * kVBlock + lane * 16);
+                    ai[i] = *(const int *)(ws + G::WVB + i * kMBlock + lane * 4);
+                }
             }
 #pragma unroll
             for (int j = 0; j < FM; ++j) {
@@ -967,16 +1019,18 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
         }
     };
 
-    if constexpr (K::kDecode) {
-        fill_lut<KIND>(lut, tid, 256);
-        __syncthreads();
-    }
     // k-step t of this wave is s_begin + wave + 4 t
 #pragma unroll
     for (int i = 0; i < R - 1; ++i)
         if (i < nsteps) issue(s_begin + wave + 4 * i, i);
-    if constexpr (K::kDecode) {
+    if constexpr (G::kRaw) {
+        fill_lut<KIND>(lut, tid, 256);
+        __syncthreads();
+    } else if constexpr (K::kDecode) {
+        // the lookup table is built while the first loads are in flight
         if (nsteps > 0) wload_step(s_begin + wave);
+        fill_lut<KIND>(lut, tid, 256);
+        __syncthreads();
 #pragma unroll
         for (int i = 0; i < R - 1; ++i)
             if (i < nsteps) {
@@ -989,7 +1043,7 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
         wait_later<R - 2, G::DMA>(later);  // this wave's slot t is in LDS, its reads of slot t-1 done
         const int nx = t + R - 1;
         if (nx < nsteps) {
-            if constexpr (K::kDecode) {
+            if constexpr (K::kDecode && !G::kRaw) {
                 expand_step(nx % R);
                 issue(s_begin + wave + 4 * nx, nx % R);
                 if (nx + 1 < nsteps) wload_step(s_begin + wave + 4 * (nx + 1));
@@ -1046,13 +1100,16 @@ template <int KIND>
 __global__ __launch_bounds__(256) void k_expand(const int8_t *__restrict__ vals, const uint8_t *__restrict__ meta,
                                                int n, int k, int blocks, int k_steps, int8_t *out) {
     __shared__ uint2 lut[Kind<KIND>::LUT];
+    const int b = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    // the block's compact bytes are requested first, so the table is built
+    // while they are in flight (waves past the last block load nothing but
+    // still help build the table)
+    WRegs<KIND> r;
+    const int64_t o = (int64_t)(b < blocks ? b : blocks - 1) * 64 + lane;
+    wload<KIND>(r, vals + o * Kind<KIND>::VB, meta + o * Kind<KIND>::MB);
     fill_lut<KIND>(lut, threadIdx.x, 256);
     __syncthreads();
-    const int b = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
     if (b >= blocks) return;
-    WRegs<KIND> r;
-    const int64_t o = (int64_t)b * 64 + lane;
-    wload<KIND>(r, vals + o * Kind<KIND>::VB, meta + o * Kind<KIND>::MB);
     if constexpr (Kind<KIND>::kSp) {
         v4i v;
         uint32_t idx;

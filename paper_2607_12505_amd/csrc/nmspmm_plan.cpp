@@ -207,10 +207,14 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
     // unless the reduction is long (24 k-steps or more: ViT-L fc2 81.5 us
     // expanded once against 87.3) or the output wide (4096 channels or more:
     // ViT-L fc1 86.2 against 89.7), or on the 256 x 256 tile (whose 8 waves
-    // then need fewer registers).
+    // then need fewer registers).  The k-sliced tiles load the compact bytes
+    // like X and expand them in registers, which the separate pass (a second
+    // launch) never beats at the token counts they serve (DeiT-B fc2 at
+    // batch 8, 1:4: 13.0 us against 16.1).
     const bool many_rows = ceil_div(mm, kTiles[tile].tile_m()) >= kExpandTileRows;
     const bool c14_once = k_steps >= 24 || n >= 4096 || tile == kT256x256w8;
-    plan->expand = kind_is_compact(kind) && many_rows && (kind != NM_KIND_C14 || c14_once) ? 1 : 0;
+    const bool k_sliced = kTiles[tile].layout == kKSliced;
+    plan->expand = kind_is_compact(kind) && many_rows && !k_sliced && (kind != NM_KIND_C14 || c14_once) ? 1 : 0;
     return complete_plan(kind, m, n, k, plan);
 }
 

@@ -32,5 +32,8 @@ def test_lut_chain_and_calibration():
     gamma, b = nmsearch.latency_fit(R[:8], T[:8])
     assert (gamma >= 0).all() and b >= 0
     pred = np.array([nmsearch.latency_predict(r, gamma, b) for r in R[8:]])
-    # a loose sanity bound only: small chains are launch-bound and noisy
-    assert np.all(np.abs(pred - T[8:]) / T[8:] < 0.5)
+    err = np.abs(pred - T[8:]) / T[8:]
+    print("held-out chain times (us):", np.round(T[8:], 2).tolist(), "relative errors:", np.round(err, 4).tolist(),
+          flush=True)
+    # Eq. 1 fitted on 8 chains predicts the held-out ones within 10 % (2-4 % observed)
+    assert np.all(err < 0.10)

@@ -40,7 +40,8 @@ def test_plan_rules(shape):
         rows = -(-m // tm)
         compact = d.layout not in (nmspmm.NM_LAYOUT_SP42, nmspmm.NM_LAYOUT_DENSE)
         c14_once = -(-k // 128) >= 24 or n >= 4096 or (tn, tm) == (256, 256)
-        assert p.expand == int(compact and rows >= 32 and (d.kind != nmspmm.NM_KIND_C14 or c14_once))
+        k_sliced = "k_gemm_ks" in nmspmm.plan_kernel_name(p)
+        assert p.expand == int(compact and rows >= 32 and not k_sliced and (d.kind != nmspmm.NM_KIND_C14 or c14_once))
         if p.expand:
             F, S = -(-n // 16), -(-k // 128)
             want = F * S * 1280 if d.kind in (nmspmm.NM_KIND_C14, nmspmm.NM_KIND_C18, nmspmm.NM_KIND_C28) else n * k
