@@ -10,15 +10,22 @@
 // Dataflow of one workgroup (4 or 8 waves) over its k range, one 128-wide
 // k-step at a time (paper Sec. 4.2: sparse handling confined to packed
 // loading, the compute stage purely matrix-instruction based):
-//   - every operand byte reaches LDS through the direct-to-LDS 16-byte (and
-//     4-byte) loads of gfx950, into a ring of NST k-step slots filled NST-1
-//     steps ahead of the compute: the tile_m x 128 slice of X, and the weight
-//     slice (the packed 4:2 fragments as stored, or tile_n x 128 rows of a
-//     dense W).  Each workgroup fetches each byte once; no VGPRs are spent on
-//     staging, so the ring depth costs only LDS.  Each lane picks the source
-//     chunk that belongs at its LDS slot, so row-major slices land with their
-//     16-byte chunks XOR-swizzled by row and the operand reads of 16 rows hit
-//     distinct banks;
+//   - every X byte reaches LDS through the direct-to-LDS 16-byte loads of
+//     gfx950, into a ring of NST k-step slots filled NST-1 steps ahead of the
+//     compute: the tile_m x 128 slice of X, and with it the weight slice as
+//     stored when it is already what the matrix instruction reads (the 4:2
+//     fragments of 2:4, or tile_n x 128 rows of a dense W).  Each workgroup
+//     fetches each byte once; no VGPRs are spent on staging, so the ring
+//     depth costs only LDS.  Each lane picks the source chunk that belongs at
+//     its LDS slot, so row-major slices land with their 16-byte chunks
+//     XOR-swizzled by row and the operand reads of 16 rows hit distinct banks;
+//   - compact weights (1:4, 1:8, 2:8 and the 3:8-5:8 mask layouts) are
+//     expanded on the way (Sec. 4.2): in k_gemm each wave loads its blocks of
+//     the next k-step into registers and writes them, expanded, into the slot
+//     (the 4:2 operand or swizzled dense rows); in k_gemm_ks the 1:4, 1:8 and
+//     2:8 blocks travel through the ring like X and are expanded straight into
+//     the operand registers.  k_expand does the same expansion once per call
+//     into the workspace when the planner prefers that;
 //   - the loads are issued from inline assembly and their completion is
 //     awaited explicitly (vector-memory counter, then one barrier per k-step),
 //     so the compiler does not serialise the ring with conservative waits;
