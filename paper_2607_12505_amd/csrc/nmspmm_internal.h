@@ -66,6 +66,7 @@ constexpr TileCfg kTiles[] = {
     {1, 1, 2, 4, 3, kKSliced},   // 8:  32 ch x  64 tok, k-sliced
     {1, 1, 4, 2, 3, kKSliced},   // 9:  64 ch x  32 tok, k-sliced
     {1, 1, 2, 2, 3, kKSliced},   // 10: 32 ch x  32 tok, k-sliced
+    {2, 2, 4, 5, 2, kOutSplit},  // 11: 128 ch x 160 tok, 2-slot ring (long reductions, narrow outputs)
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 constexpr size_t kLdsPerCu = 160 * 1024;

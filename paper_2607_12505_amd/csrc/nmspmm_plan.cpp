@@ -98,7 +98,7 @@ constexpr int64_t kExpandTileRows = 32;
 // Tile indices used by the rules below (see kTiles).
 constexpr int kT128x128r2 = 0, kT128x64r2 = 1, kT64x128r2 = 2, kT64x64r2 = 3, kT256x256w8 = 4;
 constexpr int kT128x32r2 = 5, kT128x128w8 = 6;
-constexpr int kT64x64ks = 7, kT32x64ks = 8, kT64x32ks = 9, kT32x32ks = 10;
+constexpr int kT64x64ks = 7, kT32x64ks = 8, kT64x32ks = 9, kT32x32ks = 10, kT128x160r2 = 11;
 
 static int64_t tiles_of(int t, int m, int n) {
     return ceil_div(n, kTiles[t].tile_n()) * ceil_div(m, kTiles[t].tile_m());
@@ -185,8 +185,17 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
         // dense and 4:8).  Timed inside the steps of the ViT-L and DeiT-B
         // workloads with the 16-row tile groups (cold operands), 128 x 128 on
         // 8 waves won every other large shape (ViT-L qkv dense 82.7 us against
-        // 88.4 on 4 waves, fc1 103.5 against 110.5) or tied within 2 %.
-        tile = n >= 4096 && k_steps >= 24 ? kT256x256w8 : kT128x128w8;
+        // 88.4 on 4 waves, fc1 103.5 against 110.5) or tied within 2 %, except
+        // the narrow outputs (512-1024 channels) with 8 or more k-steps: 160
+        // tokens per tile on 4 waves, which reuses each weight slice over more
+        // tokens (ViT-L fc2 dense 93.1 us against 102.7, DeiT-B batch 128 fc2
+        // dense 66.8 against 74.5).
+        if (n >= 4096 && k_steps >= 24)
+            tile = kT256x256w8;
+        else if (n >= 512 && n <= 1024 && k_steps >= 8)
+            tile = kT128x160r2;
+        else
+            tile = kT128x128w8;
     } else {
         // Large outputs, 4:2-operand weights, timed the same way: long
         // reductions (24 k-steps or more) the 4-wave 128 x 128 tile, whose

@@ -40,6 +40,8 @@ CASES = [
     (8192, 2048, 512, "sp", (128, 128), False),  # large: 128 x 128
     (4096, 4096, 3072, "mk", (256, 256), False),  # large, heavier operands, 4096 wide, long reduction: 256 x 256
     (4096, 4096, 512, "mk", (128, 128), False),   # ... shorter reduction: 128 x 128 on 8 waves
+    (16500, 1024, 1024, "dn", (128, 160), False),  # ... narrow outputs, 8+ k-steps: 160 tokens (ragged rows)
+    (16500, 1024, 1024, "mk", (128, 160), False),  # ... the same for 4:8, expanded once
     # 32 or more rows of tiles: tiles walked in groups of 16 rows
     (8300, 3072, 2048, "sp", (128, 128), False),  # 65 tile rows: the last group has one row
     (5000, 1024, 512, "sp", (64, 64), False),     # 79 tile rows: the last group has 15

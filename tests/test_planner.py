@@ -120,8 +120,16 @@ def test_large_shapes_use_large_tiles():
     assert p.expand == 0 and nmspmm.plan_kernel_name(p).startswith("k_gemm_ks<2,")
     d = nmspmm.compress_size(768, 3072, 2, 4)
     assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 25216, 1)) == "k_gemm<1, 2, 2, 4, 4, 2>"
-    # the dense baseline of DeiT-B fc2 at batch 128: 8 waves
-    assert nmspmm.plan_kernel_name(nmspmm.dense_plan(25216, 768, 3072, 1)) == "k_gemm<3, 4, 2, 2, 4, 2>"
+    # the dense baseline of DeiT-B fc2 at batch 128 (768 channels, 24 k-steps):
+    # 128 channels x 160 tokens on 4 waves, and the same for ViT-L fc2 and proj;
+    # wider dense outputs keep 128 x 128 on 8 waves (DeiT-B qkv)
+    assert nmspmm.plan_kernel_name(nmspmm.dense_plan(25216, 768, 3072, 1)) == "k_gemm<3, 2, 2, 4, 5, 2>"
+    assert nmspmm.plan_kernel_name(nmspmm.dense_plan(18464, 1024, 4096, 1)) == "k_gemm<3, 2, 2, 4, 5, 2>"
+    assert nmspmm.plan_kernel_name(nmspmm.dense_plan(18464, 1024, 1024, 1)) == "k_gemm<3, 2, 2, 4, 5, 2>"
+    assert nmspmm.plan_kernel_name(nmspmm.dense_plan(25216, 2304, 768, 1)) == "k_gemm<3, 4, 2, 2, 4, 2>"
+    d = nmspmm.compress_size(1024, 4096, 4, 8)           # ... 4:8 on ViT-L fc2 too, expanded once
+    p = nmspmm.spmm_plan(d, 18464, 1)
+    assert (p.tile_n, p.tile_m) == (128, 160) and p.expand == 1
     # the widest outputs of the heavier operands with long reductions: 256 x 256 on 8 waves
     d = nmspmm.compress_size(4096, 4096, 4, 8)
     p = nmspmm.spmm_plan(d, 18464, nmspmm.NM_OUT_I32)
