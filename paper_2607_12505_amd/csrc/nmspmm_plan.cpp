@@ -220,10 +220,16 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
     // like X and expand them in registers, which the separate pass (a second
     // launch) never beats at the token counts they serve (DeiT-B fc2 at
     // batch 8, 1:4: 13.0 us against 16.1).
+    // 1:8, whose expansion is a byte spread and a permute, likewise stays
+    // inside below 2048 channels and 24 k-steps (DeiT-B batch 128 proj:
+    // 26.8 us against 30.0 expanded once; qkv and fc1, 2304 and 3072 wide,
+    // gain 2-6 % from the pass).
     const bool many_rows = ceil_div(mm, kTiles[tile].tile_m()) >= kExpandTileRows;
-    const bool c14_once = k_steps >= 24 || n >= 4096 || tile == kT256x256w8;
     const bool k_sliced = kTiles[tile].layout == kKSliced;
-    plan->expand = kind_is_compact(kind) && many_rows && !k_sliced && (kind != NM_KIND_C14 || c14_once) ? 1 : 0;
+    bool once = true;
+    if (kind == NM_KIND_C14) once = k_steps >= 24 || n >= 4096 || tile == kT256x256w8;
+    if (kind == NM_KIND_C18) once = k_steps >= 24 || n >= 2048 || tile == kT256x256w8;
+    plan->expand = kind_is_compact(kind) && many_rows && !k_sliced && once ? 1 : 0;
     return complete_plan(kind, m, n, k, plan);
 }
 

@@ -39,9 +39,11 @@ def test_plan_rules(shape):
         assert p.split_k == 1
         rows = -(-m // tm)
         compact = d.layout not in (nmspmm.NM_LAYOUT_SP42, nmspmm.NM_LAYOUT_DENSE)
-        c14_once = -(-k // 128) >= 24 or n >= 4096 or (tn, tm) == (256, 256)
+        long_k, on_256 = -(-k // 128) >= 24, (tn, tm) == (256, 256)
+        once = {nmspmm.NM_KIND_C14: long_k or n >= 4096 or on_256,
+                nmspmm.NM_KIND_C18: long_k or n >= 2048 or on_256}.get(d.kind, True)
         k_sliced = "k_gemm_ks" in nmspmm.plan_kernel_name(p)
-        assert p.expand == int(compact and rows >= 32 and not k_sliced and (d.kind != nmspmm.NM_KIND_C14 or c14_once))
+        assert p.expand == int(compact and rows >= 32 and not k_sliced and once)
         if p.expand:
             F, S = -(-n // 16), -(-k // 128)
             want = F * S * 1280 if d.kind in (nmspmm.NM_KIND_C14, nmspmm.NM_KIND_C18, nmspmm.NM_KIND_C28) else n * k
