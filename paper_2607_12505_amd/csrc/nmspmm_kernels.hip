@@ -293,6 +293,8 @@ __device__ inline bool arrive_last(const GemmArgs &a, int tile, int *s_flag) {
 // in the form the matrix instruction reads (paper Sec. 4.2: decoding
 // overlapped with shared-memory placement and matrix issue): the 4:2 operand
 // for 1:4, 1:8 and 2:8, a dense tile for the mask layouts of 3:8, 4:8 and 5:8.
+// (The k-sliced kernel instead stages the 1:4, 1:8 and 2:8 blocks in its ring
+// as stored and expands them into operand registers, see k_gemm_ks.)
 
 template <int KIND>
 struct Kind {
@@ -933,8 +935,9 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
             }
         }
     };
-    // compact kinds: the FN blocks of k-step s into registers, and their
-    // expansion into slot st
+    // mask layouts (3:8-5:8; the loop below calls these only for them): the
+    // FN blocks of k-step s into registers, and their expansion into dense
+    // rows of slot st
     WRegs<KIND> wr[FN];
     auto wload_step = [&](int s) {
         if constexpr (K::kDecode) {
