@@ -140,11 +140,14 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
             tile = kT64x64r2;
         else
             tile = ceil_div(mm, 64) * 64 * 100 <= (int64_t)mm * 115 ? kT32x64ks : kT64x32ks;
-    } else if (!heavy && k_steps >= 16 && mm <= 4096 && tiles_of(kT32x32ks, mm, n) <= 8 * cus) {
+    } else if (!heavy && k_steps >= 16 && k_steps <= 24 && mm <= 4096 && tiles_of(kT32x32ks, mm, n) <= 8 * cus) {
         // A few thousand tokens with a long reduction: the k-sliced 32 x 32
         // tile (the reduction split over the waves) still has more
         // workgroups than the output tiles of any ring tile (DeiT-B fc2 at
-        // batch 8: 16.9 us against 20.5 for 64 x 64).
+        // batch 8, 24 k-steps, inside the workload steps: 16.7 us against
+        // 19 or more for 64 x 64; back to back, 64 x 64 is faster).  At 32
+        // k-steps (Swin-B stage 4 fc2) 64 x 64 wins back to back by a third
+        // and no in-network timing says otherwise, so the rule stops at 24.
         tile = kT32x32ks;
     } else if (k_steps <= 2) {
         // Very short reductions: the output stream dominates; small tiles
