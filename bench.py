@@ -78,7 +78,16 @@ def algorithmic_bytes(g, out_i32, out_f16, sparse=True):
 
 class Prepared:
     """One GEMM of the workload with device buffers and ready-made ctypes
-    arguments for both the sparse call and the dense baseline."""
+    arguments for both the sparse call and the dense baseline.
+
+    A compact weight whose plan expands it once per call (expand = 1) is,
+    when side_stream is set, expanded by nm_expand on that stream into a
+    buffer of its own, and the GEMM on the main stream waits for it: the
+    expansion of a layer then runs while earlier GEMMs are still running,
+    instead of between two GEMMs.  The expansion waits for the previous GEMM
+    that read its buffer."""
+
+    side_stream = None
 
     def __init__(self, cfg, g, x_dev_cache, x_host_cache, out_i32, out_f16, torch, use_dense_kernel):
         self.g = g
@@ -110,7 +119,8 @@ class Prepared:
             # a dense layer inside a layer-wise chain runs the dense kernel on both sides
             self.splan = nmspmm.NmPlan.from_buffer_copy(self.dplan)
             self.sparse_fn = nmspmm.lib().nm_gemm_i8_dense_ex
-        self.sws = self.dws = None
+        self.sws = self.dws = self.ews = self.exp_buf = None
+        self.ahead = False
         self._build_args()
 
     def _workspace(self, plan, old):
@@ -135,6 +145,28 @@ class Prepared:
         else:
             self.sparse_args = (ptr(self.Xd), g.m, ptr(self.Wd), g.n, g.k, ptr(self.Y), ptr(self.scale),
                                 ptr(self.Yh), ptr(self.sws), self.sws.numel(), stream, ctypes.byref(self.splan))
+        self.ahead = bool(self.sparse_kernel and self.splan.expand and Prepared.side_stream is not None)
+        if self.ahead:
+            torch = self._torch
+            e, nbytes = nmspmm.expand_size(self.packed.desc)
+            if self.exp_buf is None or self.exp_buf.numel() < nbytes:
+                self.exp_buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+            self.edesc = e
+            # the plan of the GEMM on the expanded weight: the same tile and split
+            self.eplan = nmspmm.spmm_plan_complete(e, g.m, nmspmm.make_plan(e.kind, self.splan.tile,
+                                                                            self.splan.split_k, 0))
+            self.ews = self._workspace(self.eplan, self.ews)
+            side = ctypes.c_void_p(Prepared.side_stream.cuda_stream)
+            vals = self.exp_buf.data_ptr()
+            meta = ctypes.c_void_p(vals + e.vals_bytes) if e.meta_bytes else None
+            self.expand_args = (ctypes.byref(self.packed.desc), ptr(self.dw.vals), ptr(self.dw.meta),
+                                ptr(self.exp_buf), self.exp_buf.numel(), side)
+            self.ahead_args = (ptr(self.Xd), g.m, ctypes.c_void_p(vals), meta, ctypes.byref(self.edesc), ptr(self.Y),
+                               ptr(self.scale), ptr(self.Yh), ptr(self.ews), self.ews.numel(), stream,
+                               ctypes.byref(self.eplan))
+            self.ev_expanded = torch.cuda.Event()
+            self.ev_used = torch.cuda.Event()
+            self.main_stream = torch.cuda.current_stream()
 
     def set_sparse_plan(self, plan):
         """Runs the sparse-leg call with `plan` from now on (a completed plan
@@ -153,8 +185,23 @@ class Prepared:
     def kernel_name(self, plan):
         return nmspmm.plan_kernel_name(plan)
 
+    def expands_in_call(self):
+        """Whether the sparse call launches an expansion kernel before its GEMM."""
+        return bool(self.sparse_kernel and self.splan.expand and not self.ahead)
+
     def run_sparse(self):
-        st = self.sparse_fn(*self.sparse_args)
+        if self.ahead:
+            side = Prepared.side_stream
+            side.wait_event(self.ev_used)
+            st = nmspmm.lib().nm_expand(*self.expand_args)
+            if st:
+                raise nmspmm.NmError(st, f"expand {self.g.name}")
+            self.ev_expanded.record(side)
+            self.main_stream.wait_event(self.ev_expanded)
+            st = nmspmm.lib().nm_spmm_ex(*self.ahead_args)
+            self.ev_used.record(self.main_stream)
+        else:
+            st = self.sparse_fn(*self.sparse_args)
         if st:
             raise nmspmm.NmError(st, f"sparse {self.g.name}")
 
@@ -327,6 +374,16 @@ def sleep_cycles_for(launches: int) -> int:
     return int(2.1e9 * min(12e-6 * launches, 20e-3))
 
 
+def hold_side_stream(torch):
+    """The side stream's next work waits for everything issued so far on the
+    current stream (so expansions of a leg cannot run during an earlier,
+    untimed leg or sleep)."""
+    if Prepared.side_stream is not None:
+        ev = torch.cuda.Event()
+        ev.record()
+        Prepared.side_stream.wait_event(ev)
+
+
 def timed_steps(preps, steps, torch):
     """The contract's timed region: `steps` steps of the sparse leg back to
     back between two synchronisations.  Returns (wall ms per step, event ms of
@@ -337,6 +394,7 @@ def timed_steps(preps, steps, torch):
     w0 = time.perf_counter()
     for e0, e1 in ev:
         e0.record()
+        hold_side_stream(torch)
         for p in preps:
             p.run_sparse()
         e1.record()
@@ -362,6 +420,7 @@ def abba(torch, calls_a, calls_b, rounds, per_call=False):
         for which in (0, 1, 1, 0):
             ev = [E(enable_timing=True)]
             ev[0].record()
+            hold_side_stream(torch)
             for c in (calls_a if which == 0 else calls_b):
                 c()
                 if per_call:
@@ -447,6 +506,10 @@ def main():
                          "real launches)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after timing, run one plain device copy of MIB MiB (profiler counter calibration)")
+    ap.add_argument("--expand-ahead", action="store_true",
+                    help="for plans that expand a compact weight once per call, run nm_expand on a second stream "
+                         "ahead of the GEMM instead of inside the sparse call (measured slower on ViT-L: the "
+                         "cross-stream waits cost more than the expansion latency they hide)")
     ap.add_argument("--traffic", type=str, default=None,
                     help="JSON record of measured HBM bytes per launch of the dominant kernel "
                          "(default: profiles/traffic_<workload>.json, used only if it matches this kernel source)")
@@ -465,6 +528,8 @@ def main():
     torch.cuda.set_device(0)
 
     t0 = time.perf_counter()
+    if args.expand_ahead:
+        Prepared.side_stream = torch.cuda.Stream()   # default priority
     work, preps = prepare(args.config, torch)
     out_i32, out_f16 = work.out_int32, work.out_f16
     log(f"workload {work.name}: {len(preps)} GEMMs, outputs {'int32' if out_i32 else ''}"
@@ -515,7 +580,7 @@ def main():
     # the kernel's own launch time: calls that also expand a compact weight
     # first (a second kernel inside the same call) are left out of the
     # average when calls without it exist
-    plain = [i for i in dom_idx if not preps[i].splan.expand] or dom_idx
+    plain = [i for i in dom_idx if not preps[i].expands_in_call()] or dom_idx
     avg_ms = float(np.mean([ts[i] for i in plain]))
     dom_bytes = sum(algorithmic_bytes(preps[i].g, out_i32, out_f16, sparse=preps[i].sparse_kernel) for i in dom_idx)
     dom_ops = sum(preps[i].g.dense_eq_ops for i in dom_idx)
@@ -602,6 +667,8 @@ def main():
         "frac_of_int8_peak": round(float(value / PEAK_INT8_TOPS), 4),
         "per_pattern": per_pattern,
         "cache_state": cache_state(preps),
+        "compact_weight_expansion": ("nm_expand on a second stream ahead of the GEMM, for plans with expand = 1"
+                                     if args.expand_ahead else "in the sparse call"),
         "roofline": roofline,
     }
     if not args.no_mfma_ceiling:

@@ -280,6 +280,39 @@ nm_status nm_gemm_i8_dense_ex(const int8_t *X, int m, const int8_t *W, int n, in
                               int32_t *Y, const float *scale, uint16_t *Yh,
                               void *ws, size_t ws_bytes, void *stream, const nm_plan *plan);
 
+/* ---------------------------------------------------------------- expansion
+ * The decode of a compact weight (Sec. 4.2) as a pass of its own: the form a
+ * plan with expand = 1 builds in its workspace, written to a caller buffer
+ * instead, so that a caller can run it ahead of the GEMM that reads it (on
+ * another stream, overlapping earlier work), or once at load time. */
+
+/* Descriptor and size of the expanded form of a compact packed weight (the
+ * C14, C18, C28 and MKn layouts):
+ *   C14, C18, C28 -> NM_LAYOUT_SP42 (the descriptor nm_compress_size gives for
+ *                    2:4 and the same n, k): the values (expanded->vals_bytes)
+ *                    followed by the positions (expanded->meta_bytes) in one
+ *                    buffer.  Every group holds the layout's nonzeros; the
+ *                    padding slots hold zeros, at positions that need not be
+ *                    the canonical ones (nm_decompress may reject the result;
+ *                    the GEMMs compute with it exactly).
+ *   MK3, MK4, MK5 -> NM_LAYOUT_DENSE (the descriptor of 8:8 and the same n, k):
+ *                    W [n x k] row-major, meta_bytes 0.
+ * *bytes = expanded->vals_bytes + expanded->meta_bytes.  Host only.  Errors:
+ * NM_ERR_ARG (NULL pointer, inconsistent desc, or a layout that is already an
+ * operand form: SP42 or DENSE). */
+nm_status nm_expand_size(const nm_desc *desc, nm_desc *expanded, size_t *bytes);
+
+/* Expands a device packed weight (vals, meta as for nm_spmm) into the device
+ * buffer out of out_bytes (>= the size above), on `stream`, asynchronously.
+ * The result is a packed weight of the expanded descriptor: nm_spmm_ex (or
+ * nm_spmm_out) with that descriptor, vals = out and meta = out +
+ * expanded->vals_bytes (NULL for DENSE) computes the same outputs as the
+ * compact weight.  Errors: as nm_expand_size, NM_ERR_ARG for a NULL or
+ * misaligned pointer, NM_ERR_WORKSPACE when out_bytes is too small (nothing
+ * written), NM_ERR_HIP. */
+nm_status nm_expand(const nm_desc *desc, const int8_t *vals, const uint8_t *meta, int8_t *out,
+                    size_t out_bytes, void *stream);
+
 /* ---------------------------------------------------------------- INT8 chaining
  * The paper deploys the linears in INT8 end to end (Sec. 6.3).  Between two
  * linears the int32 result must become the next linear's int8 input; the

@@ -246,6 +246,33 @@ extern "C" nm_status nm_gemm_i8_dense(const int8_t *X, int m, const int8_t *W, i
     return nm_gemm_i8_dense_ex(X, m, W, n, k, Y, scale, Yh, ws, ws_bytes, stream, nullptr);
 }
 
+extern "C" nm_status nm_expand_size(const nm_desc *desc, nm_desc *expanded, size_t *bytes) {
+    nm_status st = check_desc(desc);
+    if (st != NM_OK) return st;
+    if (!expanded || !bytes) return NM_ERR_ARG;
+    const int kind = kind_of(desc);
+    if (!kind_is_compact(kind)) return NM_ERR_ARG;
+    // the expanded form is the packed form of 2:4 (4:2-operand kinds) or of a
+    // dense pattern (mask kinds) for the same shape
+    const bool sp = expanded_kind(kind) == NM_KIND_SP42;
+    st = nm_compress_size(desc->n, desc->k, sp ? 2 : 8, sp ? 4 : 8, expanded);
+    if (st != NM_OK) return st;
+    if (expanded->vals_bytes + expanded->meta_bytes != expanded_bytes(kind, desc->n, desc->k)) return NM_ERR_ARG;
+    *bytes = (size_t)(expanded->vals_bytes + expanded->meta_bytes);
+    return NM_OK;
+}
+
+extern "C" nm_status nm_expand(const nm_desc *desc, const int8_t *vals, const uint8_t *meta, int8_t *out,
+                               size_t out_bytes, void *stream) {
+    nm_desc e;
+    size_t need = 0;
+    nm_status st = nm_expand_size(desc, &e, &need);
+    if (st != NM_OK) return st;
+    if (!vals || !meta || !out || !aligned16(vals) || !aligned16(meta) || !aligned16(out)) return NM_ERR_ARG;
+    if (out_bytes < need) return NM_ERR_WORKSPACE;
+    return launch_expand(kind_of(desc), vals, meta, desc->n, desc->k, out, stream) == 0 ? NM_OK : NM_ERR_HIP;
+}
+
 extern "C" nm_status nm_quantize_f16(const uint16_t *x, int64_t count, float inv_scale, int8_t *xq, void *stream) {
     if (count < 0) return NM_ERR_SHAPE;
     if (count == 0) return NM_OK;

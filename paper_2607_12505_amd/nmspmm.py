@@ -33,7 +33,7 @@ EXPORTED = (
     "nm_status_string", "nm_compress_size", "nm_compress", "nm_decompress", "nm_num_tiles",
     "nm_tile_info", "nm_plan_kernel_name", "nm_spmm_plan", "nm_spmm_plan_complete", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
     "nm_spmm", "nm_spmm_ex", "nm_gemm_i8_dense", "nm_gemm_i8_dense_ex", "nm_spmm_out", "nm_gemm_i8_dense_out",
-    "nm_quantize_f16", "nm_spmm_noalloc",
+    "nm_quantize_f16", "nm_spmm_noalloc", "nm_expand_size", "nm_expand",
 )
 NM_NOALLOC_SCRATCH_BYTES = 16384 + (32 << 20)
 
@@ -111,6 +111,8 @@ def lib() -> ctypes.CDLL:
             "nm_gemm_i8_dense_out": ([vp, i32, vp, i32, i32, ctypes.POINTER(NmOutputs), vp, sz, vp, pp], i32),
             "nm_quantize_f16": ([vp, ctypes.c_int64, ctypes.c_float, vp, vp], i32),
             "nm_spmm_noalloc": ([vp, i32, vp, vp, pd, ctypes.POINTER(NmOutputs), vp, pp], i32),
+            "nm_expand_size": ([pd, pd, ctypes.POINTER(sz)], i32),
+            "nm_expand": ([pd, vp, vp, vp, sz, vp], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -474,6 +476,36 @@ def gemm_i8_dense(X, W, Y=None, scale=None, Yh=None, plan: Optional[NmPlan] = No
                                     _stream(stream), pl)
     _check(st, "nm_gemm_i8_dense_out")
     return Y, Yh, Yq
+
+
+def expand_size(desc: NmDesc):
+    """nm_expand_size: (descriptor of the expanded weight, bytes of its buffer)."""
+    e = NmDesc()
+    nbytes = ctypes.c_size_t(0)
+    _check(lib().nm_expand_size(ctypes.byref(desc), ctypes.byref(e), ctypes.byref(nbytes)), "nm_expand_size")
+    return e, nbytes.value
+
+
+def expand(w: DeviceWeight, out=None, stream=None) -> DeviceWeight:
+    """nm_expand: the compact weight w expanded (2:4 layout or dense W) into
+    out (a uint8 or int8 device buffer of at least expand_size() bytes; one is
+    allocated when None).  Returns a DeviceWeight of the expanded descriptor
+    whose vals and meta are views of out."""
+    torch = _torch()
+    d = w.desc
+    e, nbytes = expand_size(d)
+    _need(w.vals, "w.vals", (torch.int8,), numel=d.vals_bytes)
+    _need(w.meta, "w.meta", (torch.uint8,), numel=d.meta_bytes)
+    if out is None:
+        out = torch.empty(nbytes, dtype=torch.uint8, device=w.vals.device)
+    _need(out, "out", (torch.uint8, torch.int8), numel=nbytes)
+    if out.dim() != 1:
+        raise ValueError("out: must be 1-D")
+    _on_device((("w.vals", w.vals), ("w.meta", w.meta), ("out", out)))
+    _check(lib().nm_expand(ctypes.byref(d), _ptr(w.vals), _ptr(w.meta), _ptr(out), out.numel(), _stream(stream)),
+           "nm_expand")
+    b = out.view(torch.uint8)
+    return DeviceWeight(b[:e.vals_bytes].view(torch.int8), b[e.vals_bytes:e.vals_bytes + e.meta_bytes], e)
 
 
 def quantize_f16(x, inv_scale: float, xq=None, stream=None):

@@ -56,6 +56,20 @@ def test_one_hip_runtime_per_process():
     assert len(runtimes) == 1, runtimes
 
 
+def test_expanded_descriptors():
+    # every compact layout expands to the 2:4 layout or to a dense W of its shape
+    for (N, M), sp in (((1, 4), True), ((1, 8), True), ((2, 8), True), ((3, 8), False), ((4, 8), False),
+                       ((5, 8), False)):
+        for n, k in ((64, 128), (200, 1040), (4, 16 * M)):
+            d = nmspmm.compress_size(n, k, N, M)
+            e, nbytes = nmspmm.expand_size(d)
+            ref = nmspmm.compress_size(n, k, 2, 4) if sp else nmspmm.compress_size(n, k, 8, 8)
+            assert e.layout == (nmspmm.NM_LAYOUT_SP42 if sp else nmspmm.NM_LAYOUT_DENSE)
+            assert bytes(e) == bytes(ref)
+            F, S = -(-n // 16), -(-k // 128)
+            assert nbytes == (F * S * 1280 if sp else n * k)
+
+
 def test_status_strings():
     for s in range(7):
         assert nmspmm.status_string(s)
@@ -92,6 +106,16 @@ def test_host_side_argument_checks_need_no_gpu():
     d = nmspmm.compress_size(64, 128, 2, 4)
     assert L.nm_spmm_out(fake, 64, fake, fake, ctypes.byref(d), ctypes.byref(o), nul, 0, nul, None) == \
         nmspmm.NM_ERR_ARG
+    # expansion: only compact layouts, a large enough buffer, aligned pointers
+    c28 = nmspmm.compress_size(64, 128, 2, 8)
+    e, nbytes = nmspmm.NmDesc(), ctypes.c_size_t(0)
+    for stored in (d, nmspmm.compress_size(64, 128, 8, 8)):                  # SP42 and DENSE
+        assert L.nm_expand_size(ctypes.byref(stored), ctypes.byref(e), ctypes.byref(nbytes)) == nmspmm.NM_ERR_ARG
+        assert L.nm_expand(ctypes.byref(stored), fake, fake, fake, 1 << 20, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_expand_size(ctypes.byref(c28), None, ctypes.byref(nbytes)) == nmspmm.NM_ERR_ARG
+    assert L.nm_expand(ctypes.byref(c28), fake, fake, fake, 64 * 1280 // 16 - 1, nul) == nmspmm.NM_ERR_WORKSPACE
+    assert L.nm_expand(ctypes.byref(c28), fake, fake, misaligned, 1 << 20, nul) == nmspmm.NM_ERR_ARG
+    assert L.nm_expand(ctypes.byref(c28), fake, nul, fake, 1 << 20, nul) == nmspmm.NM_ERR_ARG
     assert L.nm_quantize_f16(fake, -1, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_SHAPE
     assert L.nm_quantize_f16(misaligned, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_ARG
     P = nmprobe.lib()
@@ -142,6 +166,8 @@ def test_launch_failures_report_nm_err_hip():
     assert L.nm_gemm_i8_dense_ex(fake, 64, fake, 64, 128, fake, nul, nul, nul, 0, nul, None) == nmspmm.NM_ERR_HIP
     assert L.nm_quantize_f16(fake, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_HIP
     assert L.nm_workspace_init(fake, 64, nul) == nmspmm.NM_ERR_HIP
+    c14 = nmspmm.compress_size(64, 128, 1, 4)
+    assert L.nm_expand(ctypes.byref(c14), fake, fake, fake, 1 << 20, nul) == nmspmm.NM_ERR_HIP
     P = nmprobe.lib()
     assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, fake, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_HIP
     khz = ctypes.c_int32(0)
