@@ -178,7 +178,8 @@ def sweep(configs, torch, reps, out_path):
                 "planned": list(chosen), "best": list(best), "t_planned_us": t_plan, "t_best_us": times[best],
                 "t_fixed_split1_us": t_fixed, "times": {f"{t}/{s}": v for (t, s), v in times.items()},
             })
-            log(f"cfg{cfg} {g.name:<20} m={g.m:<6} k={g.k:<5} n={g.n:<5} planned t{chosen[0]}/s{chosen[1]} "
+            wname = wl.workload(cfg).name if isinstance(cfg, int) else cfg
+            log(f"{wname} {g.name:<20} m={g.m:<6} k={g.k:<5} n={g.n:<5} planned t{chosen[0]}/s{chosen[1]} "
                 f"{t_plan:7.1f} us  best t{best[0]}/s{best[1]} {times[best]:7.1f} us  "
                 f"norm {times[best] / t_plan:.3f}")
     summary = sweep_summary([r for r in rows if r["pattern"] != "dense" and r["cfg"] != "grid"])
@@ -675,8 +676,12 @@ def write_sweep_report(sweep_json, path):
                f"performance {ds['avg_norm_perf']}, worst {ds['worst_norm_perf']}.", ""]
     md += ["| workload | m | k | n | N:M | planner tile/split | us | best tile/split | us | norm |",
            "|---|---:|---:|---:|---|---|---:|---|---:|---:|"]
+    names = {}
     for r in d["rows"]:
-        md.append(f"| cfg{r['cfg']} {r['gemm']} | {r['m']} | {r['k']} | {r['n']} | {r['pattern']} | "
+        c = r["cfg"]
+        if c not in names:
+            names[c] = wl.workload(c).name if isinstance(c, int) else str(c)
+        md.append(f"| {names[c]} {r['gemm']} | {r['m']} | {r['k']} | {r['n']} | {r['pattern']} | "
                   f"{r['planned'][0]}/{r['planned'][1]} | {r['t_planned_us']:.1f} | {r['best'][0]}/{r['best'][1]} | "
                   f"{r['t_best_us']:.1f} | {r['t_best_us'] / r['t_planned_us']:.3f} |")
     with open(path, "w") as f:

@@ -93,7 +93,7 @@ def test_sweep_report(tmp_path):
     src.write_text(json.dumps(d))
     subprocess.run([sys.executable, os.path.join(ROOT, "bench_experiments.py"), "--sweep-report", str(src), "--report", str(out)],
                    check=True)
-    assert "| cfg1 qkv | 12608 | 384 | 1152 | 2:4 | 17/1 | 19.5 | 17/1 | 19.5 | 1.000 |" in out.read_text()
+    assert "| deit_small_b64 qkv | 12608 | 384 | 1152 | 2:4 | 17/1 | 19.5 | 17/1 | 19.5 | 1.000 |" in out.read_text()
 
 
 def test_more_than_one_gpu_is_refused():
