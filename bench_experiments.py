@@ -793,7 +793,8 @@ def launch_labels(cfg):
     from paper_2607_12505_amd import workloads as wl
     labels = {}
     for g in wl.workload(cfg).gemms:
-        short = g.name.split(" ", 1)[1].split(" ")[0]
+        # the linear with its batch or stage prefix, without the pattern or the layer index
+        short = " ".join(t for t in g.name.split() if ":" not in t and not (t[0] == "L" and t[1:].isdigit()))
         if g.N == g.M:
             plans = [("dense", nmspmm.dense_plan(g.m, g.n, g.k, nmspmm.NM_OUT_I32))]
         else:
@@ -840,8 +841,82 @@ def _grid_counters(d, kernel, grid):
 
 
 def _workload_cfg(line):
-    return {"deit_small_b64": 1, "deit_base_b128": 2, "swin_base_b64": 3,
-            "vit_large_384_b32_chain": 4}.get(line["config"]["workload"])
+    from paper_2607_12505_amd import workloads as wl
+    names = {wl.workload(c).name: c for c in range(5)}
+    return names.get(line["config"]["workload"])
+
+
+# Derived columns of the stall-counter table: (title, numerator, denominator,
+# scale, format); a column is shown when its counters are present.
+_STALL_COLUMNS = (
+    ("waiting %", "SQ_WAIT_ANY", "SQ_WAVE_CYCLES", 100.0, "{:.0f}"),
+    ("issue-blocked %", "SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES", 100.0, "{:.0f}"),
+    ("issuing %", "SQ_ACTIVE_INST_ANY", "SQ_WAVE_CYCLES", 100.0, "{:.0f}"),
+    ("LDS-issue wait %", "SQ_WAIT_INST_LDS", "SQ_WAVE_CYCLES", 100.0, "{:.1f}"),
+    ("MFMA busy %", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", 100.0 * 8 / 1024, "{:.1f}"),
+    ("LDS conflict %", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", 100.0, "{:.2f}"),
+    ("LDS data FIFO full %", "SQ_LDS_DATA_FIFO_FULL", "SQ_LDS_IDX_ACTIVE", 100.0, "{:.1f}"),
+    ("L2 read latency (cycles)", "TCP_TCC_READ_REQ_LATENCY_sum", "TCP_TCC_READ_REQ_sum", 1.0, "{:.0f}"),
+)
+
+
+def pmc_stall_table(dirs, cfg, commands, out_md):
+    """Per launch shape (kernel and grid) of workload cfg: per-dispatch means of
+    the counters found in the rocprofv3 counter-collection CSVs of `dirs` (one
+    directory per --pmc pass of the same bench run), as the ratios of
+    _STALL_COLUMNS.  Wave-cycle counters are summed over all waves, so their
+    ratios are fractions of the waves' resident time."""
+    import csv
+    import glob
+    import re
+    per = {}
+    for d in dirs:
+        for r in csv.DictReader(open(glob.glob(os.path.join(d, "*_counter_collection.csv"))[0])):
+            m = re.search(r"(k_gemm(?:_ks)?<[^>]*>)", r["Kernel_Name"])
+            if not m:
+                continue
+            k = m.group(1)
+            key = (k, _workgroups(k, int(r["Grid_Size"])))
+            disp = per.setdefault(key, {}).setdefault(r["Counter_Name"], {})
+            tag = (d, r["Dispatch_Id"])
+            disp[tag] = disp.get(tag, 0.0) + float(r["Counter_Value"])
+    labels = launch_labels(cfg)
+    from paper_2607_12505_amd import workloads as wl
+    cols = [c for c in _STALL_COLUMNS if any(c[1] in v and c[2] in v for v in per.values())]
+    md = [f"# rocprofv3 stall counters per launch shape: workload `{wl.workload(cfg).name}`", "",
+          "Commands (repository root as working directory of the bench; rocprofv3 run from /tmp):", "", "```"]
+    md += list(commands) + ["```", "",
+                            "Per dispatch means; the wave-cycle counters (SQ_WAVE_CYCLES, SQ_WAIT_ANY, SQ_WAIT_INST_ANY, "
+                            "SQ_ACTIVE_INST_ANY, SQ_WAIT_INST_LDS) are summed over every resident wave, so their ratios "
+                            "are shares of the waves' resident time: *waiting* = at an s_waitcnt or barrier, "
+                            "*issue-blocked* = ready but its functional unit (mostly the matrix core) busy, *issuing* = "
+                            "issuing an instruction.  MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x "
+                            "1024 SIMDs); LDS ratios per LDS-active cycle; L2 read latency = TCP_TCC_READ_REQ_LATENCY / "
+                            "TCP_TCC_READ_REQ (cycles from the CU's L1 to L2 and back, per request).", "",
+          "| kernel | workgroups | GEMMs | dispatches | " + " | ".join(c[0] for c in cols) + " |",
+          "|---|---:|---|---:|" + "---:|" * len(cols)]
+    rows = []
+    for key, cs in per.items():
+        if not cols or not all(c[1] in cs and c[2] in cs for c in cols[:1]):
+            continue
+        gemms = labels.get(key)
+        what = ", ".join(sorted({f"{g[0]} {g[4]}" for g in gemms})) if gemms else "other"
+        if gemms and len({g[1:4] for g in gemms}) == 1:
+            _, m, k, n, _ = sorted(gemms)[0]
+            what += f" (m {m}, k {k}, n {n})"
+        vals = []
+        for _, num, den, scale, fmt in cols:
+            if num in cs and den in cs:
+                a, b = np.mean(list(cs[num].values())), np.mean(list(cs[den].values()))
+                vals.append(fmt.format(scale * a / b) if b else "")
+            else:
+                vals.append("")
+        nd = len(cs[cols[0][2]])   # dispatches of the pass that holds the first column's counters
+        rows.append((-nd, f"| `{key[0]}` | {key[1]} | {what} | {nd} | " + " | ".join(vals) + " |"))
+    md += [r for _, r in sorted(rows)]
+    with open(out_md, "w") as f:
+        f.write("\n".join(md) + "\n")
+    print("\n".join(md))
 
 
 def launch_shape_table(line, trace_dir, fetch_dir, write_dir, f_scale, w_scale, sq_dir):
@@ -1026,6 +1101,10 @@ def main():
     ap.add_argument("--bench-json", type=str, default=None, help="bench output line used by --rocprof-summary")
     ap.add_argument("--rocprof-sq", type=str, default=None,
                     help="rocprofv3 counter output with MFMA busy / LDS bank conflict counters (--rocprof-summary)")
+    ap.add_argument("--pmc-stalls", nargs="+", metavar="PASS_DIR", default=None,
+                    help="per-launch-shape table of stall counters from rocprofv3 --pmc passes of one bench run "
+                         "(no GPU needed; with --summary-out, --commands, --stall-config)")
+    ap.add_argument("--stall-config", type=int, default=4, help="workload of the --pmc-stalls bench run")
     ap.add_argument("--summary-out", type=str, default=None, help="markdown file written by --rocprof-summary")
     ap.add_argument("--commands", type=str, default=None, help="file with the profiling commands to quote")
     ap.add_argument("--copy-calibration", type=int, default=256, metavar="MIB",
@@ -1050,6 +1129,10 @@ def main():
 
     if args.sweep_report:
         write_sweep_report(args.sweep_report, args.report)
+        return
+    if args.pmc_stalls:
+        cmds = open(args.commands).read().strip().splitlines() if args.commands else []
+        pmc_stall_table(args.pmc_stalls, args.stall_config, cmds, args.summary_out)
         return
     if args.rocprof_summary:
         cmds = open(args.commands).read().strip().splitlines() if args.commands else []

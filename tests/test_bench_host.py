@@ -99,3 +99,33 @@ def test_sweep_report(tmp_path):
 def test_more_than_one_gpu_is_refused():
     p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True, text=True)
     assert p.returncode == 2 and "one GPU" in p.stderr
+
+
+def test_pmc_stall_table_by_hand(tmp_path):
+    # one launch shape of the DeiT-Tiny workload (the planner's 2:4 kernel on fc1), two passes
+    from paper_2607_12505_amd import nmspmm
+    g = wl.workload(0).gemms[0]
+    plan = nmspmm.spmm_plan(nmspmm.compress_size(g.n, g.k, g.N, g.M), g.m, nmspmm.NM_OUT_I32)
+    name = nmspmm.plan_kernel_name(plan)
+    threads = 256 if name.startswith("k_gemm_ks") else 64 * int(name.split(",")[1]) * int(name.split(",")[2])
+    kern = f"void nmspmm::(anonymous namespace)::{name}(nmspmm::GemmArgs)"
+    cols = ["Dispatch_Id", "Grid_Size", "Kernel_Name", "Counter_Name", "Counter_Value"]
+    p1, p2 = tmp_path / "p1", tmp_path / "p2"
+    p1.mkdir()
+    p2.mkdir()
+    grid = plan.grid * threads
+    # two dispatches, two counter rows each (summed per dispatch)
+    _write_csv(p1 / "b_counter_collection.csv", cols,
+               [[1, grid, kern, "SQ_WAVE_CYCLES", 600], [1, grid, kern, "SQ_WAVE_CYCLES", 400],
+                [1, grid, kern, "SQ_WAIT_ANY", 250], [1, grid, kern, "SQ_WAIT_ANY", 250],
+                [2, grid, kern, "SQ_WAVE_CYCLES", 1000], [2, grid, kern, "SQ_WAIT_ANY", 300]])
+    _write_csv(p2 / "b_counter_collection.csv", cols,
+               [[7, grid, kern, "TCP_TCC_READ_REQ_LATENCY_sum", 5000], [7, grid, kern, "TCP_TCC_READ_REQ_sum", 20]])
+    out = tmp_path / "s.md"
+    bench_experiments.pmc_stall_table([str(p1), str(p2)], 0, ["cmd"], str(out))
+    text = out.read_text()
+    # waiting = mean(500, 300) / mean(1000, 1000) = 40 %; L2 latency 5000 / 20 = 250 cycles
+    row = [line for line in text.splitlines() if line.startswith(f"| `{name}`")][0]
+    cells = [c.strip() for c in row.strip("|").split("|")]
+    assert cells[1] == str(plan.grid) and cells[3] == "2"
+    assert cells[4] == "40" and cells[-1] == "250"
