@@ -228,13 +228,14 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
     // 26.8 us against 30.0 expanded once; qkv and fc1, 2304 and 3072 wide,
     // gain 2-6 % from the pass).  The pass costs a few microseconds whatever
     // the size (a second launch that waits for the first), so it is taken
-    // only for GEMMs of 2^34 multiply-adds or more: inside the steps of
+    // only for GEMMs of 2^33 multiply-adds or more: inside the steps of
     // DeiT-S (at most 7.4e9) and Swin-B (at most 6.6e9) the in-kernel
     // expansion won every 2:8 and 4:8 GEMM, by 10-25 % (e.g. Swin-B stage 3
-    // fc1 2:8 19.5 us against 24.3).
+    // fc1 2:8 19.5 us against 24.3); from DeiT-B batch 128 proj up (1.5e10)
+    // the pass wins (proj 2:8 30.0 us against 34.9).
     const bool many_rows = ceil_div(mm, kTiles[tile].tile_m()) >= kExpandTileRows;
     const bool k_sliced = kTiles[tile].layout == kKSliced;
-    const bool long_gemm = (int64_t)mm * n * k >= ((int64_t)1 << 34);
+    const bool long_gemm = (int64_t)mm * n * k >= ((int64_t)1 << 33);
     bool once = long_gemm;
     if (kind == NM_KIND_C14) once = once && (k_steps >= 24 || n >= 4096 || tile == kT256x256w8);
     if (kind == NM_KIND_C18) once = once && (k_steps >= 24 || n >= 2048 || tile == kT256x256w8);

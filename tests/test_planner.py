@@ -41,7 +41,7 @@ def test_plan_rules(shape):
         compact = d.layout not in (nmspmm.NM_LAYOUT_SP42, nmspmm.NM_LAYOUT_DENSE)
         long_k, on_256 = -(-k // 128) >= 24, (tn, tm) == (256, 256)
         once = {nmspmm.NM_KIND_C14: long_k or n >= 4096 or on_256,
-                nmspmm.NM_KIND_C18: long_k or n >= 2048 or on_256}.get(d.kind, True) and m * n * k >= 2 ** 34
+                nmspmm.NM_KIND_C18: long_k or n >= 2048 or on_256}.get(d.kind, True) and m * n * k >= 2 ** 33
         k_sliced = "k_gemm_ks" in nmspmm.plan_kernel_name(p)
         assert p.expand == int(compact and rows >= 32 and not k_sliced and once)
         if p.expand:
