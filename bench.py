@@ -121,6 +121,8 @@ class Prepared:
             self.sparse_fn = nmspmm.lib().nm_gemm_i8_dense_ex
         self.sws = self.dws = self.ews = self.exp_buf = None
         self.ahead = False
+        self.pre_expanded = False     # the weight is expanded by the previous GEMM's launch (tail mode)
+        self.tail_next = None         # the next GEMM, whose weight this launch expands (tail mode)
         self._build_args()
 
     def _workspace(self, plan, old):
@@ -168,6 +170,50 @@ class Prepared:
             self.ev_used = torch.cuda.Event()
             self.main_stream = torch.cuda.current_stream()
 
+    def _build_expanded(self):
+        """Buffer, descriptor, plan and ctypes arguments of the GEMM on this
+        layer's expanded weight (the same tile and split as its plan)."""
+        torch = self._torch
+        g = self.g
+        ptr = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None
+        e, nbytes = nmspmm.expand_size(self.packed.desc)
+        if self.exp_buf is None or self.exp_buf.numel() < nbytes:
+            self.exp_buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        self.edesc = e
+        self.eplan = nmspmm.spmm_plan_complete(e, g.m, nmspmm.make_plan(e.kind, self.splan.tile, self.splan.split_k, 0))
+        self.ews = self._workspace(self.eplan, self.ews)
+        vals = self.exp_buf.data_ptr()
+        meta = ctypes.c_void_p(vals + e.vals_bytes) if e.meta_bytes else None
+        stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        self.pre_args = (ptr(self.Xd), g.m, ctypes.c_void_p(vals), meta, ctypes.byref(self.edesc), ptr(self.Y),
+                         ptr(self.scale), ptr(self.Yh), ptr(self.ews), self.ews.numel(), stream,
+                         ctypes.byref(self.eplan))
+
+    def carry_expansion_of(self, nxt):
+        """Tail mode: this GEMM's launch also expands the weight of `nxt` (a
+        GEMM whose plan expands its compact weight once per call), which then
+        runs on the expanded weight with no expansion launch of its own."""
+        nxt.pre_expanded = True
+        nxt._build_expanded()
+        self.tail_next = nxt
+        self.job = nmspmm.NmExpandJob(ctypes.pointer(nxt.packed.desc), nxt.dw.vals.data_ptr(),
+                                      nxt.dw.meta.data_ptr(), nxt.exp_buf.data_ptr(), nxt.exp_buf.numel())
+        self.outs = nmspmm.NmOutputs(self.Y.data_ptr() if self.Y is not None else None,
+                                     self.Yh.data_ptr() if self.Yh is not None else None,
+                                     self.scale.data_ptr(), None, None)
+        a = self.sparse_args
+        if self.pre_expanded:
+            a = self.pre_args
+        if self.sparse_kernel:
+            # (X, m, vals, meta, desc, out, ws, ws_bytes, stream, plan, job)
+            self.tail_fn = nmspmm.lib().nm_spmm_out_expand
+            self.tail_args = (a[0], a[1], a[2], a[3], a[4], ctypes.byref(self.outs), a[8], a[9], a[10], a[11],
+                              ctypes.byref(self.job))
+        else:
+            self.tail_fn = nmspmm.lib().nm_gemm_i8_dense_out_expand
+            self.tail_args = (a[0], a[1], a[2], a[3], a[4], ctypes.byref(self.outs), a[8], a[9], a[10], a[11],
+                              ctypes.byref(self.job))
+
     def set_sparse_plan(self, plan):
         """Runs the sparse-leg call with `plan` from now on (a completed plan
         of this GEMM's kind); the workspace grows as the plan needs."""
@@ -186,11 +232,17 @@ class Prepared:
         return nmspmm.plan_kernel_name(plan)
 
     def expands_in_call(self):
-        """Whether the sparse call launches an expansion kernel before its GEMM."""
-        return bool(self.sparse_kernel and self.splan.expand and not self.ahead)
+        """Whether the sparse call launches an expansion (a kernel before its
+        GEMM, or workgroups appended to it)."""
+        own = self.sparse_kernel and self.splan.expand and not self.ahead and not self.pre_expanded
+        return bool(own or self.tail_next is not None)
 
     def run_sparse(self):
-        if self.ahead:
+        if self.tail_next is not None:
+            st = self.tail_fn(*self.tail_args)
+        elif self.pre_expanded:
+            st = nmspmm.lib().nm_spmm_ex(*self.pre_args)
+        elif self.ahead:
             side = Prepared.side_stream
             side.wait_event(self.ev_used)
             st = nmspmm.lib().nm_expand(*self.expand_args)
@@ -471,6 +523,15 @@ def prepare(cfg, torch):
     return work, preps
 
 
+def carry_expansions(preps):
+    """Tail mode over a sequence of GEMMs: every GEMM whose plan expands its
+    compact weight once per call, except the first of the sequence, has that
+    expansion carried by the launch of the GEMM before it."""
+    for prev, nxt in zip(preps, preps[1:]):
+        if nxt.sparse_kernel and nxt.splan.expand and prev.tail_next is None:
+            prev.carry_expansion_of(nxt)
+
+
 def secondary_workload(cfg, rounds, torch):
     """Speedup over the dense baseline per (token count, N:M) on another
     workload: ABBA rounds with an event after every GEMM; reported beside the
@@ -506,9 +567,11 @@ def main():
                          "real launches)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after timing, run one plain device copy of MIB MiB (profiler counter calibration)")
-    ap.add_argument("--expand-ahead", action="store_true",
-                    help="for plans that expand a compact weight once per call, run nm_expand on a second stream "
-                         "ahead of the GEMM instead of inside the sparse call (measured slower on ViT-L: the "
+    ap.add_argument("--expansion", choices=("tail", "call", "ahead"), default="tail",
+                    help="where a plan that expands a compact weight once per call gets that expansion: 'tail' "
+                         "(default) the previous GEMM's launch carries it (nm_spmm_out_expand) and the GEMM runs on "
+                         "the expanded weight; 'call' inside the sparse call (nm_spmm's own expansion launch); "
+                         "'ahead' nm_expand on a second stream with an event wait (measured slower on ViT-L: the "
                          "cross-stream waits cost more than the expansion latency they hide)")
     ap.add_argument("--traffic", type=str, default=None,
                     help="JSON record of measured HBM bytes per launch of the dominant kernel "
@@ -528,9 +591,11 @@ def main():
     torch.cuda.set_device(0)
 
     t0 = time.perf_counter()
-    if args.expand_ahead:
+    if args.expansion == "ahead":
         Prepared.side_stream = torch.cuda.Stream()   # default priority
     work, preps = prepare(args.config, torch)
+    if args.expansion == "tail":
+        carry_expansions(preps)
     out_i32, out_f16 = work.out_int32, work.out_f16
     log(f"workload {work.name}: {len(preps)} GEMMs, outputs {'int32' if out_i32 else ''}"
         f"{'+fp16' if out_f16 else ''}; inputs generated, packed and uploaded in {time.perf_counter() - t0:.1f} s")
@@ -667,8 +732,10 @@ def main():
         "frac_of_int8_peak": round(float(value / PEAK_INT8_TOPS), 4),
         "per_pattern": per_pattern,
         "cache_state": cache_state(preps),
-        "compact_weight_expansion": ("nm_expand on a second stream ahead of the GEMM, for plans with expand = 1"
-                                     if args.expand_ahead else "in the sparse call"),
+        "compact_weight_expansion": {
+            "tail": "carried by the previous GEMM's launch (nm_spmm_out_expand), for plans with expand = 1",
+            "call": "in the sparse call",
+            "ahead": "nm_expand on a second stream ahead of the GEMM, for plans with expand = 1"}[args.expansion],
         "roofline": roofline,
     }
     if not args.no_mfma_ceiling:

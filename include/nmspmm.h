@@ -313,6 +313,17 @@ nm_status nm_expand_size(const nm_desc *desc, nm_desc *expanded, size_t *bytes);
 nm_status nm_expand(const nm_desc *desc, const int8_t *vals, const uint8_t *meta, int8_t *out,
                     size_t out_bytes, void *stream);
 
+/* An expansion (nm_expand's work) that a GEMM launch carries along: the
+ * compact packed weight (desc, device vals and meta) and the device buffer
+ * out of out_bytes (>= nm_expand_size) it is expanded into. */
+typedef struct nm_expand_job {
+    const nm_desc *desc;
+    const int8_t *vals;
+    const uint8_t *meta;
+    int8_t *out;
+    size_t out_bytes;
+} nm_expand_job;
+
 /* ---------------------------------------------------------------- INT8 chaining
  * The paper deploys the linears in INT8 end to end (Sec. 6.3).  Between two
  * linears the int32 result must become the next linear's int8 input; the
@@ -368,6 +379,24 @@ nm_status nm_spmm_noalloc(const int8_t *X, int m, const int8_t *vals, const uint
 nm_status nm_gemm_i8_dense_out(const int8_t *X, int m, const int8_t *W, int n, int k,
                                const nm_outputs *out,
                                void *ws, size_t ws_bytes, void *stream, const nm_plan *plan);
+
+/* nm_spmm_out (or nm_gemm_i8_dense_out) that also runs `job` in the same
+ * kernel launch: workgroups appended after the GEMM's own expand the job's
+ * weight, one block per wave, so they are dispatched last and fill the
+ * compute units the GEMM's final round of workgroups leaves idle.  A caller
+ * that runs linears in sequence expands the next linear's weight this way and
+ * then runs that linear on the expanded form (nm_spmm_out with the descriptor
+ * nm_expand_size gives, vals = job->out, meta = job->out + its vals_bytes),
+ * with no launch of its own for the expansion.  job->out must not overlap any
+ * buffer of the GEMM; job == NULL is exactly nm_spmm_out.  With m == 0 the
+ * job is still run (alone).  Errors: as nm_spmm_out, plus those of nm_expand
+ * for the job (checked before anything is launched). */
+nm_status nm_spmm_out_expand(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
+                             const nm_desc *desc, const nm_outputs *out, void *ws, size_t ws_bytes,
+                             void *stream, const nm_plan *plan, const nm_expand_job *job);
+nm_status nm_gemm_i8_dense_out_expand(const int8_t *X, int m, const int8_t *W, int n, int k,
+                                      const nm_outputs *out, void *ws, size_t ws_bytes, void *stream,
+                                      const nm_plan *plan, const nm_expand_job *job);
 
 /* Quantisation of binary16 activations: xq[c] = q8(fp32(x[c]) * inv_scale)
  * for 0 <= c < count (a per-tensor scale s_x gives inv_scale = 1 / s_x).

@@ -50,11 +50,32 @@ int group_rows_for(int tiles_m) { return tiles_m >= 2 * kGroupRows ? kGroupRows 
 
 namespace nmspmm {
 
+// Checks an expansion job before anything is launched.
+static nm_status check_job(const nm_expand_job *job) {
+    nm_desc e;
+    size_t need = 0;
+    nm_status st = nm_expand_size(job->desc, &e, &need);
+    if (st != NM_OK) return st;
+    if (!job->vals || !job->meta || !job->out || !aligned16(job->vals) || !aligned16(job->meta) ||
+        !aligned16(job->out))
+        return NM_ERR_ARG;
+    return job->out_bytes < need ? NM_ERR_WORKSPACE : NM_OK;
+}
+
 nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint8_t *meta, int n, int k,
                    int k_steps, int n_frags, const nm_outputs *out, void *ws, size_t ws_bytes, void *stream,
-                   const nm_plan *forced, WorkspaceFn ws_fn) {
+                   const nm_plan *forced, WorkspaceFn ws_fn, const nm_expand_job *job) {
     if (m < 0) return NM_ERR_SHAPE;
-    if (m == 0) return NM_OK;  // nothing to compute; empty tensors may carry null pointers
+    if (job) {
+        nm_status st = check_job(job);
+        if (st != NM_OK) return st;
+    }
+    if (m == 0) {
+        // nothing to compute (empty tensors may carry null pointers); a job still runs
+        if (!job) return NM_OK;
+        const nm_desc *d = job->desc;
+        return launch_expand(kind_of(d), job->vals, job->meta, d->n, d->k, job->out, stream) == 0 ? NM_OK : NM_ERR_HIP;
+    }
     if (!out) return NM_ERR_ARG;
     const nm_outputs o = *out;
     if (!X || !A || (kind != NM_KIND_DENSE && !meta)) return NM_ERR_ARG;
@@ -115,7 +136,26 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
     a.tiles_m = (m + plan.tile_m - 1) / plan.tile_m;
     a.split_k = plan.split_k;
     a.group_rows = group_rows_for(a.tiles_m);
-    int err = launch_gemm(run_kind, plan.tile, a, plan.grid, stream);
+    a.gemm_grid = plan.grid;
+    int grid = plan.grid;
+    if (job) {
+        // the job's blocks go to workgroups appended after the GEMM's, one per wave
+        const nm_desc *d = job->desc;
+        const int per = tile_waves(kTiles[plan.tile]);
+        const int64_t blocks = (int64_t)d->n_frags * d->k_steps;
+        const int64_t extra = (blocks + per - 1) / per;
+        if ((int64_t)grid + extra > 0x7fffffff) return NM_ERR_SHAPE;
+        a.x_kind = kind_of(d);
+        a.x_vals = job->vals;
+        a.x_meta = job->meta;
+        a.x_out = job->out;
+        a.x_n = d->n;
+        a.x_k = d->k;
+        a.x_blocks = (int)blocks;
+        a.x_k_steps = d->k_steps;
+        grid += (int)extra;
+    }
+    int err = launch_gemm(run_kind, plan.tile, a, grid, stream);
     return err == 0 ? NM_OK : NM_ERR_HIP;
 }
 
@@ -210,6 +250,15 @@ extern "C" nm_status nm_spmm_out(const int8_t *X, int m, const int8_t *vals, con
                     ws_bytes, stream, plan, nullptr);
 }
 
+extern "C" nm_status nm_spmm_out_expand(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
+                                        const nm_desc *desc, const nm_outputs *out, void *ws, size_t ws_bytes,
+                                        void *stream, const nm_plan *plan, const nm_expand_job *job) {
+    nm_status st = check_desc(desc);
+    if (st != NM_OK) return st;
+    return run_gemm(kind_of(desc), X, m, vals, meta, desc->n, desc->k, desc->k_steps, desc->n_frags, out, ws,
+                    ws_bytes, stream, plan, nullptr, job);
+}
+
 extern "C" nm_status nm_spmm_ex(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
                                 const nm_desc *desc, int32_t *Y, const float *scale, uint16_t *Yh,
                                 void *ws, size_t ws_bytes, void *stream, const nm_plan *plan) {
@@ -231,6 +280,16 @@ extern "C" nm_status nm_gemm_i8_dense_out(const int8_t *X, int m, const int8_t *
     const int k_steps = (k + kKStep - 1) / kKStep;
     return run_gemm(NM_KIND_DENSE, X, m, W, nullptr, n, k, k_steps, (n + kFragRows - 1) / kFragRows, out, ws,
                     ws_bytes, stream, plan, nullptr);
+}
+
+extern "C" nm_status nm_gemm_i8_dense_out_expand(const int8_t *X, int m, const int8_t *W, int n, int k,
+                                                 const nm_outputs *out, void *ws, size_t ws_bytes, void *stream,
+                                                 const nm_plan *plan, const nm_expand_job *job) {
+    if (n < 1 || k < 1) return NM_ERR_ARG;
+    if (k % 16 != 0 || n % 4 != 0) return NM_ERR_SHAPE;
+    const int k_steps = (k + kKStep - 1) / kKStep;
+    return run_gemm(NM_KIND_DENSE, X, m, W, nullptr, n, k, k_steps, (n + kFragRows - 1) / kFragRows, out, ws,
+                    ws_bytes, stream, plan, nullptr, job);
 }
 
 extern "C" nm_status nm_gemm_i8_dense_ex(const int8_t *X, int m, const int8_t *W, int n, int k,

@@ -87,6 +87,15 @@ struct GemmArgs {
     int k_steps, n_frags;
     int tiles_n, tiles_m, split_k;
     int group_rows;         // tile order: 0 row by row, else groups of this many tile rows
+    // Workgroups gemm_grid .. gridDim.x - 1 of the launch do not belong to the
+    // GEMM: they expand another compact weight (x_kind, blocks as in the
+    // packed layout) into x_out, one block per wave (nm_spmm_out_expand).
+    int gemm_grid = 0x7fffffff;
+    int x_kind = 0;
+    const int8_t *x_vals = nullptr;
+    const uint8_t *x_meta = nullptr;
+    int8_t *x_out = nullptr;
+    int x_n = 0, x_k = 0, x_blocks = 0, x_k_steps = 0;
 };
 
 // Workspace of a plan: with split_k > 1 a fixed block of per-tile arrival
@@ -110,6 +119,9 @@ constexpr bool kind_is_compact(int kind) { return kind != NM_KIND_SP42 && kind !
 constexpr int expanded_kind(int kind) { return kind_is_sp42(kind) ? NM_KIND_SP42 : NM_KIND_DENSE; }
 int64_t expanded_bytes(int kind, int n, int k);
 int launch_expand(int kind, const int8_t *vals, const uint8_t *meta, int n, int k, int8_t *out, void *stream);
+// Waves per workgroup of a tile's kernel (each tail workgroup of a launch
+// that carries an expansion expands one block per wave).
+constexpr int tile_waves(const TileCfg &t) { return t.layout == kKSliced ? kThreads / 64 : t.wn * t.wm; }
 
 int device_cu_count();     // cached per device; 256 when no device is visible
 
@@ -124,7 +136,7 @@ int launch_quantize_f16(const uint16_t *x, int64_t count, float inv_scale, int8_
 typedef nm_status (*WorkspaceFn)(size_t need, void *stream, void **ws, size_t *ws_bytes);
 nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint8_t *meta, int n, int k,
                    int k_steps, int n_frags, const nm_outputs *out, void *ws, size_t ws_bytes, void *stream,
-                   const nm_plan *forced, WorkspaceFn ws_fn);
+                   const nm_plan *forced, WorkspaceFn ws_fn, const nm_expand_job *job = nullptr);
 nm_status check_desc(const nm_desc *d);
 int kind_of(const nm_desc *d);
 

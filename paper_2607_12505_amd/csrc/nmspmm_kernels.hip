@@ -473,6 +473,46 @@ __device__ __forceinline__ void expand_to_lds(const WRegs<KIND> &r, const uint2 
     }
 }
 
+// A workgroup past the GEMM's own (blockIdx.x >= gemm_grid) expands blocks
+// of another compact weight, one per wave, with its lookup table in the
+// GEMM's LDS (at least 2 KB): so a launch can carry the expansion a later
+// GEMM needs without a launch of its own.
+template <int KIND>
+__device__ __forceinline__ void expand_block(const int8_t *__restrict__ vals, const uint8_t *__restrict__ meta, int n,
+                                             int k, int blocks, int k_steps, int8_t *out, int b, int lane, uint2 *lut,
+                                             int tid, int nthreads);
+
+__device__ inline void expand_tail(const GemmArgs &a, uint2 *lut) {
+    const int tid = threadIdx.x, nthreads = blockDim.x;
+    const int b = ((int)blockIdx.x - a.gemm_grid) * (nthreads >> 6) + (tid >> 6), lane = tid & 63;
+    switch (a.x_kind) {
+        case NM_KIND_C14:
+            expand_block<NM_KIND_C14>(a.x_vals, a.x_meta, a.x_n, a.x_k, a.x_blocks, a.x_k_steps, a.x_out, b, lane, lut,
+                                      tid, nthreads);
+            break;
+        case NM_KIND_C18:
+            expand_block<NM_KIND_C18>(a.x_vals, a.x_meta, a.x_n, a.x_k, a.x_blocks, a.x_k_steps, a.x_out, b, lane, lut,
+                                      tid, nthreads);
+            break;
+        case NM_KIND_C28:
+            expand_block<NM_KIND_C28>(a.x_vals, a.x_meta, a.x_n, a.x_k, a.x_blocks, a.x_k_steps, a.x_out, b, lane, lut,
+                                      tid, nthreads);
+            break;
+        case NM_KIND_MK3:
+            expand_block<NM_KIND_MK3>(a.x_vals, a.x_meta, a.x_n, a.x_k, a.x_blocks, a.x_k_steps, a.x_out, b, lane, lut,
+                                      tid, nthreads);
+            break;
+        case NM_KIND_MK4:
+            expand_block<NM_KIND_MK4>(a.x_vals, a.x_meta, a.x_n, a.x_k, a.x_blocks, a.x_k_steps, a.x_out, b, lane, lut,
+                                      tid, nthreads);
+            break;
+        case NM_KIND_MK5:
+            expand_block<NM_KIND_MK5>(a.x_vals, a.x_meta, a.x_n, a.x_k, a.x_blocks, a.x_k_steps, a.x_out, b, lane, lut,
+                                      tid, nthreads);
+            break;
+    }
+}
+
 template <int KIND, int WN_, int WM_, int FN_, int FM_, int NST>
 struct Geometry {
     using K = Kind<KIND>;
@@ -727,8 +767,13 @@ __global__ __launch_bounds__(64 * WN * WM) void k_gemm(GemmArgs a) {
     __shared__ uint2 lut[K::LUT];
     __shared__ int s_last;
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
+    static_assert(G::LDSB >= 256 * 8, "room for the expansion table of a tail workgroup");
+    if ((int)blockIdx.x >= a.gemm_grid) {
+        expand_tail(a, (uint2 *)lds);
+        return;
+    }
 
-    const int lid = map_block(blockIdx.x, gridDim.x);
+    const int lid = map_block(blockIdx.x, (int)gridDim.x < a.gemm_grid ? (int)gridDim.x : a.gemm_grid);
     int tn, rest;
     tile_order(lid, a.tiles_n, a.tiles_m * a.split_k, a.group_rows, &tn, &rest);
     const int split = rest % a.split_k;
@@ -855,8 +900,13 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
     __shared__ uint2 lut[K::LUT];
     __shared__ int s_last;
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t *)lds;
+    static_assert(G::LDSB >= 256 * 8, "room for the expansion table of a tail workgroup");
+    if ((int)blockIdx.x >= a.gemm_grid) {
+        expand_tail(a, (uint2 *)lds);
+        return;
+    }
 
-    const int lid = map_block(blockIdx.x, gridDim.x);
+    const int lid = map_block(blockIdx.x, (int)gridDim.x < a.gemm_grid ? (int)gridDim.x : a.gemm_grid);
     const int tn = lid % a.tiles_n;
     const int rest = lid / a.tiles_n;
     const int split = rest % a.split_k;
@@ -1106,18 +1156,19 @@ __global__ __launch_bounds__(256) void k_gemm_ks(GemmArgs a) {
 // (C14, C18, C28) or as dense W [n x k] row-major (mask layouts; rows >= n and
 // columns >= k of the padded blocks are not written).  4 blocks per
 // workgroup; blocks = n_frags * k_steps.
+// One wave expands block b of a compact weight (1:4, 1:8, 2:8 to the 4:2
+// operand; 3:8-5:8 to dense rows of W) into out.  The workgroup's lookup
+// table is built while the block's bytes are in flight; every wave of the
+// workgroup must call this (it holds a barrier), waves past the last block
+// load a valid block and store nothing.
 template <int KIND>
-__global__ __launch_bounds__(256) void k_expand(const int8_t *__restrict__ vals, const uint8_t *__restrict__ meta,
-                                               int n, int k, int blocks, int k_steps, int8_t *out) {
-    __shared__ uint2 lut[Kind<KIND>::LUT];
-    const int b = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-    // the block's compact bytes are requested first, so the table is built
-    // while they are in flight (waves past the last block load nothing but
-    // still help build the table)
+__device__ __forceinline__ void expand_block(const int8_t *__restrict__ vals, const uint8_t *__restrict__ meta, int n,
+                                             int k, int blocks, int k_steps, int8_t *out, int b, int lane, uint2 *lut,
+                                             int tid, int nthreads) {
     WRegs<KIND> r;
     const int64_t o = (int64_t)(b < blocks ? b : blocks - 1) * 64 + lane;
     wload<KIND>(r, vals + o * Kind<KIND>::VB, meta + o * Kind<KIND>::MB);
-    fill_lut<KIND>(lut, threadIdx.x, 256);
+    fill_lut<KIND>(lut, tid, nthreads);
     __syncthreads();
     if (b >= blocks) return;
     if constexpr (Kind<KIND>::kSp) {
@@ -1138,6 +1189,14 @@ __global__ __launch_bounds__(256) void k_expand(const int8_t *__restrict__ vals,
             if (col + 16 < k) *(v4i *)(dst + 16) = c1;
         }
     }
+}
+
+template <int KIND>
+__global__ __launch_bounds__(256) void k_expand(const int8_t *__restrict__ vals, const uint8_t *__restrict__ meta,
+                                               int n, int k, int blocks, int k_steps, int8_t *out) {
+    __shared__ uint2 lut[Kind<KIND>::LUT];
+    expand_block<KIND>(vals, meta, n, k, blocks, k_steps, out, blockIdx.x * 4 + (threadIdx.x >> 6), threadIdx.x & 63,
+                       lut, threadIdx.x, 256);
 }
 
 __global__ void k_zero(int *p, size_t n4, unsigned char *tail, int tail_bytes) {

@@ -33,7 +33,8 @@ EXPORTED = (
     "nm_status_string", "nm_compress_size", "nm_compress", "nm_decompress", "nm_num_tiles",
     "nm_tile_info", "nm_plan_kernel_name", "nm_spmm_plan", "nm_spmm_plan_complete", "nm_gemm_i8_dense_plan", "nm_workspace_size", "nm_workspace_init",
     "nm_spmm", "nm_spmm_ex", "nm_gemm_i8_dense", "nm_gemm_i8_dense_ex", "nm_spmm_out", "nm_gemm_i8_dense_out",
-    "nm_quantize_f16", "nm_spmm_noalloc", "nm_expand_size", "nm_expand",
+    "nm_quantize_f16", "nm_spmm_noalloc", "nm_expand_size", "nm_expand", "nm_spmm_out_expand",
+    "nm_gemm_i8_dense_out_expand",
 )
 NM_NOALLOC_SCRATCH_BYTES = 16384 + (32 << 20)
 
@@ -57,6 +58,11 @@ class NmPlan(ctypes.Structure):
 class NmOutputs(ctypes.Structure):
     _fields_ = [("y", ctypes.c_void_p), ("yh", ctypes.c_void_p), ("scale", ctypes.c_void_p),
                 ("yq", ctypes.c_void_p), ("qscale", ctypes.c_void_p)]
+
+
+class NmExpandJob(ctypes.Structure):
+    _fields_ = [("desc", ctypes.POINTER(NmDesc)), ("vals", ctypes.c_void_p), ("meta", ctypes.c_void_p),
+                ("out", ctypes.c_void_p), ("out_bytes", ctypes.c_size_t)]
 
 
 class NmError(RuntimeError):
@@ -113,6 +119,10 @@ def lib() -> ctypes.CDLL:
             "nm_spmm_noalloc": ([vp, i32, vp, vp, pd, ctypes.POINTER(NmOutputs), vp, pp], i32),
             "nm_expand_size": ([pd, pd, ctypes.POINTER(sz)], i32),
             "nm_expand": ([pd, vp, vp, vp, sz, vp], i32),
+            "nm_spmm_out_expand": ([vp, i32, vp, vp, pd, ctypes.POINTER(NmOutputs), vp, sz, vp, pp,
+                                    ctypes.POINTER(NmExpandJob)], i32),
+            "nm_gemm_i8_dense_out_expand": ([vp, i32, vp, i32, i32, ctypes.POINTER(NmOutputs), vp, sz, vp, pp,
+                                             ctypes.POINTER(NmExpandJob)], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -385,11 +395,11 @@ def _out_mode(Y, Yh, Yq) -> int:
 
 
 def spmm(X, w: DeviceWeight, Y=None, scale=None, Yh=None, plan: Optional[NmPlan] = None, ws=None,
-         stream=None, Yq=None, qscale=None):
+         stream=None, Yq=None, qscale=None, job: Optional[NmExpandJob] = None):
     """Sparse GEMM on torch device tensors.  Y (int32), Yh (float16, or int16
     view of binary16) and Yq (int8) are written in place; returns (Y, Yh), or
     (Y, Yh, Yq) when Yq is given.  Without Yq this calls nm_spmm_ex, with it
-    nm_spmm_out."""
+    nm_spmm_out; with an expansion job (expand_job()) nm_spmm_out_expand."""
     torch = _torch()
     d = w.desc
     if X.dim() != 2:
@@ -410,6 +420,12 @@ def spmm(X, w: DeviceWeight, Y=None, scale=None, Yh=None, plan: Optional[NmPlan]
     else:
         ws_bytes = ws.numel() * ws.element_size()
     pl = ctypes.byref(plan) if plan is not None else None
+    if job is not None:
+        o = _outputs(Y, scale, Yh, Yq, qscale)
+        st = lib().nm_spmm_out_expand(_ptr(X), m, _ptr(w.vals), _ptr(w.meta), ctypes.byref(w.desc), ctypes.byref(o),
+                                      _ptr(ws), ws_bytes, _stream(stream), pl, ctypes.byref(job))
+        _check(st, "nm_spmm_out_expand")
+        return (Y, Yh) if Yq is None and qscale is None else (Y, Yh, Yq)
     if Yq is None and qscale is None:
         st = lib().nm_spmm_ex(_ptr(X), m, _ptr(w.vals), _ptr(w.meta), ctypes.byref(w.desc), _ptr(Y), _ptr(scale),
                               _ptr(Yh), _ptr(ws), ws_bytes, _stream(stream), pl)
@@ -445,8 +461,9 @@ def spmm_noalloc(X, w: DeviceWeight, Y=None, scale=None, Yh=None, Yq=None, qscal
 
 
 def gemm_i8_dense(X, W, Y=None, scale=None, Yh=None, plan: Optional[NmPlan] = None, ws=None, stream=None,
-                  Yq=None, qscale=None):
-    """Dense baseline GEMM (nm_gemm_i8_dense_ex, or nm_gemm_i8_dense_out when Yq is given)."""
+                  Yq=None, qscale=None, job: Optional[NmExpandJob] = None):
+    """Dense baseline GEMM (nm_gemm_i8_dense_ex, or nm_gemm_i8_dense_out when Yq is given, or
+    nm_gemm_i8_dense_out_expand with an expansion job)."""
     torch = _torch()
     if X.dim() != 2 or W.dim() != 2:
         raise ValueError("X and W must be 2-D ([m x k] and [n x k])")
@@ -466,6 +483,12 @@ def gemm_i8_dense(X, W, Y=None, scale=None, Yh=None, plan: Optional[NmPlan] = No
     else:
         ws_bytes = ws.numel() * ws.element_size()
     pl = ctypes.byref(plan) if plan is not None else None
+    if job is not None:
+        o = _outputs(Y, scale, Yh, Yq, qscale)
+        st = lib().nm_gemm_i8_dense_out_expand(_ptr(X), m, _ptr(W), n, k, ctypes.byref(o), _ptr(ws), ws_bytes,
+                                               _stream(stream), pl, ctypes.byref(job))
+        _check(st, "nm_gemm_i8_dense_out_expand")
+        return (Y, Yh) if Yq is None and qscale is None else (Y, Yh, Yq)
     if Yq is None and qscale is None:
         st = lib().nm_gemm_i8_dense_ex(_ptr(X), m, _ptr(W), n, k, _ptr(Y), _ptr(scale), _ptr(Yh), _ptr(ws),
                                        ws_bytes, _stream(stream), pl)
@@ -504,8 +527,31 @@ def expand(w: DeviceWeight, out=None, stream=None) -> DeviceWeight:
     _on_device((("w.vals", w.vals), ("w.meta", w.meta), ("out", out)))
     _check(lib().nm_expand(ctypes.byref(d), _ptr(w.vals), _ptr(w.meta), _ptr(out), out.numel(), _stream(stream)),
            "nm_expand")
+    return _expanded_view(out, e)
+
+
+def _expanded_view(out, e):
+    torch = _torch()
     b = out.view(torch.uint8)
     return DeviceWeight(b[:e.vals_bytes].view(torch.int8), b[e.vals_bytes:e.vals_bytes + e.meta_bytes], e)
+
+
+def expand_job(w: DeviceWeight, out):
+    """An nm_expand_job for a GEMM launch to carry: w expanded into out (a
+    uint8 or int8 device buffer of at least expand_size() bytes).  Returns
+    (job, expanded DeviceWeight viewing out); keep both alive until the launch
+    has run."""
+    torch = _torch()
+    d = w.desc
+    e, nbytes = expand_size(d)
+    _need(w.vals, "w.vals", (torch.int8,), numel=d.vals_bytes)
+    _need(w.meta, "w.meta", (torch.uint8,), numel=d.meta_bytes)
+    _need(out, "out", (torch.uint8, torch.int8), numel=nbytes)
+    if out.dim() != 1:
+        raise ValueError("out: must be 1-D")
+    _on_device((("w.vals", w.vals), ("w.meta", w.meta), ("out", out)))
+    job = NmExpandJob(ctypes.pointer(d), _ptr(w.vals), _ptr(w.meta), _ptr(out), out.numel())
+    return job, _expanded_view(out, e)
 
 
 def quantize_f16(x, inv_scale: float, xq=None, stream=None):

@@ -116,6 +116,16 @@ def test_host_side_argument_checks_need_no_gpu():
     assert L.nm_expand(ctypes.byref(c28), fake, fake, fake, 64 * 1280 // 16 - 1, nul) == nmspmm.NM_ERR_WORKSPACE
     assert L.nm_expand(ctypes.byref(c28), fake, fake, misaligned, 1 << 20, nul) == nmspmm.NM_ERR_ARG
     assert L.nm_expand(ctypes.byref(c28), fake, nul, fake, 1 << 20, nul) == nmspmm.NM_ERR_ARG
+    # a GEMM launch carrying an expansion: the job is checked before anything is launched
+    y_out = nmspmm.NmOutputs(fake.value, None, None, None, None)
+    job = nmspmm.NmExpandJob(ctypes.pointer(d), fake.value, fake.value, fake.value, 1 << 20)   # d is 2:4: stored form
+    assert L.nm_spmm_out_expand(fake, 64, fake, fake, ctypes.byref(d), ctypes.byref(y_out), nul, 0, nul, None,
+                                ctypes.byref(job)) == nmspmm.NM_ERR_ARG
+    small = nmspmm.NmExpandJob(ctypes.pointer(c28), fake.value, fake.value, fake.value, 64)
+    assert L.nm_gemm_i8_dense_out_expand(fake, 64, fake, 64, 128, ctypes.byref(y_out), nul, 0, nul, None,
+                                         ctypes.byref(small)) == nmspmm.NM_ERR_WORKSPACE
+    assert L.nm_gemm_i8_dense_out_expand(fake, -1, fake, 64, 128, ctypes.byref(y_out), nul, 0, nul, None,
+                                         ctypes.byref(small)) == nmspmm.NM_ERR_SHAPE
     assert L.nm_quantize_f16(fake, -1, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_SHAPE
     assert L.nm_quantize_f16(misaligned, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_ARG
     P = nmprobe.lib()
@@ -168,6 +178,12 @@ def test_launch_failures_report_nm_err_hip():
     assert L.nm_workspace_init(fake, 64, nul) == nmspmm.NM_ERR_HIP
     c14 = nmspmm.compress_size(64, 128, 1, 4)
     assert L.nm_expand(ctypes.byref(c14), fake, fake, fake, 1 << 20, nul) == nmspmm.NM_ERR_HIP
+    y_out = nmspmm.NmOutputs(fake.value, None, None, None, None)
+    job = nmspmm.NmExpandJob(ctypes.pointer(c14), fake.value, fake.value, fake.value, 1 << 20)
+    assert L.nm_spmm_out_expand(fake, 64, fake, fake, ctypes.byref(d), ctypes.byref(y_out), nul, 0, nul, None,
+                                ctypes.byref(job)) == nmspmm.NM_ERR_HIP
+    assert L.nm_gemm_i8_dense_out_expand(fake, 0, fake, 64, 128, ctypes.byref(y_out), nul, 0, nul, None,
+                                         ctypes.byref(job)) == nmspmm.NM_ERR_HIP     # m == 0: the job alone
     P = nmprobe.lib()
     assert P.nm_probe_mfma_rate(nmspmm.NM_KIND_SP42, fake, 1, 1, fake, nul, nul) == nmspmm.NM_ERR_HIP
     khz = ctypes.c_int32(0)

@@ -42,17 +42,32 @@ def test_bench_config_line(cfg, capsys, monkeypatch):
 
 def test_bench_expand_ahead_matches_oracle_rows(capsys, monkeypatch):
     # DeiT-B (batch 1, 8 and 128) has GEMMs whose plans expand the compact
-    # weight once per call; with --expand-ahead those run nm_expand on a second
+    # weight once per call; with --expansion ahead those run nm_expand on a second
     # stream and the GEMM on the expanded weight.  The CPU baseline compares
     # the sampled rows of every GEMM with the oracle.
     import bench
     monkeypatch.setattr(sys, "argv", ["bench.py", "--config", "2", "--steps", "1", "--warmup", "1", "--rounds", "2",
-                                      "--cpu-budget", "2", "--no-secondary", "--no-mfma-ceiling", "--expand-ahead"])
+                                      "--cpu-budget", "2", "--no-secondary", "--no-mfma-ceiling", "--expansion", "ahead"])
     try:
         bench.main()
     finally:
         bench.Prepared.side_stream = None
     line = json.loads(capsys.readouterr().out.strip().splitlines()[-1])
     assert line["compact_weight_expansion"].startswith("nm_expand")
+    assert line["parity_sampled_rows_mismatches"] == 0
+    assert line["value"] > 0
+
+
+def test_bench_expand_in_tail_matches_oracle_rows(capsys, monkeypatch):
+    # ViT-L chain: every GEMM whose plan expands its weight once per call has
+    # that expansion carried by the previous GEMM's launch; the CPU baseline
+    # compares the sampled rows of every GEMM with the oracle.
+    import bench
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--config", "4", "--steps", "1", "--warmup", "1", "--rounds", "2",
+                                      "--cpu-budget", "2", "--no-secondary", "--no-mfma-ceiling", "--no-store-only",
+                                      "--expansion", "tail"])
+    bench.main()
+    line = json.loads(capsys.readouterr().out.strip().splitlines()[-1])
+    assert line["compact_weight_expansion"].startswith("carried")
     assert line["parity_sampled_rows_mismatches"] == 0
     assert line["value"] > 0

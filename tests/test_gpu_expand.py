@@ -1,8 +1,9 @@
 """nm_expand (the decode of a compact weight as a pass of its own, Sec. 4.2)
-through the C ABI: the expanded buffer, read by the header's formulas, holds
-exactly the weight that was packed; the GEMM on the expanded descriptor gives
-the oracle's product bit for bit; nothing is written past the buffer, and an
-undersized buffer is rejected before anything is written."""
+through the C ABI, alone and carried by a GEMM launch: the expanded buffer,
+read by the header's formulas, holds exactly the weight that was packed; the
+GEMM on the expanded descriptor gives the oracle's product bit for bit;
+nothing is written past the buffer, and an undersized buffer is rejected
+before anything is written."""
 import numpy as np
 import pytest
 
@@ -112,3 +113,120 @@ def test_stored_layouts_are_rejected():
         packed = nmspmm.compress(wl.random_nm(32, 128, N, M, rng), N, M)
         with pytest.raises(nmspmm.NmError):
             nmspmm.expand(nmspmm.DeviceWeight.from_packed(packed))
+
+
+# ---------------------------------------------------------------------------
+# GEMM launches that carry an expansion (nm_spmm_out_expand,
+# nm_gemm_i8_dense_out_expand): the GEMM's outputs are the oracle's product,
+# the carried expansion is byte-identical to nm_expand's, nothing is written
+# past either, for GEMMs on every kernel layout (output-split on 4 and 8
+# waves, k-sliced, split-K, a GEMM that expands its own weight first).
+
+GEMMS = (
+    # (m, n, k, N, M, tile or None (planner), split)
+    (333, 200, 1040, 2, 4, None, 1),
+    (333, 200, 1040, 2, 8, 0, 1),        # compact weight, expanded inside the workgroups
+    (333, 200, 1040, 1, 8, 6, 1),        # 8 waves
+    (333, 200, 1040, 2, 4, 3, 2),        # split-K
+    (100, 256, 256, 2, 4, None, 1),      # k-sliced
+    (333, 200, 1040, 4, 8, 0, 1),        # mask layout: the dense kernel
+    (2000, 512, 512, 8, 8, None, 1),     # dense weight
+)
+
+
+def _carry(m, n, k, N, M, tile, split, expand_self, job_N, job_M, seed):
+    import torch
+    rng = np.random.default_rng(seed)
+    X = rng.integers(-128, 128, (m, k), dtype=np.int64).astype(np.int8)
+    W = wl.random_nm(n, k, N, M, rng, full=True)
+    ref = oracle.matmul_i8(X, W)
+    Wj = wl.random_nm(96, 1024, job_N, job_M, rng, full=True)
+    pj = nmspmm.compress(Wj, job_N, job_M)
+    dj = nmspmm.DeviceWeight.from_packed(pj)
+    e, nbytes = nmspmm.expand_size(pj.desc)
+    want = torch.full((nbytes,), SENTINEL, dtype=torch.uint8, device="cuda")
+    nmspmm.expand(dj, out=want)
+    out = torch.full((nbytes + GUARD,), SENTINEL, dtype=torch.uint8, device="cuda")
+    job, ew = nmspmm.expand_job(dj, out)
+    Xd = torch.from_numpy(X).cuda()
+    Y = torch.full((m, n), -7, dtype=torch.int32, device="cuda")
+    dense = N == M
+    if dense:
+        plan = None if tile is None else nmspmm.make_plan(nmspmm.NM_KIND_DENSE, tile, split)
+        nmspmm.gemm_i8_dense(Xd, torch.from_numpy(W).cuda(), Y=Y, plan=plan, job=job)
+    else:
+        p = nmspmm.compress(W, N, M)
+        plan = None if tile is None else nmspmm.make_plan(p.desc.kind, tile, split, expand_self)
+        nmspmm.spmm(Xd, nmspmm.DeviceWeight.from_packed(p), Y=Y, plan=plan, job=job)
+    torch.cuda.synchronize()
+    assert np.array_equal(Y.cpu().numpy(), ref)
+    h = out.cpu().numpy()
+    assert (h[nbytes:] == SENTINEL).all(), "write past the carried expansion"
+    assert np.array_equal(h[:nbytes], want.cpu().numpy())
+    return ew, Wj
+
+
+@pytest.mark.parametrize("job_N,job_M", COMPACT)
+@pytest.mark.parametrize("gemm", GEMMS)
+def test_gemm_carries_an_expansion(gemm, job_N, job_M):
+    m, n, k, N, M, tile, split = gemm
+    _carry(m, n, k, N, M, tile, split, 0, job_N, job_M, seed=10 * GEMMS.index(gemm) + COMPACT.index((job_N, job_M)))
+
+
+def test_gemm_that_expands_its_own_weight_carries_another():
+    # the call launches the expansion of its own weight, then the GEMM with the carried one
+    ew, Wj = _carry(2000, 256, 1024, 2, 8, 0, 1, 1, 4, 8, seed=3)
+    # and the carried expansion is usable as a weight of its own
+    import torch
+    rng = np.random.default_rng(4)
+    X = rng.integers(-128, 128, (150, 1024), dtype=np.int64).astype(np.int8)
+    Y = torch.full((150, 96), -7, dtype=torch.int32, device="cuda")
+    nmspmm.spmm(torch.from_numpy(X).cuda(), ew, Y=Y)
+    torch.cuda.synchronize()
+    assert np.array_equal(Y.cpu().numpy(), oracle.matmul_i8(X, Wj))
+
+
+def test_no_tokens_still_runs_the_job():
+    import torch
+    rng = np.random.default_rng(8)
+    Wj = wl.random_nm(64, 256, 1, 4, rng, full=True)
+    pj = nmspmm.compress(Wj, 1, 4)
+    dj = nmspmm.DeviceWeight.from_packed(pj)
+    _, nbytes = nmspmm.expand_size(pj.desc)
+    want = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    nmspmm.expand(dj, out=want)
+    out = torch.full((nbytes,), SENTINEL, dtype=torch.uint8, device="cuda")
+    job, _ = nmspmm.expand_job(dj, out)
+    X = torch.empty((0, 128), dtype=torch.int8, device="cuda")
+    W = torch.zeros((64, 128), dtype=torch.int8, device="cuda")
+    nmspmm.gemm_i8_dense(X, W, Y=torch.empty((0, 64), dtype=torch.int32, device="cuda"), job=job)
+    torch.cuda.synchronize()
+    assert torch.equal(out, want)
+
+
+def test_bad_job_launches_nothing():
+    import ctypes
+    import torch
+    rng = np.random.default_rng(9)
+    W = wl.random_nm(64, 256, 2, 4, rng, full=True)
+    p = nmspmm.compress(W, 2, 4)
+    dw = nmspmm.DeviceWeight.from_packed(p)
+    Wj = wl.random_nm(64, 256, 2, 8, rng, full=True)
+    pj = nmspmm.compress(Wj, 2, 8)
+    dj = nmspmm.DeviceWeight.from_packed(pj)
+    _, nbytes = nmspmm.expand_size(pj.desc)
+    out = torch.full((nbytes,), SENTINEL, dtype=torch.uint8, device="cuda")
+    X = torch.ones((100, 256), dtype=torch.int8, device="cuda")
+    Y = torch.full((100, 64), -7, dtype=torch.int32, device="cuda")
+    small = nmspmm.NmExpandJob(ctypes.pointer(pj.desc), dj.vals.data_ptr(), dj.meta.data_ptr(), out.data_ptr(),
+                               nbytes - 16)
+    with pytest.raises(nmspmm.NmError) as e:
+        nmspmm.spmm(X, dw, Y=Y, job=small)
+    assert e.value.status == nmspmm.NM_ERR_WORKSPACE
+    stored = nmspmm.NmExpandJob(ctypes.pointer(p.desc), dw.vals.data_ptr(), dw.meta.data_ptr(), out.data_ptr(),
+                                nbytes)
+    with pytest.raises(nmspmm.NmError) as e:
+        nmspmm.spmm(X, dw, Y=Y, job=stored)
+    assert e.value.status == nmspmm.NM_ERR_ARG
+    torch.cuda.synchronize()
+    assert (Y == -7).all().item() and (out == SENTINEL).all().item()
