@@ -900,7 +900,8 @@ def pmc_stall_table(dirs, cfg, commands, out_md):
         if not cols or not all(c[1] in cs and c[2] in cs for c in cols[:1]):
             continue
         gemms = labels.get(key)
-        what = ", ".join(sorted({f"{g[0]} {g[4]}" for g in gemms})) if gemms else "other"
+        what = (", ".join(sorted({f"{g[0]} {g[4]}" for g in gemms})) if gemms else
+                "a launch with workgroups beyond the planned grid (a GEMM carrying an expansion)")
         if gemms and len({g[1:4] for g in gemms}) == 1:
             _, m, k, n, _ = sorted(gemms)[0]
             what += f" (m {m}, k {k}, n {n})"
