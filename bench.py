@@ -29,6 +29,7 @@ Prints one JSON line on stdout; human-readable tables go to stderr.
 from __future__ import annotations
 
 import argparse
+import gc
 import ctypes
 import json
 import os
@@ -436,10 +437,29 @@ def hold_side_stream(torch):
         Prepared.side_stream.wait_event(ev)
 
 
+class _NoGC:
+    """Python's garbage collector paused while the host queues timed work: a
+    collection pause longer than the device sleep that gives the host its head
+    start would otherwise land inside an event interval."""
+
+    def __enter__(self):
+        self.was = gc.isenabled()
+        gc.disable()
+
+    def __exit__(self, *exc):
+        if self.was:
+            gc.enable()
+
+
 def timed_steps(preps, steps, torch):
     """The contract's timed region: `steps` steps of the sparse leg back to
     back between two synchronisations.  Returns (wall ms per step, event ms of
     each step)."""
+    with _NoGC():
+        return _timed_steps(preps, steps, torch)
+
+
+def _timed_steps(preps, steps, torch):
     E = torch.cuda.Event
     ev = [(E(enable_timing=True), E(enable_timing=True)) for _ in range(steps)]
     torch.cuda.synchronize()
@@ -462,6 +482,11 @@ def abba(torch, calls_a, calls_b, rounds, per_call=False):
     leaves).  Returns the times of A and of B: one value per leg
     ([2 * rounds]) or, with per_call, one per call ([2 * rounds,
     len(calls)]), in ms."""
+    with _NoGC():
+        return _abba(torch, calls_a, calls_b, rounds, per_call)
+
+
+def _abba(torch, calls_a, calls_b, rounds, per_call):
     E = torch.cuda.Event
     recs = []
     n = len(calls_a) + len(calls_b)
@@ -524,9 +549,14 @@ def prepare(cfg, torch):
 
 
 def carry_expansions(preps):
-    """Tail mode over a sequence of GEMMs: every GEMM whose plan expands its
-    compact weight once per call, except the first of the sequence, has that
-    expansion carried by the launch of the GEMM before it."""
+    """Tail mode over a sequence of GEMMs: the compact weights are planned for
+    carried expansions (NM_PLAN_EXPAND_CARRIED), and every GEMM whose plan
+    expands its weight once per call, except the first of the sequence, has
+    that expansion carried by the launch of the GEMM before it."""
+    for p in preps:
+        if p.sparse_kernel and p.packed.desc.kind not in (nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_DENSE):
+            mode = (nmspmm.NM_OUT_I32 if p.out_i32 else 0) | (nmspmm.NM_OUT_F16 if p.out_f16 else 0)
+            p.set_sparse_plan(nmspmm.spmm_plan(p.packed.desc, p.g.m, mode | nmspmm.NM_PLAN_EXPAND_CARRIED))
     for prev, nxt in zip(preps, preps[1:]):
         if nxt.sparse_kernel and nxt.splan.expand and prev.tail_next is None:
             prev.carry_expansion_of(nxt)

@@ -56,6 +56,10 @@ typedef enum nm_status {
 #define NM_OUT_I32 1
 #define NM_OUT_F16 2
 #define NM_OUT_I8 4
+/* Planner hint (may be or-ed into the out_mode of nm_spmm_plan): the caller
+ * runs any once-per-call expansion the plan asks for in an earlier launch
+ * (nm_spmm_out_expand), so the expansion costs no launch of its own. */
+#define NM_PLAN_EXPAND_CARRIED 8
 
 /* Physical layouts of the packed weight produced by nm_compress, and the
  * kernel families they feed (nm_desc.layout, nm_desc.kind, nm_plan.kind; a
@@ -199,7 +203,11 @@ nm_status nm_tile_info(int tile, int *tile_n, int *tile_m);
  * (m, n, k, pattern) so that small-token shapes still occupy every compute
  * unit, with split_k from {1, 2, 4, 8}, k-splits on 128-wide k-step
  * boundaries and at least two k-steps per split.  Needs no GPU: without one
- * it assumes 256 compute units.  out_mode is a mask of NM_OUT_* bits. */
+ * it assumes 256 compute units.  out_mode is a mask of NM_OUT_* bits, plus
+ * NM_PLAN_EXPAND_CARRIED when the caller carries once-per-call expansions in
+ * an earlier launch: a compact weight is then expanded once per call whenever
+ * an output-split tile has many rows of tiles (without the hint, only for
+ * GEMMs large enough to amortise a launch of its own). */
 nm_status nm_spmm_plan(const nm_desc *desc, int m, int out_mode, nm_plan *plan);
 
 /* Completes a plan built by the caller (kind, tile, split_k, expand set) for

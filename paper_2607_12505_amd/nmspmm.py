@@ -22,6 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libnmspmm.so")
 
 NM_OK, NM_ERR_ARG, NM_ERR_SHAPE, NM_ERR_PATTERN, NM_ERR_UNSUPPORTED, NM_ERR_WORKSPACE, NM_ERR_HIP = range(7)
 NM_OUT_I32, NM_OUT_F16, NM_OUT_I8 = 1, 2, 4
+NM_PLAN_EXPAND_CARRIED = 8
 # kernel families; a packed layout and the family that consumes it share a number
 NM_KIND_SP42, NM_KIND_C14, NM_KIND_DENSE, NM_KIND_C18, NM_KIND_C28, NM_KIND_MK3, NM_KIND_MK4, NM_KIND_MK5 = range(1, 9)
 (NM_LAYOUT_SP42, NM_LAYOUT_C14, NM_LAYOUT_DENSE, NM_LAYOUT_C18, NM_LAYOUT_C28, NM_LAYOUT_MK3, NM_LAYOUT_MK4,

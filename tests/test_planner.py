@@ -51,6 +51,12 @@ def test_plan_rules(shape):
             assert nmspmm.workspace_size(p, m, n) == 16384 + want
         else:
             assert p.expand_bytes == 0 and nmspmm.workspace_size(p, m, n) == 0
+        # with the expansion carried by an earlier launch, every compact weight
+        # with many rows of output-split tiles is expanded once per call; the
+        # tile and split stay the same
+        c = nmspmm.spmm_plan(d, m, out | nmspmm.NM_PLAN_EXPAND_CARRIED)
+        assert (c.tile, c.split_k, c.grid) == (p.tile, p.split_k, p.grid)
+        assert c.expand == int(compact and rows >= 32 and not k_sliced)
         # deterministic
         q = nmspmm.spmm_plan(d, m, out)
         assert q.as_dict() == p.as_dict()
