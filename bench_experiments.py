@@ -787,10 +787,13 @@ def rocprof_summary(trace_dir, fetch_dir, write_dir, bench_json, copy_mib, comma
 
 
 
-def launch_labels(cfg):
+def launch_labels(cfg, carried=True):
     """(kernel name, grid in threads) -> the GEMMs of workload cfg launched that
-    way by the planner (sparse leg and dense baseline), from the plans alone."""
+    way by the planner (sparse leg and dense baseline), from the plans alone.
+    carried: the sparse leg was planned with NM_PLAN_EXPAND_CARRIED (bench.py's
+    default --expansion tail)."""
     from paper_2607_12505_amd import workloads as wl
+    hint = nmspmm.NM_PLAN_EXPAND_CARRIED if carried else 0
     labels = {}
     for g in wl.workload(cfg).gemms:
         # the linear with its batch or stage prefix, without the pattern or the layer index
@@ -799,7 +802,7 @@ def launch_labels(cfg):
             plans = [("dense", nmspmm.dense_plan(g.m, g.n, g.k, nmspmm.NM_OUT_I32))]
         else:
             plans = [(f"{g.N}:{g.M}", nmspmm.spmm_plan(nmspmm.compress_size(g.n, g.k, g.N, g.M), g.m,
-                                                     nmspmm.NM_OUT_I32)),
+                                                     nmspmm.NM_OUT_I32 | hint)),
                      ("dense baseline", nmspmm.dense_plan(g.m, g.n, g.k, nmspmm.NM_OUT_I32))]
         for pat, p in plans:
             name = nmspmm.plan_kernel_name(p)
@@ -931,7 +934,7 @@ def launch_shape_table(line, trace_dir, fetch_dir, write_dir, f_scale, w_scale, 
     cfg = _workload_cfg(line)
     if cfg is None:
         return []
-    labels = launch_labels(cfg)
+    labels = launch_labels(cfg, carried=str(line.get("compact_weight_expansion", "")).startswith("carried"))
 
     def short(n):
         m = re.search(r"(k_gemm(?:_ks)?<[^>]*>)", n)
