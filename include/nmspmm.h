@@ -395,10 +395,11 @@ nm_status nm_gemm_i8_dense_out(const int8_t *X, int m, const int8_t *W, int n, i
  * that runs linears in sequence expands the next linear's weight this way and
  * then runs that linear on the expanded form (nm_spmm_out with the descriptor
  * nm_expand_size gives, vals = job->out, meta = job->out + its vals_bytes),
- * with no launch of its own for the expansion.  job->out must not overlap any
- * buffer of the GEMM; job == NULL is exactly nm_spmm_out.  With m == 0 the
- * job is still run (alone).  Errors: as nm_spmm_out, plus those of nm_expand
- * for the job (checked before anything is launched). */
+ * with no launch of its own for the expansion.  job == NULL is exactly
+ * nm_spmm_out.  With m == 0 the job is still run (alone).  Errors: as
+ * nm_spmm_out, plus those of nm_expand for the job, and NM_ERR_ARG when
+ * job->out overlaps X, the weight, an output, the workspace the plan uses or
+ * the job's own packed weight (all checked before anything is launched). */
 nm_status nm_spmm_out_expand(const int8_t *X, int m, const int8_t *vals, const uint8_t *meta,
                              const nm_desc *desc, const nm_outputs *out, void *ws, size_t ws_bytes,
                              void *stream, const nm_plan *plan, const nm_expand_job *job);

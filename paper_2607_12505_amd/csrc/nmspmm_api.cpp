@@ -46,6 +46,14 @@ int64_t stored_weight_bytes(int kind, int n, int k, int n_frags, int k_steps) {
 
 int group_rows_for(int tiles_m) { return tiles_m >= 2 * kGroupRows ? kGroupRows : 0; }
 
+// Whether the byte ranges [a, a + na) and [b, b + nb) intersect (a null or
+// empty range intersects nothing).
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
+    if (!a || !b || na <= 0 || nb <= 0) return false;
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
 }  // namespace
 
 namespace nmspmm {
@@ -104,6 +112,21 @@ nm_status run_gemm(int kind, const int8_t *X, int m, const int8_t *A, const uint
         if (st != NM_OK) return st;
     }
     if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return NM_ERR_WORKSPACE;
+    if (job) {
+        // the expansion a launch carries writes job->out while the GEMM runs:
+        // it may not overlap anything the GEMM reads or writes
+        const int64_t jb = (int64_t)job->out_bytes, mn = (int64_t)m * n;
+        if (overlaps(job->out, jb, X, (int64_t)m * k) ||
+            overlaps(job->out, jb, A, kind == NM_KIND_DENSE ? (int64_t)n * k
+                                                            : (int64_t)n_frags * k_steps * 64 * layout_lane_vbytes(kind)) ||
+            overlaps(job->out, jb, meta, kind == NM_KIND_DENSE ? 0
+                                                               : (int64_t)n_frags * k_steps * 64 * layout_lane_mbytes(kind)) ||
+            overlaps(job->out, jb, o.y, 4 * mn) || overlaps(job->out, jb, o.yh, 2 * mn) ||
+            overlaps(job->out, jb, o.yq, mn) || overlaps(job->out, jb, ws, (int64_t)need) ||
+            overlaps(job->out, jb, job->vals, job->desc->vals_bytes) ||
+            overlaps(job->out, jb, job->meta, job->desc->meta_bytes))
+            return NM_ERR_ARG;
+    }
 
     // With expand = 1 the compact weight is first expanded into the workspace
     // (after the split-K area), and the 4:2-operand or dense kernel runs on it.

@@ -126,6 +126,14 @@ def test_host_side_argument_checks_need_no_gpu():
                                          ctypes.byref(small)) == nmspmm.NM_ERR_WORKSPACE
     assert L.nm_gemm_i8_dense_out_expand(fake, -1, fake, 64, 128, ctypes.byref(y_out), nul, 0, nul, None,
                                          ctypes.byref(small)) == nmspmm.NM_ERR_SHAPE
+    # the carried expansion may not write into anything the GEMM touches (checked before any launch)
+    base = 1 << 30
+    X, W, Yp = base, base + (1 << 24), base + (2 << 24)
+    y_at = nmspmm.NmOutputs(Yp, None, None, None, None)
+    for out_at in (X + 4096, W, Yp + 64 * 64 * 4 - 16):
+        job = nmspmm.NmExpandJob(ctypes.pointer(c28), base + (3 << 24), base + (4 << 24), out_at, 1 << 16)
+        assert L.nm_gemm_i8_dense_out_expand(ctypes.c_void_p(X), 64, ctypes.c_void_p(W), 64, 128, ctypes.byref(y_at),
+                                             nul, 0, nul, None, ctypes.byref(job)) == nmspmm.NM_ERR_ARG
     assert L.nm_quantize_f16(fake, -1, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_SHAPE
     assert L.nm_quantize_f16(misaligned, 16, ctypes.c_float(1.0), fake, nul) == nmspmm.NM_ERR_ARG
     P = nmprobe.lib()
@@ -179,7 +187,8 @@ def test_launch_failures_report_nm_err_hip():
     c14 = nmspmm.compress_size(64, 128, 1, 4)
     assert L.nm_expand(ctypes.byref(c14), fake, fake, fake, 1 << 20, nul) == nmspmm.NM_ERR_HIP
     y_out = nmspmm.NmOutputs(fake.value, None, None, None, None)
-    job = nmspmm.NmExpandJob(ctypes.pointer(c14), fake.value, fake.value, fake.value, 1 << 20)
+    far = [ctypes.c_void_p((1 << 32) + (i << 24)) for i in range(3)]    # the job's buffers, apart from the GEMM's
+    job = nmspmm.NmExpandJob(ctypes.pointer(c14), far[0].value, far[1].value, far[2].value, 1 << 20)
     assert L.nm_spmm_out_expand(fake, 64, fake, fake, ctypes.byref(d), ctypes.byref(y_out), nul, 0, nul, None,
                                 ctypes.byref(job)) == nmspmm.NM_ERR_HIP
     assert L.nm_gemm_i8_dense_out_expand(fake, 0, fake, 64, 128, ctypes.byref(y_out), nul, 0, nul, None,

@@ -230,3 +230,25 @@ def test_bad_job_launches_nothing():
     assert e.value.status == nmspmm.NM_ERR_ARG
     torch.cuda.synchronize()
     assert (Y == -7).all().item() and (out == SENTINEL).all().item()
+
+
+def test_job_overlapping_the_gemm_is_refused():
+    import ctypes
+    import torch
+    rng = np.random.default_rng(10)
+    W = wl.random_nm(64, 256, 2, 4, rng, full=True)
+    dw = nmspmm.DeviceWeight.from_packed(nmspmm.compress(W, 2, 4))
+    pj = nmspmm.compress(wl.random_nm(64, 256, 2, 8, rng, full=True), 2, 8)
+    dj = nmspmm.DeviceWeight.from_packed(pj)
+    _, nbytes = nmspmm.expand_size(pj.desc)
+    X = torch.ones((100, 256), dtype=torch.int8, device="cuda")
+    Y = torch.full((100, 64), -7, dtype=torch.int32, device="cuda")     # 25600 bytes >= nbytes
+    assert Y.numel() * 4 >= nbytes
+    for target in (Y, X):
+        job = nmspmm.NmExpandJob(ctypes.pointer(pj.desc), dj.vals.data_ptr(), dj.meta.data_ptr(), target.data_ptr(),
+                                 nbytes)
+        with pytest.raises(nmspmm.NmError) as e:
+            nmspmm.spmm(X, dw, Y=Y, job=job)
+        assert e.value.status == nmspmm.NM_ERR_ARG
+    torch.cuda.synchronize()
+    assert (Y == -7).all().item() and (X == 1).all().item()
