@@ -553,10 +553,21 @@ def carry_expansions(preps):
     carried expansions (NM_PLAN_EXPAND_CARRIED), and every GEMM whose plan
     expands its weight once per call, except the first of the sequence, has
     that expansion carried by the launch of the GEMM before it."""
-    for p in preps:
-        if p.sparse_kernel and p.packed.desc.kind not in (nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_DENSE):
+    for i, p in enumerate(preps):
+        # the first GEMM of the sequence has no launch before it to carry its expansion
+        if i > 0 and p.sparse_kernel and p.packed.desc.kind not in (nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_DENSE):
             mode = (nmspmm.NM_OUT_I32 if p.out_i32 else 0) | (nmspmm.NM_OUT_F16 if p.out_f16 else 0)
             p.set_sparse_plan(nmspmm.spmm_plan(p.packed.desc, p.g.m, mode | nmspmm.NM_PLAN_EXPAND_CARRIED))
+    relink_carried(preps)
+
+
+def relink_carried(preps):
+    """Re-derives which launch carries which expansion from the current plans
+    (after plans changed)."""
+    for p in preps:
+        p.tail_next = None
+        p.pre_expanded = False
+        p._build_args()
     for prev, nxt in zip(preps, preps[1:]):
         if nxt.sparse_kernel and nxt.splan.expand and prev.tail_next is None:
             prev.carry_expansion_of(nxt)

@@ -1009,16 +1009,22 @@ def launch_shape_table(line, trace_dir, fetch_dir, write_dir, f_scale, w_scale, 
     return md
 
 
-def chain_sweep(torch, cfg, rounds, out_path, report):
+def chain_sweep(torch, cfg, rounds, out_path, report, carried=False):
     """Planner evaluation inside a workload's own steps: for every distinct
     (shape, kind) of the sparse leg, every (tile, expansion) candidate with
     split_k = 1 is put on all GEMMs of that key and timed in ABBA rounds of
     whole steps (sparse leg, dense leg) with an event after every GEMM, so each
     candidate sees the cache state of the step itself (every layer with its
     own cold inputs and outputs in the ViT-L chain).  Reports per key the
-    planner's choice, the fastest candidate and their times."""
+    planner's choice, the fastest candidate and their times.
+
+    carried: the steps run as bench.py's default does (expansions carried by
+    the previous launch, plans with NM_PLAN_EXPAND_CARRIED); a candidate's
+    time then also counts the launches that carry its expansions."""
     import bench
     work, preps = bench.prepare(cfg, torch)
+    if carried:
+        bench.carry_expansions(preps)
     sp = [p.run_sparse for p in preps]
     dn = [p.run_dense for p in preps]
     bench.abba(torch, sp, dn, 1, per_call=True)
@@ -1035,6 +1041,7 @@ def chain_sweep(torch, cfg, rounds, out_path, report):
         planned = nmspmm.NmPlan.from_buffer_copy(first.dplan if baseline else first.splan)
         compact = not baseline and kind not in (nmspmm.NM_KIND_SP42, nmspmm.NM_KIND_DENSE)
         times = {}
+        ref = {}   # carried: per-call times under the first in-kernel-expansion candidate
         for tile in range(nmspmm.num_tiles()):
             for expand in ((0, 1) if compact else (0,)):
                 cand = nmspmm.make_plan(nmspmm.NM_KIND_DENSE if baseline else kind, tile, 1, expand)
@@ -1047,13 +1054,31 @@ def chain_sweep(torch, cfg, rounds, out_path, report):
                     continue
                 for i in idx:
                     preps[i].set_dense_plan(cand) if baseline else preps[i].set_sparse_plan(cand)
+                if carried:
+                    bench.relink_carried(preps)
                 try:
                     ta, tb = bench.abba(torch, sp, dn, rounds, per_call=True)
                 except nmspmm.NmError:
                     continue
-                times[(tile, expand)] = float((tb if baseline else ta)[:, idx].mean()) * 1e3
+                if carried and not baseline:
+                    # per GEMM of the key: its own time, plus what carrying its
+                    # expansion adds to the launch before it (that launch's time
+                    # here minus its time under an in-kernel-expansion candidate)
+                    pc = ta.mean(axis=0) * 1e3
+                    carriers = [i - 1 for i in idx
+                                if i > 0 and i - 1 not in idx and preps[i - 1].tail_next is preps[i]]
+                    if expand == 0:
+                        ref.setdefault("pc", pc)
+                    if carriers and "pc" not in ref:
+                        continue
+                    extra = sum(pc[j] - ref["pc"][j] for j in carriers)
+                    times[(tile, expand)] = float(pc[idx].sum() + extra) / len(idx)
+                else:
+                    times[(tile, expand)] = float((tb if baseline else ta)[:, idx].mean()) * 1e3
         for i in idx:
             preps[i].set_dense_plan(planned) if baseline else preps[i].set_sparse_plan(planned)
+        if carried:
+            bench.relink_carried(preps)
         best = min(times, key=times.get)
         t_plan = times.get((planned.tile, planned.expand))
         row = {"m": m, "k": k, "n": n, "kind": kind, "gemms": len(idx), "planned": [planned.tile, planned.expand],
@@ -1070,14 +1095,18 @@ def chain_sweep(torch, cfg, rounds, out_path, report):
         with open(out_path, "w") as f:
             json.dump({"summary": summary, "rows": rows}, f)
     if report:
-        md = [f"# Planner choices inside the {work.name} steps", "",
-              f"Command: `python3 bench_experiments.py --chain-sweep {cfg} --rounds {rounds} --report {report}` (repository root).  "
+        flag = " --carried" if carried else ""
+        md = [f"# Planner choices inside the {work.name} steps" + (" with carried expansions" if carried else ""), "",
+              f"Command: `python3 bench_experiments.py --chain-sweep {cfg}{flag} --rounds {rounds} --report {report}` (repository root).  "
               "For every distinct (shape, kind) of the sparse leg, every tile with split_k = 1 (and, for the compact "
               "kinds, both places of the weight expansion: e0 inside every workgroup, e1 once per call) is put on "
               "all GEMMs of that key and timed inside whole steps (ABBA rounds of the sparse and dense legs, an "
               f"event after every GEMM, {rounds} rounds); times are means per GEMM in microseconds.  Kinds: "
               "1 = 2:4, 2 = 1:4, 3 = dense, 4 = 1:8, 5 = 2:8, 6-8 = 3:8-5:8; \"baseline\": the dense leg (the "
-              "dense INT8 GEMM every speedup divides by) of that shape.", "",
+              "dense INT8 GEMM every speedup divides by) of that shape." +
+              (("  Expansions once per call are carried by the previous GEMM's launch, as bench.py runs the steps; a "
+                "compact kind's time per GEMM includes the share of those launches (the planned choice is "
+                "NM_PLAN_EXPAND_CARRIED's).") if carried else ""), "",
               f"Top-1 hit rate {summary['top1_hit_rate']}, average normalised performance "
               f"{summary['avg_norm_perf']}, worst {summary['worst_norm_perf']}.", "",
               "| m | k | n | kind | GEMMs | planned | us | best | us | ratio | all candidates (tile/expand: us) |",
@@ -1109,6 +1138,8 @@ def main():
                     help="per-launch-shape table of stall counters from rocprofv3 --pmc passes of one bench run "
                          "(no GPU needed; with --summary-out, --commands, --stall-config)")
     ap.add_argument("--stall-config", type=int, default=4, help="workload of the --pmc-stalls bench run")
+    ap.add_argument("--carried", action="store_true",
+                    help="--chain-sweep with the expansions carried by the previous launch (bench.py's default)")
     ap.add_argument("--summary-out", type=str, default=None, help="markdown file written by --rocprof-summary")
     ap.add_argument("--commands", type=str, default=None, help="file with the profiling commands to quote")
     ap.add_argument("--copy-calibration", type=int, default=256, metavar="MIB",
@@ -1152,7 +1183,7 @@ def main():
     torch.cuda.set_device(0)
     if args.chain_sweep is not None:
         print(json.dumps({"chain_sweep": chain_sweep(torch, args.chain_sweep, args.rounds, args.sweep_out,
-                                                     args.report)}), flush=True)
+                                                     args.report, carried=args.carried)}), flush=True)
     elif args.sweep:
         summary = sweep([c if c == "grid" else int(c) for c in args.sweep.split(",")], torch, 10, args.sweep_out)
         print(json.dumps({"planner_evaluation": summary}), flush=True)

@@ -205,9 +205,10 @@ nm_status nm_tile_info(int tile, int *tile_n, int *tile_m);
  * boundaries and at least two k-steps per split.  Needs no GPU: without one
  * it assumes 256 compute units.  out_mode is a mask of NM_OUT_* bits, plus
  * NM_PLAN_EXPAND_CARRIED when the caller carries once-per-call expansions in
- * an earlier launch: a compact weight is then expanded once per call whenever
- * an output-split tile has many rows of tiles (without the hint, only for
- * GEMMs large enough to amortise a launch of its own). */
+ * an earlier launch: a compact weight is then expanded once per call (1:4,
+ * whose in-kernel decode is cheapest, only with many rows of output-split
+ * tiles); without the hint, only GEMMs large enough to amortise a launch of
+ * its own expand once per call. */
 nm_status nm_spmm_plan(const nm_desc *desc, int m, int out_mode, nm_plan *plan);
 
 /* Completes a plan built by the caller (kind, tile, split_k, expand set) for

@@ -236,14 +236,23 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
     const bool many_rows = ceil_div(mm, kTiles[tile].tile_m()) >= kExpandTileRows;
     const bool k_sliced = kTiles[tile].layout == kKSliced;
     const bool long_gemm = (int64_t)mm * n * k >= ((int64_t)1 << 33);
-    // With the expansion carried by an earlier launch, the pass costs no
-    // launch of its own and the 4:2-operand or dense kernel on the expanded
-    // weight beats the decode repeated per row of tiles for every kind.
+    // With the expansion carried by an earlier launch the pass costs no
+    // launch of its own.  Timed inside the workload steps with the expansions
+    // carried: the 4:2-operand or dense kernel on the expanded weight then
+    // beats the in-kernel decode for 1:8, 2:8 and the mask layouts at every
+    // token count, k-sliced tiles included (DeiT-B batch 8 qkv 2:8 11.3 us
+    // against 13.1, Swin-B stage 4 proj 2:8 9.0 against 12.1, ViT-L fc1 4:8
+    // 112 against 127), and for 1:4, whose decode is a few permutes, only
+    // with many rows of output-split tiles (DeiT-B batch 1 fc2 1:4 8.7 us
+    // in-kernel against 10.3).
     const bool carried = (out_mode & NM_PLAN_EXPAND_CARRIED) != 0;
-    bool once = carried || long_gemm;
-    if (!carried && kind == NM_KIND_C14) once = once && (k_steps >= 24 || n >= 4096 || tile == kT256x256w8);
-    if (!carried && kind == NM_KIND_C18) once = once && (k_steps >= 24 || n >= 2048 || tile == kT256x256w8);
-    plan->expand = kind_is_compact(kind) && many_rows && !k_sliced && once ? 1 : 0;
+    bool once = long_gemm;
+    if (kind == NM_KIND_C14) once = once && (k_steps >= 24 || n >= 4096 || tile == kT256x256w8);
+    if (kind == NM_KIND_C18) once = once && (k_steps >= 24 || n >= 2048 || tile == kT256x256w8);
+    if (carried)
+        plan->expand = kind_is_compact(kind) && (kind != NM_KIND_C14 || (many_rows && !k_sliced)) ? 1 : 0;
+    else
+        plan->expand = kind_is_compact(kind) && many_rows && !k_sliced && once ? 1 : 0;
     return complete_plan(kind, m, n, k, plan);
 }
 
