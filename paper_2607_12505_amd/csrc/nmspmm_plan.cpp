@@ -157,14 +157,23 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
         tile = (!heavy && k_steps == 1 && n >= 384) ? kT128x32r2 : kT64x64r2;
     } else if (k_steps == 3) {
         // Three k-steps (DeiT-S, k = 384): 128 x 32 for one-stream weights,
-        // 64 x 64 for the heavier operands.
-        tile = heavy ? kT64x64r2 : kT128x32r2;
+        // 128 ch x 64 tok for the heavier operands (DeiT-S batch 64 proj,
+        // dense, inside the steps: 12.5 us against 13.8-14.1 for 64 x 64; qkv
+        // and fc1 within 1-3 %).
+        tile = heavy ? kT128x64r2 : kT128x32r2;
     } else if (tiles_of(kT128x128r2, mm, n) < 4 * cus) {
         // Medium: with long reductions (8 k-steps or more) the operand fill
         // per output decides, so 128 x 128 as long as every compute unit
-        // still gets a tile; otherwise half-height tiles (narrower for the
-        // heavier operands).
-        if (k_steps >= 8 && tiles_of(kT128x128r2, mm, n) >= cus) {
+        // still gets a tile and the last tiles do not leave most units with
+        // one while a few run two (1.25 tiles per unit or more); otherwise
+        // half-height tiles (narrower for the heavier operands): DeiT-S batch
+        // 64 fc2 (297 tiles of 128 x 128) 2:4 17.3 us against 18.5-18.7,
+        // Swin-B stage 4 fc1 (312 tiles) dense 13.8-14.5 against 14.9-15.6.
+        // A heavier operand whose channels fit one 128-row tile keeps 128 x
+        // 128, which reads X once (Swin-B stage 1 fc2, 128 channels, dense:
+        // 22.4-23.6 us against 23.7-25.3 for 64 x 128).
+        const int64_t t128 = tiles_of(kT128x128r2, mm, n);
+        if ((k_steps >= 8 && 4 * t128 >= 5 * cus) || (heavy && n <= 128 && t128 >= cus)) {
             tile = kT128x128r2;
         } else if (!heavy && k_steps < 8 && tiles_of(kT64x64r2, mm, n) <= 6 * cus) {
             // short reductions: 64 x 64 while it gives at most 6 workgroups
@@ -172,7 +181,12 @@ nm_status make_plan(int kind, int m, int n, int k, int out_mode, nm_plan *plan) 
             // 13.4 and 15.0 for 128 x 64)
             tile = kT64x64r2;
         } else {
-            tile = heavy ? kT64x128r2 : kT128x64r2;
+            // the heavier operands take 64 ch x 128 tok, except with long
+            // reductions (12 k-steps or more), where 128 ch x 64 tok won in
+            // every sweep inside the steps (DeiT-S batch 64 fc2 dense 18.8-19.6
+            // us against 20.2-21.3, Swin-B stage 3 fc2 dense 17.4-18.0
+            // against 18.0-19.1)
+            tile = heavy && k_steps < 12 ? kT64x128r2 : kT128x64r2;
             // 64 x 64 when those would leave compute units without a tile,
             // and for one-stream weights when they already give 4 or more
             // workgroups per compute unit

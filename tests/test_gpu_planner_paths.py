@@ -31,11 +31,16 @@ CASES = [
     (3000, 256, 128, "sp", (64, 64), False),    # ... narrower: 64 x 64
     (3000, 512, 256, "sp", (64, 64), False),    # two k-steps: 64 x 64
     (2000, 768, 384, "sp", (128, 32), False),   # three k-steps, one stream: 128 x 32
-    (2000, 768, 384, "mk", (64, 64), False),    # ... heavier operands: 64 x 64
-    (4000, 1024, 1024, "sp", (128, 128), False),  # medium, long reduction: 128 x 128
+    (2000, 768, 384, "mk", (128, 64), False),   # ... heavier operands: 128 ch x 64 tok
+    (5200, 1024, 1024, "sp", (128, 128), False),  # medium, long reduction: 128 x 128
+    (4000, 1152, 1024, "sp", (128, 64), False),   # ... half-height under 1.25 such tiles per CU
+    (1568, 3072, 1024, "dn", (64, 128), False),   # ... narrower for the heavier operands
+    (33000, 128, 512, "dn", (128, 128), False),   # ... heavier operands 128 channels wide: 128 x 128
+    (33000, 128, 512, "mk", (128, 128), False),
     (1600, 2304, 768, "sp", (64, 64), False),   # medium, short reduction: 64 x 64 up to 6 per CU
     (2560, 2560, 768, "sp", (128, 64), False),  # ... past that, half-height tiles
     (1600, 2304, 768, "dn", (64, 128), False),  # ... narrower for the heavier operands
+    (6272, 512, 2048, "dn", (128, 64), False),  # ... but not with 12 or more k-steps
     (6272, 1536, 512, "sp", (64, 64), False),   # ... 64 x 64 past 4 half-height tiles per CU
     (8192, 2048, 512, "sp", (128, 128), False),  # large: 128 x 128
     (4096, 4096, 3072, "mk", (256, 256), False),  # large, heavier operands, 4096 wide, long reduction: 256 x 256

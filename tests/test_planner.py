@@ -156,12 +156,13 @@ def test_large_shapes_use_large_tiles():
     p = nmspmm.spmm_plan(d, 25216, nmspmm.NM_OUT_I32)    # fc2 at batch 128
     assert (p.tile_n, p.tile_m) == (128, 128)
     # three k-steps (DeiT-Small, k = 384): 128 channels x 32 tokens for
-    # 4:2-operand weights, 64 x 64 for the dense-tile ones
+    # 4:2-operand weights, 128 channels x 64 tokens for the dense-tile ones
     d = nmspmm.compress_size(1152, 384, 2, 4)
     assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 12608, 1)) == "k_gemm<1, 2, 2, 4, 1, 2>"
     d = nmspmm.compress_size(1152, 384, 4, 8)
     # expanded inside the workgroups (a GEMM of 5.6e9 multiply-adds, too short for the extra pass)
-    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 12608, 1)) == "k_gemm<7, 2, 2, 2, 2, 2>"
+    assert nmspmm.plan_kernel_name(nmspmm.spmm_plan(d, 12608, 1)) == "k_gemm<7, 2, 2, 4, 2, 2>"
+    assert nmspmm.plan_kernel_name(nmspmm.dense_plan(12608, 384, 384, 1)) == "k_gemm<3, 2, 2, 4, 2, 2>"
     d = nmspmm.compress_size(384, 384, 2, 4)
     assert (nmspmm.spmm_plan(d, 12608, 1).tile_n, nmspmm.spmm_plan(d, 12608, 1).tile_m) == (128, 32)
     # medium token counts, short reductions: 64 x 64 while it gives at most 4
@@ -188,6 +189,25 @@ def test_large_shapes_use_large_tiles():
     assert (nmspmm.spmm_plan(d, 25088, 1).tile_n, nmspmm.spmm_plan(d, 25088, 1).tile_m) == (128, 128)
     d = nmspmm.compress_size(512, 2048, 2, 4)
     assert (nmspmm.spmm_plan(d, 6272, 1).tile_n, nmspmm.spmm_plan(d, 6272, 1).tile_m) == (128, 64)
+    # ... and half-height tiles when 128 x 128 gives fewer than 1.25 tiles per
+    # compute unit (DeiT-S batch 64 fc2, k = 1536: 297 tiles; Swin-B stage 4
+    # fc1, k = 1024: 312 tiles), narrower for the dense-tile weights
+    d = nmspmm.compress_size(384, 1536, 2, 4)
+    assert (nmspmm.spmm_plan(d, 12608, 1).tile_n, nmspmm.spmm_plan(d, 12608, 1).tile_m) == (128, 64)
+    p = nmspmm.dense_plan(1568, 3072, 1024, 1)
+    assert (p.tile_n, p.tile_m) == (64, 128)
+    # ... except with 12 or more k-steps (DeiT-S batch 64 fc2, Swin-B stage 3
+    # fc2 of the dense baseline): 128 ch x 64 tok
+    p = nmspmm.dense_plan(12608, 384, 1536, 1)
+    assert (p.tile_n, p.tile_m) == (128, 64)
+    p = nmspmm.dense_plan(6272, 512, 2048, 1)
+    assert (p.tile_n, p.tile_m) == (128, 64)
+    d = nmspmm.compress_size(3072, 1024, 2, 4)
+    assert (nmspmm.spmm_plan(d, 1568, 1).tile_n, nmspmm.spmm_plan(d, 1568, 1).tile_m) == (128, 64)
+    # a dense-tile weight whose channels fit one 128-row tile keeps 128 x 128
+    # at short reductions (Swin-B stage 1 fc2: 128 channels, k = 512)
+    p = nmspmm.dense_plan(100352, 128, 512, 1)
+    assert (p.tile_n, p.tile_m, p.tile) == (128, 128, 0)
     # ... or 64 x 64 when half-height tiles would leave compute units idle
     # (Swin-B stage 4 fc2 of the dense baseline: 96 tiles of 64 x 128)
     assert nmspmm.plan_kernel_name(nmspmm.dense_plan(1568, 1024, 4096, 1)) == "k_gemm<3, 2, 2, 2, 2, 2>"
