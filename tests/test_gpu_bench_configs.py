@@ -58,14 +58,17 @@ def test_bench_expand_ahead_matches_oracle_rows(capsys, monkeypatch):
     assert line["value"] > 0
 
 
-def test_bench_expand_in_tail_matches_oracle_rows(capsys, monkeypatch):
-    # ViT-L chain: every GEMM whose plan expands its weight once per call has
-    # that expansion carried by the previous GEMM's launch; the CPU baseline
-    # compares the sampled rows of every GEMM with the oracle.
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_bench_expand_in_tail_matches_oracle_rows(cfg, capsys, monkeypatch):
+    # Every GEMM whose plan expands its weight once per call has that
+    # expansion carried by the previous GEMM's launch (on DeiT-S, DeiT-B and
+    # Swin-B also at few tokens and on k-sliced tiles, and carried by k-sliced
+    # launches); the CPU baseline compares the sampled rows of every GEMM with
+    # the oracle.
     import bench
-    monkeypatch.setattr(sys, "argv", ["bench.py", "--config", "4", "--steps", "1", "--warmup", "1", "--rounds", "2",
-                                      "--cpu-budget", "2", "--no-secondary", "--no-mfma-ceiling", "--no-store-only",
-                                      "--expansion", "tail"])
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--config", str(cfg), "--steps", "1", "--warmup", "1", "--rounds",
+                                      "2", "--cpu-budget", "2", "--no-secondary", "--no-mfma-ceiling",
+                                      "--no-store-only", "--expansion", "tail"])
     bench.main()
     line = json.loads(capsys.readouterr().out.strip().splitlines()[-1])
     assert line["compact_weight_expansion"].startswith("carried")
