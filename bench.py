@@ -421,10 +421,11 @@ def mfma_ceiling(torch, iters: int = 4000, reps: int = 3) -> dict:
 # timing
 
 def sleep_cycles_for(launches: int) -> int:
-    """Device-side sleep before a batch of `launches` launches, long enough for
-    the host to queue them ahead of the GPU (about 12 us per launch, at most
-    20 ms), so host launch overhead stays out of the event times."""
-    return int(2.1e9 * min(12e-6 * launches, 20e-3))
+    """Device-side sleep before a batch of `launches` host-side queue
+    operations (kernel launches and event records), long enough for the host
+    to queue them ahead of the GPU (about 15 us each, at most 20 ms), so host
+    launch overhead stays out of the event times."""
+    return int(2.1e9 * min(15e-6 * launches, 20e-3))
 
 
 def hold_side_stream(torch):
@@ -489,9 +490,13 @@ def abba(torch, calls_a, calls_b, rounds, per_call=False):
 def _abba(torch, calls_a, calls_b, rounds, per_call):
     E = torch.cuda.Event
     recs = []
-    n = len(calls_a) + len(calls_b)
+    # a round queues an untimed leg and four timed legs, with an event after
+    # every call in per-call mode: the sleep covers all of it, so that the
+    # GPU never waits for the host inside a timed leg (a short GEMM's event
+    # time would otherwise include that wait)
+    ops = 5 * max(len(calls_a), len(calls_b)) * (2 if per_call else 1) + 8
     for _ in range(rounds):
-        torch.cuda._sleep(sleep_cycles_for(2 * n))
+        torch.cuda._sleep(sleep_cycles_for(ops))
         for c in calls_b:
             c()
         for which in (0, 1, 1, 0):

@@ -935,6 +935,7 @@ def launch_shape_table(line, trace_dir, fetch_dir, write_dir, f_scale, w_scale, 
     if cfg is None:
         return []
     labels = launch_labels(cfg, carried=str(line.get("compact_weight_expansion", "")).startswith("carried"))
+    work = wl.workload(cfg)
 
     def short(n):
         m = re.search(r"(k_gemm(?:_ks)?<[^>]*>)", n)
@@ -965,7 +966,8 @@ def launch_shape_table(line, trace_dir, fetch_dir, write_dir, f_scale, w_scale, 
     active = per_shape(sq_dir, "GRBM_GUI_ACTIVE") if sq_dir else {}
     md = ["", "Per launch shape of the workload (kernel and grid, matched to the GEMMs the planner launches that "
           "way): average duration from the kernel trace, HBM bytes per dispatch from the scaled counters, "
-          "algorithmic bytes (X + stored weight + int32 Y) and dense-equivalent ops of those GEMMs, and the "
+          "algorithmic bytes (X + stored weight + the workload's outputs: int32 Y, and fp16 Yh with its scales "
+          "where the workload writes it) and dense-equivalent ops of those GEMMs, and the "
           "fraction of the HBM peak (8 TB/s) and of the matrix-instruction peak of the kind (2:4-operand "
           "kernels against 10.07 dense-equivalent POPS, dense against 5.03):", "",
           "| kernel | workgroups | GEMMs | us | HBM MB | alg. MB | HBM frac | POPS | MFMA frac | MFMA busy % |",
@@ -993,7 +995,8 @@ def launch_shape_table(line, trace_dir, fetch_dir, write_dir, f_scale, w_scale, 
 
         # the GEMMs of one launch shape share m, k and n; their stored weights
         # differ by pattern (a small part of the bytes): averaged
-        alg = m * k + 4 * m * n + float(np.mean([stored(p) for *_, p in gemms]))
+        alg = (m * k + (4 * m * n if work.out_int32 else 0) + (2 * m * n + 4 * n if work.out_f16 else 0)
+               + float(np.mean([stored(p) for *_, p in gemms])))
         ops = 2.0 * m * n * k
         hbm = ((np.mean(fetch[key]) * 1024 * f_scale + np.mean(write[key]) * 1024 * w_scale) / 1e6
                if key in fetch and key in write else float("nan"))
