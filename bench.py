@@ -282,8 +282,7 @@ def store_only_time(preps, idx, torch, reps=10):
     for plan, m, n, o in calls:
         if L.nm_probe_store_only(plan, m, n, ctypes.byref(o), stream) != nmspmm.NM_OK:
             return None
-    E = torch.cuda.Event
-    ev = [(E(enable_timing=True), E(enable_timing=True)) for _ in range(reps)]
+    ev = [(timing_event(), timing_event()) for _ in range(reps)]
     for e0, e1 in ev:
         torch.cuda._sleep(int(2.4e9 * 25e-6 * len(calls)))
         e0.record()
@@ -420,6 +419,13 @@ def mfma_ceiling(torch, iters: int = 4000, reps: int = 3) -> dict:
 # ---------------------------------------------------------------------------
 # timing
 
+def timing_event():
+    """An event for the timings below, recorded without the system-scope fence
+    of a default HIP event (whose cache write-back and invalidation would add
+    microseconds after every timed GEMM and hand the next one cold caches)."""
+    return nmprobe.TimingEvent()
+
+
 def sleep_cycles_for(launches: int) -> int:
     """Device-side sleep before a batch of `launches` host-side queue
     operations (kernel launches and event records), long enough for the host
@@ -461,8 +467,7 @@ def timed_steps(preps, steps, torch):
 
 
 def _timed_steps(preps, steps, torch):
-    E = torch.cuda.Event
-    ev = [(E(enable_timing=True), E(enable_timing=True)) for _ in range(steps)]
+    ev = [(timing_event(), timing_event()) for _ in range(steps)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     for e0, e1 in ev:
@@ -488,7 +493,6 @@ def abba(torch, calls_a, calls_b, rounds, per_call=False):
 
 
 def _abba(torch, calls_a, calls_b, rounds, per_call):
-    E = torch.cuda.Event
     recs = []
     # a round queues an untimed leg and four timed legs, with an event after
     # every call in per-call mode: the sleep covers all of it, so that the
@@ -500,16 +504,16 @@ def _abba(torch, calls_a, calls_b, rounds, per_call):
         for c in calls_b:
             c()
         for which in (0, 1, 1, 0):
-            ev = [E(enable_timing=True)]
+            ev = [timing_event()]
             ev[0].record()
             hold_side_stream(torch)
             for c in (calls_a if which == 0 else calls_b):
                 c()
                 if per_call:
-                    ev.append(E(enable_timing=True))
+                    ev.append(timing_event())
                     ev[-1].record()
             if not per_call:
-                ev.append(E(enable_timing=True))
+                ev.append(timing_event())
                 ev[-1].record()
             recs.append((which, ev))
     torch.cuda.synchronize()

@@ -77,6 +77,25 @@ nm_status nm_probe_mfma_layout(int kind, const int32_t *a, const int32_t *b, con
  * m == 0 writes nothing. */
 nm_status nm_probe_store_only(const nm_plan *plan, int m, int n, const nm_outputs *out, void *stream);
 
+/* Timing events (hipEvent_t behind a void pointer) created with
+ * hipEventDisableSystemFence: recording one adds no system-scope memory
+ * fence (no cache write-back and invalidation) when it completes, so events
+ * placed between the GEMMs of a sequence time them without changing what the
+ * caches hold or adding that fence's cost to the next GEMM.  Only for timing:
+ * elapsed times are valid once the host has synchronised with the stream.
+ *   nm_probe_event_create:      *event = a new event (caller destroys it)
+ *   nm_probe_event_destroy:     frees it
+ *   nm_probe_event_record:      records it on `stream` (a hipStream_t, NULL =
+ *                               default), asynchronously
+ *   nm_probe_event_elapsed_ms:  *ms = time from `start` to `stop`, both
+ *                               recorded and complete
+ * Errors: NM_ERR_ARG for a NULL pointer; NM_ERR_HIP if the runtime call fails
+ * (e.g. an event not yet complete). */
+nm_status nm_probe_event_create(void **event);
+nm_status nm_probe_event_destroy(void *event);
+nm_status nm_probe_event_record(void *event, void *stream);
+nm_status nm_probe_event_elapsed_ms(float *ms, void *start, void *stop);
+
 #ifdef __cplusplus
 }
 #endif

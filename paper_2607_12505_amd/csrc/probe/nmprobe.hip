@@ -165,3 +165,45 @@ extern "C" nm_status nm_probe_store_only(const nm_plan *plan, int m, int n, cons
     a.group_rows = 0;
     return launch_gemm(p.kind, p.tile, a, p.grid, stream) == 0 ? NM_OK : NM_ERR_HIP;
 }
+
+// Timing events without the system-scope fence a default event performs when
+// it completes (a write-back and invalidation of the caches): between two
+// GEMMs such a fence costs microseconds and leaves the next GEMM with cold
+// caches, which the GEMMs of a real sequence of layers do not see.
+extern "C" nm_status nm_probe_event_create(void **event) {
+    if (!event) return NM_ERR_ARG;
+    hipEvent_t e = nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) {
+        (void)hipGetLastError();
+        return NM_ERR_HIP;
+    }
+    *event = (void *)e;
+    return NM_OK;
+}
+
+extern "C" nm_status nm_probe_event_destroy(void *event) {
+    if (!event) return NM_ERR_ARG;
+    if (hipEventDestroy((hipEvent_t)event) != hipSuccess) {
+        (void)hipGetLastError();
+        return NM_ERR_HIP;
+    }
+    return NM_OK;
+}
+
+extern "C" nm_status nm_probe_event_record(void *event, void *stream) {
+    if (!event) return NM_ERR_ARG;
+    if (hipEventRecord((hipEvent_t)event, (hipStream_t)stream) != hipSuccess) {
+        (void)hipGetLastError();
+        return NM_ERR_HIP;
+    }
+    return NM_OK;
+}
+
+extern "C" nm_status nm_probe_event_elapsed_ms(float *ms, void *start, void *stop) {
+    if (!ms || !start || !stop) return NM_ERR_ARG;
+    if (hipEventElapsedTime(ms, (hipEvent_t)start, (hipEvent_t)stop) != hipSuccess) {
+        (void)hipGetLastError();
+        return NM_ERR_HIP;
+    }
+    return NM_OK;
+}

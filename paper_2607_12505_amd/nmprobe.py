@@ -17,7 +17,8 @@ from .nmspmm import _ptr, _stream, _torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libnmprobe.so")
 
 # Every symbol include/nmprobe.h declares (checked by the CPU tests).
-EXPORTED = ("nm_probe_mfma_rate", "nm_probe_mfma_layout", "nm_wall_clock_khz", "nm_probe_store_only")
+EXPORTED = ("nm_probe_mfma_rate", "nm_probe_mfma_layout", "nm_wall_clock_khz", "nm_probe_store_only",
+            "nm_probe_event_create", "nm_probe_event_destroy", "nm_probe_event_record", "nm_probe_event_elapsed_ms")
 NM_PROBE_WORDS = 4096
 
 _lib = None
@@ -42,6 +43,10 @@ def lib() -> ctypes.CDLL:
             "nm_wall_clock_khz": ([ctypes.POINTER(ctypes.c_int32)], i32),
             "nm_probe_mfma_layout": ([i32, vp, vp, vp, vp, vp], i32),
             "nm_probe_store_only": ([ctypes.POINTER(NmPlan), i32, i32, ctypes.POINTER(NmOutputs), vp], i32),
+            "nm_probe_event_create": ([ctypes.POINTER(vp)], i32),
+            "nm_probe_event_destroy": ([vp], i32),
+            "nm_probe_event_record": ([vp, vp], i32),
+            "nm_probe_event_elapsed_ms": ([ctypes.POINTER(ctypes.c_float), vp, vp], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -97,3 +102,26 @@ def probe_store_only(plan: NmPlan, m: int, n: int, Y=None, scale=None, Yh=None, 
 
 __all__ = ["EXPORTED", "NM_PROBE_WORDS", "NM_KIND_DENSE", "NM_KIND_SP42", "lib", "probe_mfma_rate",
            "wall_clock_khz", "probe_mfma_layout", "probe_store_only"]
+
+
+class TimingEvent:
+    """A fence-free timing event (nm_probe_event_*), with the record /
+    elapsed_time interface of torch.cuda.Event(enable_timing=True)."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        _check(lib().nm_probe_event_create(ctypes.byref(h)), "nm_probe_event_create")
+        self._h = h
+
+    def record(self, stream=None):
+        _check(lib().nm_probe_event_record(self._h, _stream(stream)), "nm_probe_event_record")
+
+    def elapsed_time(self, end: "TimingEvent") -> float:
+        ms = ctypes.c_float()
+        _check(lib().nm_probe_event_elapsed_ms(ctypes.byref(ms), self._h, end._h), "nm_probe_event_elapsed_ms")
+        return float(ms.value)
+
+    def __del__(self):
+        h, self._h = getattr(self, "_h", None), None
+        if h and _lib is not None:
+            _lib.nm_probe_event_destroy(h)

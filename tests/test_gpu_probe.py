@@ -82,3 +82,26 @@ def test_store_only_probe_writes_zeros_exactly_in_the_outputs(m, n):
                 Y.fill_(7)
                 Yh.fill_(7)
                 Yq.fill_(7)
+
+
+def test_fence_free_events_time_a_device_sleep_like_torch_events():
+    # The timing events of the bench (no system-scope fence) bracket the same
+    # work as PyTorch's default events: a device sleep of about 2 ms between
+    # them reads the same elapsed time within 5 %, and the interval of two
+    # events recorded back to back is short.
+    import torch
+    from paper_2607_12505_amd import nmprobe
+    a, b, c = nmprobe.TimingEvent(), nmprobe.TimingEvent(), nmprobe.TimingEvent()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    a.record()
+    torch.cuda._sleep(int(2.0e9 * 2e-3))
+    b.record()
+    t1.record()
+    c.record()
+    torch.cuda.synchronize()
+    mine, ref = a.elapsed_time(b), t0.elapsed_time(t1)
+    assert mine > 0.5 and ref > 0.5
+    assert abs(mine - ref) <= 0.05 * ref
+    assert 0 <= b.elapsed_time(c) < 0.2
