@@ -39,6 +39,20 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(probe, name), name
 
 
+def test_timing_event_calls_reject_null_pointers():
+    # argument checks come before any runtime call, so they hold without a GPU
+    import ctypes
+    probe = nmprobe.lib()
+    ms = ctypes.c_float()
+    h = ctypes.c_void_p(1)
+    assert probe.nm_probe_event_create(None) == nmspmm.NM_ERR_ARG
+    assert probe.nm_probe_event_destroy(None) == nmspmm.NM_ERR_ARG
+    assert probe.nm_probe_event_record(None, None) == nmspmm.NM_ERR_ARG
+    assert probe.nm_probe_event_elapsed_ms(None, h, h) == nmspmm.NM_ERR_ARG
+    assert probe.nm_probe_event_elapsed_ms(ctypes.byref(ms), None, h) == nmspmm.NM_ERR_ARG
+    assert probe.nm_probe_event_elapsed_ms(ctypes.byref(ms), h, None) == nmspmm.NM_ERR_ARG
+
+
 def test_method_library_carries_no_probe():
     # the measurement aids live in libnmprobe.so only
     import subprocess
